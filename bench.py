@@ -1,0 +1,229 @@
+#!/usr/bin/env python3
+"""Throughput of the Mirror-SD verification step on one MI355X.
+
+One step = the target's whole verification of one draft block (every row of
+the hot path): embedding, N decoder layers over the block against the KV
+cache, the early-exit top-kappa message after layer l_e, the final head,
+acceptance and the KV commit/rollback. Inputs are seeded and synthetic
+(random-init weights of the named shape, random cached K/V and draft
+tokens), resident in HBM before the timed region.
+
+Prints ONE JSON line: verified draft tokens/s (the metric), ms per step, the
+roofline of the dominant kernel (the FFN up-projection GEMM, timed with HIP
+events around each of its launches in a second, instrumented pass over the
+same number of steps) and the fp64 oracle's throughput on the host cores
+over a bounded sample of the same step.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+METRIC = "verified tokens/sec per verify step + % HBM roofline, 14B-shaped γ=8"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="14b_chain")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile-pass", action="store_true",
+                    help="skip the instrumented pass (rocprofv3 runs)")
+    ap.add_argument("--cpu-layers", type=int, default=2,
+                    help="decoder layers the oracle times for the CPU baseline sample")
+    return ap.parse_args()
+
+
+def step_bytes(shape, w, ctx_mean: float) -> dict:
+    """Algorithmic HBM bytes of one step: every weight once, the LM head twice
+    (early exit + final), cached K/V read once, block K/V written, logits out."""
+    from paper_2510_13161_amd import synth
+    specs = synth.tensor_specs(shape)
+    layer_w = sum(2 * int(__import__("numpy").prod(s.shape)) for s in specs if s.name.startswith("l"))
+    head = 2 * shape.vocab * shape.d_model
+    M = w.rows
+    kv_read = shape.n_layers * 2 * shape.n_kv_heads * shape.head_dim * 2 * (ctx_mean + w.n_slots) * w.batch
+    kv_write = shape.n_layers * 2 * shape.n_kv_heads * shape.head_dim * 2 * M
+    logits = M * shape.vocab * 4
+    return {"weights": layer_w, "heads": 2 * head, "kv": kv_read + kv_write, "logits": logits,
+            "total": layer_w + 2 * head + kv_read + kv_write + logits}
+
+
+def ffn_up_bytes(shape, M: int) -> int:
+    """Algorithmic bytes of one FFN up-projection launch: its weights (gate and
+    up for SwiGLU) once, the normed rows in, the activation rows out."""
+    n_mats = 2 if shape.act == "swiglu" else 1
+    return n_mats * shape.d_ffn * shape.d_model * 2 + M * shape.d_model * 2 + M * shape.d_ffn * 2
+
+
+def cpu_baseline(shape, w, layers: int) -> dict:
+    """The fp64 oracle on the host: embed + `layers` decoder layers + both heads
+    of sequence 0, scaled to the full depth (the layers are identical in cost)."""
+    import numpy as np
+    import oracle as orc
+    from paper_2510_13161_amd import synth
+    if not os.path.exists(orc.LIB_PATH):
+        orc.build()
+    si = synth.step_inputs(w)
+    L = int(si.ctx_len[0])
+    sub = shape.with_layers(layers)
+    weights = synth.host_weights(sub, w.seed)
+    o = orc.Oracle(sub, weights)
+    ctx = [(synth.host_ctx(shape, w.seed, l, "k", 0, L), synth.host_ctx(shape, w.seed, l, "v", 0, L))
+           for l in range(layers)]
+    pos = L + orc.depths(si.parent)
+    t0 = time.perf_counter()
+    x = o.embed(si.tokens[0], pos)
+    t1 = time.perf_counter()
+    for l in range(layers):
+        o.layer(l, x, pos, si.parent, ctx[l][0], ctx[l][1], L)
+    t2 = time.perf_counter()
+    z = o.head(x)
+    ids, logp, _ = orc.Oracle.topk(z, w.kappa)
+    t3 = time.perf_counter()
+    o.accept(si.parent, si.tokens[0], z)
+    t4 = time.perf_counter()
+    t_step = (t1 - t0) + (t2 - t1) * shape.n_layers / layers + 2 * (t3 - t2) + (t4 - t3)
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    per_seq_tokens = w.n_slots - 1
+    return {"value": per_seq_tokens / t_step, "unit": "verified tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": (f"sequence 0 of workload {w.name}: embed + {layers} of {shape.n_layers} "
+                       f"decoder layers + one head pass (timed {t4 - t0:.2f} s), layer time x "
+                       f"{shape.n_layers}/{layers}, head x2; fp64 C oracle, OpenMP"),
+            "s_per_step": t_step}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the multi-GPU sharding is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from paper_2510_13161_amd import msd, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    w = synth.WORKLOADS[args.workload]
+    shape = w.model
+    si = synth.step_inputs(w)
+    dev = "cuda"
+    total_steps = args.warmup + args.steps * (1 if args.no_profile_pass else 2)
+    capacity = int(-(-(int(si.ctx_len.max()) + w.n_slots + total_steps + 8) // 64) * 64)
+
+    t0 = time.perf_counter()
+    weights = synth.device_weights(shape, w.seed, dev)
+    maxpos = capacity if shape.pos == "rope" else shape.max_positions
+    model = msd.Model(shape, weights, max_positions=maxpos)
+    cache = msd.Cache(shape, w.batch, capacity, dev)
+    len0 = torch.from_numpy(si.ctx_len).to(dev)
+    cache.len.copy_(len0)
+    synth.device_fill_ctx(shape, w.seed, cache.k, cache.v, cache.len)
+    torch.cuda.synchronize()
+    t_setup = time.perf_counter() - t0
+
+    B, n = w.batch, w.n_slots
+    M = B * n
+    tokens = torch.from_numpy(si.tokens).to(dev)
+    blk = msd.make_block(tokens, None if w.topology == "chain" else si.parent)
+    logits = torch.empty((M, shape.vocab), dtype=torch.float32, device=dev)
+    argmax = torch.empty(M, dtype=torch.int32, device=dev)
+    lse = torch.empty(M, dtype=torch.float32, device=dev)
+    ids = torch.empty((M, w.kappa), dtype=torch.int32, device=dev)
+    logp = torch.empty((M, w.kappa), dtype=torch.float32, device=dev)
+    ee = msd.EERequest(w.ee_layer, w.kappa, ids.data_ptr(), logp.data_ptr(), None)
+    ws = torch.empty(msd.workspace_bytes(model.handle, B, n, w.kappa, capacity), dtype=torch.uint8,
+                     device=dev)
+    acc = torch.empty(B, dtype=torch.int32, device=dev)
+    nxt = torch.empty(B, dtype=torch.int32, device=dev)
+    path = torch.empty((B, n), dtype=torch.int32, device=dev)
+    smp = None
+    keep = []
+    if w.mode != "greedy":
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        keep = [t(si.cand_ids), t(si.cand_q), t(si.u_accept), t(si.u_sample)]
+        smp = msd.Sampling(msd.MODES[w.mode], float(w.temperature), si.cand_ids.shape[-1],
+                           *[k.data_ptr() for k in keep])
+
+    def step():
+        msd.verify_block(model.handle, cache.c, blk, ee, logits, argmax, lse, ws)
+        msd.accept(model.handle, blk, logits, argmax, smp, acc, nxt, path, cache.status)
+        msd.kv_commit(model.handle, cache.c, blk, acc, path)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    status = int(cache.status.item())
+    if status != 0:
+        print(f"bench.py: device status {status}", file=sys.stderr)
+        sys.exit(1)
+
+    # second pass: HIP events around each FFN up-projection launch
+    roof = None
+    if not args.no_profile_pass:
+        evb = [torch.cuda.Event(enable_timing=True) for _ in range(shape.n_layers)]
+        eve = [torch.cuda.Event(enable_timing=True) for _ in range(shape.n_layers)]
+        for e in evb + eve:
+            e.record()
+        torch.cuda.synchronize()
+        msd.set_profile(model.handle, msd.MSD_K_FFN_UP, [e.cuda_event for e in evb],
+                        [e.cuda_event for e in eve])
+        dur = []
+        for _ in range(args.steps):
+            step()
+            torch.cuda.synchronize()
+            dur += [b.elapsed_time(e) for b, e in zip(evb, eve)]
+        msd.set_profile(model.handle, msd.MSD_K_FFN_UP, [], [])
+        avg_ms = float(np.mean(dur))
+        per_launch = ffn_up_bytes(shape, M)
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "gemm_kernel<EPI_SWIGLU> (FFN gate+up projection)",
+                "bytes_per_launch": per_launch, "avg_launch_us": round(avg_ms * 1e3, 2),
+                "launches": len(dur)}
+
+    ctx_mean = float(si.ctx_len.mean()) + (args.warmup + args.steps)  # len grows by 1 per step
+    sb = step_bytes(shape, w, ctx_mean)
+    step_gbs = sb["total"] / (ms * 1e-3) / 1e9
+    value = w.draft_tokens / (ms * 1e-3)
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "verified tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights, random cached K/V and draft tokens)",
+        "config": {"workload": w.name, "model": shape.name, "n_layers": shape.n_layers,
+                   "d_model": shape.d_model, "batch": w.batch, "n_slots": n,
+                   "topology": w.topology, "ctx": list(w.ctx), "ee_layer": w.ee_layer,
+                   "kappa": w.kappa, "acceptance": w.mode},
+        "step_bytes": sb["total"], "step_hbm_gbs": round(step_gbs, 1),
+        "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
+        "roofline": roof,
+        "setup_s": round(t_setup, 2),
+    }
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline(shape, w, args.cpu_layers)
+        cb.pop("s_per_step")
+        out["cpu_baseline"] = cb
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

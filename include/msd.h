@@ -1,0 +1,263 @@
+/*
+ * msd.h — C ABI of the Mirror-SD verification step on MI355X (gfx950).
+ *
+ * Mirror Speculative Decoding (arXiv 2510.13161) overlaps a draft model with
+ * the target's verification pass. This library is the target side of one
+ * decoding step, on one GPU:
+ *
+ *   msd_verify_block     Sec. 2 (speculative verification: one teacher-forced
+ *                        pass of the target over the draft window) and
+ *                        Sec. 3.1 (the window may be the branch-complete
+ *                        hypothesis tree; a depth-r node holds the token at
+ *                        position t + r). Emits the early-exit message on the
+ *                        way (Sec. 3.1: p^(l_e) = Softmax(W_LM h^(l_e)),
+ *                        M_t = Top-kappa(p^(l_e)) = {(v_i, log p_i)}).
+ *   msd_early_exit_topk  the Sec. 3.1 token channel on its own, from a residual.
+ *   msd_accept           App. B acceptance operator: the longest verified
+ *                        prefix A_t, the accepted path and the next token
+ *                        (Sec. 2 greedy rule; stochastic rules, see below).
+ *   msd_kv_commit        Sec. 2: commit the accepted tokens (and the root) to
+ *                        the KV cache; everything else rolls back.
+ *
+ * Conventions
+ *  - Every pointer marked "device" is HIP device memory owned by the caller;
+ *    "host" pointers are read during the call only. The library never takes
+ *    ownership of caller memory; it allocates device memory only in
+ *    msd_model_create (a small rotary table) and never per call.
+ *  - All work is enqueued asynchronously on the caller's `stream`; nothing
+ *    blocks, nothing throws across the ABI. Calls are graph-capturable.
+ *  - Host-checkable errors (NULL pointers, sizes out of range, topology that
+ *    is not a forest in slot order, workspace too small) return a negative
+ *    msd_status and enqueue nothing; msd_last_error() then describes it.
+ *  - Device-detected errors (a committed length plus the block exceeding the
+ *    cache capacity; a draft token outside its parent's candidate set) set a
+ *    non-zero code in the caller's device status word and the affected
+ *    sequence's outputs are left unspecified.
+ *  - Row-major everywhere. bf16 = IEEE binary16-brain, stored as 16 bits.
+ */
+#ifndef MSD_H
+#define MSD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MSD_OK = 0,
+  MSD_ERR_INVALID_ARG = -1, /* NULL pointer or out-of-range scalar             */
+  MSD_ERR_SHAPE = -2,       /* shapes the kernels do not support               */
+  MSD_ERR_CAPACITY = -3,    /* block does not fit the cache (host-detectable)  */
+  MSD_ERR_UNSUPPORTED = -4, /* mode / option not available                     */
+  MSD_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than required         */
+  MSD_ERR_HIP = -6          /* a HIP runtime call failed                       */
+} msd_status;
+
+/* Device status word codes (OR-ed in by kernels). */
+#define MSD_DEV_CAPACITY 1u  /* len[b] + n_slots > capacity                    */
+#define MSD_DEV_CANDIDATE 2u /* REJECTION: child token without draft mass      */
+#define MSD_DEV_TOKEN 4u     /* a block token outside [0, vocab)               */
+
+/* Thread-local text of the last non-OK status returned on this thread. */
+const char* msd_last_error(void);
+
+enum { MSD_NORM_RMS = 0, MSD_NORM_LAYER = 1 };
+enum { MSD_ACT_SWIGLU = 0, MSD_ACT_RELU = 1 };
+enum { MSD_POS_ROPE = 0, MSD_POS_LEARNED = 1 };
+
+/*
+ * Decoder-only target (Sec. 2: p(y_t | .) = Softmax(W h_t)): n_layers pre-norm
+ * blocks (attention, then FFN), a final norm and the LM head.
+ *  norm          RMSNorm (x / sqrt(mean x^2 + eps) * g) or LayerNorm.
+ *  act           SwiGLU (down(silu(gate h) * up h)) or ReLU (down(relu(up h + b)) + b).
+ *  pos           rotary (rotate-half pairs (j, j + head_dim/2), angle
+ *                pos * rope_theta^(-2j/head_dim)) or a learned table added to
+ *                the embedding.
+ *  max_positions largest position + 1 the model will see (rotary table size /
+ *                learned table rows).
+ * Limits: head_dim in {64, 128}; n_heads % n_kv_heads == 0; d_model,
+ * n_heads*head_dim and d_ffn multiples of 64; vocab >= 64 and a multiple of 16.
+ */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
+  int32_t norm, act, pos, has_bias, tied_head;
+  int32_t max_positions;
+  float rope_theta, norm_eps;
+} msd_model_config;
+
+/* Tensor slots. All tensors are device bf16, row-major [out][in] for
+ * matrices. Absent tensors (biases without has_bias, LayerNorm shifts with
+ * RMSNorm, the learned table with rotary positions, the gate with ReLU, the
+ * separate head when tied) are NULL. */
+enum {
+  MSD_T_EMBED = 0,     /* [vocab][d_model]                              */
+  MSD_T_POS_EMBED,     /* [max_positions][d_model]   (learned only)     */
+  MSD_T_FINAL_G,       /* [d_model]                                     */
+  MSD_T_FINAL_B,       /* [d_model]                  (LayerNorm only)   */
+  MSD_T_LM_HEAD,       /* [vocab][d_model]           (NULL when tied)   */
+  MSD_T_GLOBAL_COUNT
+};
+enum {
+  MSD_L_ATTN_G = 0, MSD_L_ATTN_B,
+  MSD_L_WQ,          /* [n_heads*head_dim][d_model]     */
+  MSD_L_WK,          /* [n_kv_heads*head_dim][d_model]  */
+  MSD_L_WV,          /* [n_kv_heads*head_dim][d_model]  */
+  MSD_L_BQ, MSD_L_BK, MSD_L_BV,
+  MSD_L_WO,          /* [d_model][n_heads*head_dim]     */
+  MSD_L_BO,
+  MSD_L_MLP_G, MSD_L_MLP_B,
+  MSD_L_W_GATE,      /* [d_ffn][d_model]  (SwiGLU)      */
+  MSD_L_W_UP,        /* [d_ffn][d_model]                */
+  MSD_L_B_UP,        /* [d_ffn]           (ReLU)        */
+  MSD_L_W_DOWN,      /* [d_model][d_ffn]                */
+  MSD_L_B_DOWN,      /* [d_model]         (ReLU)        */
+  MSD_L_COUNT
+};
+#define MSD_TENSOR_INDEX(layer, slot) (MSD_T_GLOBAL_COUNT + (layer) * MSD_L_COUNT + (slot))
+#define MSD_N_TENSORS(n_layers) (MSD_T_GLOBAL_COUNT + (n_layers) * MSD_L_COUNT)
+
+typedef struct msd_model msd_model;
+
+/* Validates the configuration and tensor table (n_tensors must equal
+ * MSD_N_TENSORS(n_layers)) and builds the model on the current HIP device.
+ * The tensors stay caller-owned and must outlive the model.
+ * Weight layout: the call rearranges every projection matrix (q, k, v, o,
+ * gate, up, down and the LM head; the embedding too when tied) IN PLACE into
+ * the library's fragment-major layout (16-row groups stored as consecutive
+ * 1 KB MFMA operands along K), so the verify pass reads HBM sequentially.
+ * After the call those tensors are opaque to the caller, and one set of
+ * tensors can back only one model. The call synchronises the device and
+ * briefly allocates a temporary buffer the size of the largest matrix. */
+msd_status msd_model_create(const msd_model_config* cfg, const void* const* tensors,
+                            int32_t n_tensors, msd_model** out);
+void msd_model_destroy(msd_model* model);
+
+/* KV cache, device bf16 [n_layers][batch_cap][n_kv_heads][capacity][head_dim]
+ * for k and v; len[b] (device int32) = committed positions of sequence b.
+ * The block's rows go to positions len[b] + slot. */
+typedef struct {
+  void* k;
+  void* v;
+  int32_t* len;       /* device [batch_cap]                                  */
+  uint32_t* status;   /* device word; kernels OR MSD_DEV_* codes into it     */
+  int32_t batch_cap, capacity;
+} msd_kv_cache;
+
+/* Draft block shared by every sequence of the batch.
+ * Slot 0 is the root: the last committed token, not yet in the cache, at
+ * position len[b]; slot i sits at position len[b] + depth(i).
+ * parent == NULL means a chain (parent[i] = i - 1); otherwise parent[0] = -1
+ * and 0 <= parent[i] < i. */
+typedef struct {
+  int32_t batch, n_slots;   /* 1 <= n_slots <= 64, batch <= batch_cap      */
+  const int32_t* tokens;    /* device [batch][n_slots]                     */
+  const int32_t* parent;    /* host [n_slots] or NULL                      */
+} msd_block;
+
+/* Early-exit request: after layer `layer` (1-indexed, 1 <= layer <= n_layers-1)
+ * write, for every block row, the kappa (1..32) most likely tokens under the
+ * final-normed LM head (ties: smaller id first) and their log-probabilities
+ * (log-softmax over the full vocabulary). If `ready` is non-NULL it is
+ * recorded on the stream once ids/logp are complete. */
+typedef struct {
+  int32_t layer;
+  int32_t kappa;
+  int32_t* ids;       /* device [batch*n_slots][kappa] */
+  float* logp;        /* device [batch*n_slots][kappa] */
+  hipEvent_t ready;
+} msd_ee_request;
+
+/* Workspace needed by msd_verify_block / msd_early_exit_topk / msd_accept
+ * for this batch, block size, kappa and cache capacity. */
+size_t msd_workspace_bytes(const msd_model* model, int32_t batch, int32_t n_slots,
+                           int32_t kappa, int32_t capacity);
+
+/*
+ * Verification pass of the target over the block (Sec. 2; Sec. 3.1 tree).
+ * Writes the block's K/V into the cache after len[b] (len is not changed:
+ * only msd_kv_commit advances it). Outputs, rows m = b*n_slots + slot:
+ *  logits  device fp32 [M][vocab] final-layer logits, or NULL
+ *  argmax  device int32 [M] (ties: smaller id), required
+ *  lse     device fp32 [M] logsumexp of the logits, or NULL
+ *  ee      early-exit request, or NULL
+ * ws must hold msd_workspace_bytes(model, batch, n_slots, kappa, capacity).
+ */
+msd_status msd_verify_block(const msd_model* model, msd_kv_cache* kv, const msd_block* block,
+                            const msd_ee_request* ee, float* logits, int32_t* argmax,
+                            float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Token channel of Sec. 3.1 from a residual: hidden is device fp32 [M][d_model]
+ * (the residual stream after some layer); applies the final norm and the LM
+ * head and writes the kappa best ids and log-probabilities per row.
+ */
+msd_status msd_early_exit_topk(const msd_model* model, const float* hidden, int32_t M,
+                               int32_t kappa, int32_t* ids, float* logp, void* ws,
+                               size_t ws_bytes, hipStream_t stream);
+
+enum { MSD_GREEDY = 0, MSD_REJECTION = 1, MSD_MATCH = 2 };
+
+/*
+ * Sampling inputs of the stochastic rules (unused by MSD_GREEDY).
+ * REJECTION: at a node whose children were drawn from the sparse draft law
+ * q (cand_ids/cand_q at that node) without replacement, child x is accepted
+ * iff u_accept[child] < min(1, r(x)/q(x)); after a rejection
+ * r <- normalise((r - q)^+) and x leaves q; if every child is rejected the
+ * next token is drawn from r with u_sample[node] (inverse CDF over ids
+ * ascending); r starts as p = Softmax(logits / temperature). With a single
+ * child this is Leviathan et al. 2023; it leaves the target law intact.
+ * MATCH: the paper's sample-and-compare (Sec. 3.1, App. B): y is drawn from p
+ * with u_sample[node]; descend to the child carrying y, else y is next.
+ */
+typedef struct {
+  int32_t mode;
+  float temperature;
+  int32_t n_cand;           /* <= 64                                       */
+  const int32_t* cand_ids;  /* device [batch][n_slots][n_cand]             */
+  const float* cand_q;      /* device [batch][n_slots][n_cand], rows sum 1 */
+  const float* u_accept;    /* device [batch][n_slots] in [0, 1)           */
+  const float* u_sample;    /* device [batch][n_slots] in [0, 1)           */
+} msd_sampling;
+
+/*
+ * App. B acceptance operator over the verified block, per sequence:
+ *  acc_len  device int32 [batch]  A_b = accepted draft tokens (depth reached)
+ *  next_tok device int32 [batch]  correction (mismatch) or bonus token
+ *  path     device int32 [batch][n_slots]; path[b][r] = slot accepted at depth r,
+ *           path[b][0] = 0; entries after A_b are -1
+ * GREEDY reads argmax only (children tried in slot order); the stochastic
+ * modes read logits (fp32 [M][vocab]). sampling may be NULL for GREEDY.
+ * status: device word for MSD_DEV_CANDIDATE, may be NULL.
+ */
+msd_status msd_accept(const msd_model* model, const msd_block* block, const float* logits,
+                      const int32_t* argmax, const msd_sampling* sampling, int32_t* acc_len,
+                      int32_t* next_tok, int32_t* path, uint32_t* status, void* ws,
+                      size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Commit / rollback (Sec. 2): for every layer, row len[b] + path[b][r] of
+ * the cache moves to len[b] + r for r = 1..A_b, then len[b] += 1 + A_b (the
+ * root and the accepted tokens). Rows past the new length are stale.
+ */
+msd_status msd_kv_commit(const msd_model* model, msd_kv_cache* kv, const msd_block* block,
+                         const int32_t* acc_len, const int32_t* path, hipStream_t stream);
+
+/*
+ * Instrumentation (benchmarking only): when set, msd_verify_block records
+ * begin[i] / end[i] on its stream around the launch of kernel class `kclass`
+ * in layer i (i < n; classes: 0 QKV projection, 1 attention, 2 output
+ * projection, 3 FFN up projection, 4 FFN down projection). The events are
+ * caller-owned HIP events; pass n = 0 to switch it off. Not thread-safe
+ * with concurrent verify calls on the same model.
+ */
+enum { MSD_K_QKV = 0, MSD_K_ATTN = 1, MSD_K_OPROJ = 2, MSD_K_FFN_UP = 3, MSD_K_FFN_DOWN = 4 };
+msd_status msd_set_profile(msd_model* model, int32_t kclass, hipEvent_t* begin, hipEvent_t* end,
+                           int32_t n);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MSD_H */

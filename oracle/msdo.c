@@ -43,7 +43,7 @@ static inline double bf(uint16_t b) {
 }
 
 static void* xmalloc(size_t n) {
-  void* p = malloc(n ? n : 1);
+  void* p = calloc(n ? n : 1, 1);
   if (!p) abort();
   return p;
 }

@@ -1,0 +1,203 @@
+// Device-side helpers shared by the verification kernels (gfx950, wave64).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace msd {
+
+constexpr int kWave = 64;
+constexpr int kMaxSlots = 64;
+constexpr int kMaxKappa = 32;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Block topology, passed by value to kernels (no device upload needed).
+// anc[i] bit a = slot a is an ancestor of slot i or i itself.
+struct Topo {
+  uint64_t anc[kMaxSlots];
+  int32_t depth[kMaxSlots];
+  int32_t parent[kMaxSlots];
+  int32_t n_slots;
+  int32_t max_depth;
+};
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Eight fp32 values as bf16 hi + lo parts (x ~= hi + lo to ~16 bits).
+__device__ __forceinline__ void split_vals(const float (&v)[8], bf16x8& hi, bf16x8& lo) {
+  u32x4 h, l;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    h[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
+    l[i] = pack_bf16x2(v[2 * i] - bf_lo(h[i]), v[2 * i + 1] - bf_hi(h[i]));
+  }
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+__device__ __forceinline__ bf16x8 round_vals(const float (&v)[8]) {
+  u32x4 h;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) h[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
+  return __builtin_bit_cast(bf16x8, h);
+}
+
+// LDS-only workgroup barrier: waits for this wave's LDS traffic, not for its
+// outstanding global loads (a full __syncthreads would drain those too).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0), vmcnt/expcnt left open
+  __builtin_amdgcn_s_barrier();
+}
+
+// 16-byte loads. Weights are streamed once per pass: non-temporal.
+__device__ __forceinline__ bf16x8 load_nt(const uint16_t* p) {
+  u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return __builtin_bit_cast(bf16x8, v);
+}
+__device__ __forceinline__ bf16x8 load16(const uint16_t* p) {
+  u32x4 v = *reinterpret_cast<const u32x4*>(p);
+  return __builtin_bit_cast(bf16x8, v);
+}
+__device__ __forceinline__ bf16x8 zero_bf16x8() {
+  u32x4 z = {0u, 0u, 0u, 0u};
+  return __builtin_bit_cast(bf16x8, z);
+}
+
+// Eight consecutive fp32 values split into bf16 hi + lo parts (x ~= hi + lo to
+// about 16 significant bits): activations stay fp32 and enter the MFMA as two
+// bf16 operands against the exact bf16 weights.
+__device__ __forceinline__ void load_split8(const float* p, bf16x8& hi, bf16x8& lo) {
+  const u32x4 a = *reinterpret_cast<const u32x4*>(p);
+  const u32x4 b = *reinterpret_cast<const u32x4*>(p + 4);
+  const float v[8] = {__uint_as_float(a[0]), __uint_as_float(a[1]), __uint_as_float(a[2]),
+                      __uint_as_float(a[3]), __uint_as_float(b[0]), __uint_as_float(b[1]),
+                      __uint_as_float(b[2]), __uint_as_float(b[3])};
+  u32x4 h, l;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint16_t h0 = f2bf(v[2 * i]), h1 = f2bf(v[2 * i + 1]);
+    const uint16_t l0 = f2bf(v[2 * i] - bf2f(h0)), l1 = f2bf(v[2 * i + 1] - bf2f(h1));
+    h[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    l[i] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+  }
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+// Same split for a pre-normalised operand: v = (x - mu) * s * g (+ b).
+__device__ __forceinline__ void load_norm_split8(const float* x, const uint16_t* g,
+                                                 const uint16_t* bsh, float mu, float s,
+                                                 bool split, bf16x8& hi, bf16x8& lo) {
+  const u32x4 a = *reinterpret_cast<const u32x4*>(x);
+  const u32x4 b = *reinterpret_cast<const u32x4*>(x + 4);
+  const u32x4 gw = *reinterpret_cast<const u32x4*>(g);
+  u32x4 bw = {0u, 0u, 0u, 0u};
+  if (bsh) bw = *reinterpret_cast<const u32x4*>(bsh);
+  const float xv[8] = {__uint_as_float(a[0]), __uint_as_float(a[1]), __uint_as_float(a[2]),
+                       __uint_as_float(a[3]), __uint_as_float(b[0]), __uint_as_float(b[1]),
+                       __uint_as_float(b[2]), __uint_as_float(b[3])};
+  u32x4 h, l;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float g0 = __uint_as_float(gw[i] << 16), g1 = __uint_as_float(gw[i] & 0xFFFF0000u);
+    const float b0 = __uint_as_float(bw[i] << 16), b1 = __uint_as_float(bw[i] & 0xFFFF0000u);
+    const float v0 = (xv[2 * i] - mu) * s * g0 + b0;
+    const float v1 = (xv[2 * i + 1] - mu) * s * g1 + b1;
+    const uint16_t h0 = f2bf(v0), h1 = f2bf(v1);
+    h[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    l[i] = split ? pack_bf16x2(v0 - bf2f(h0), v1 - bf2f(h1)) : 0u;
+  }
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
+__device__ __forceinline__ bf16x8 load_round8(const float* p) {
+  const u32x4 a = *reinterpret_cast<const u32x4*>(p);
+  const u32x4 b = *reinterpret_cast<const u32x4*>(p + 4);
+  u32x4 h;
+  h[0] = pack_bf16x2(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  h[1] = pack_bf16x2(__uint_as_float(a[2]), __uint_as_float(a[3]));
+  h[2] = pack_bf16x2(__uint_as_float(b[0]), __uint_as_float(b[1]));
+  h[3] = pack_bf16x2(__uint_as_float(b[2]), __uint_as_float(b[3]));
+  return __builtin_bit_cast(bf16x8, h);
+}
+
+// D = A * B + C on a 16x16 tile, K = 32, bf16 inputs, fp32 accumulate.
+// Lane l: A row l%16, k 8*(l/16)..+8; B column l%16, same k;
+// D rows 4*(l/16)+r (r = 0..3), column l%16.
+__device__ __forceinline__ floatx4 mfma16x16x32(bf16x8 a, bf16x8 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Order-preserving map of fp32 onto uint32 (larger float -> larger key).
+__device__ __forceinline__ uint32_t ordered_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float from_ordered_bits(uint32_t k) {
+  uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+  return __uint_as_float(u);
+}
+// Ranking key: larger logit first, then smaller id. 0 = no candidate.
+__device__ __forceinline__ uint64_t rank_key(float v, int32_t id) {
+  return ((uint64_t)ordered_bits(v) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)id);
+}
+__device__ __forceinline__ int32_t key_id(uint64_t k) {
+  return (int32_t)(0xFFFFFFFFu - (uint32_t)(k & 0xFFFFFFFFull));
+}
+__device__ __forceinline__ float key_val(uint64_t k) { return from_ordered_bits((uint32_t)(k >> 32)); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint64_t w = __shfl_xor(v, o);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
+// Cross-workgroup hand-off inside one kernel (split-K partials, attention
+// chunks). The payload is written and read with agent-scope atomic accesses,
+// which the gfx950 memory model implements as L2-coherent (sc1) stores and
+// loads; the writer drains its stores (s_waitcnt) before bumping the counter.
+// No whole-L2 writeback or invalidate is needed, unlike a device-scope fence.
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_coherent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void drain_stores() { __builtin_amdgcn_s_waitcnt(0); }
+__device__ __forceinline__ int counter_add(int32_t* c, int v) {
+  return __hip_atomic_fetch_add(c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void counter_reset(int32_t* c) {
+  __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+}  // namespace msd

@@ -1,0 +1,660 @@
+// C ABI of the verification step (include/msd.h): argument checks, block
+// topology preparation, workspace layout and the launch sequence. Every call
+// is asynchronous on the caller's stream and allocates nothing.
+#include <stdlib.h>
+
+#include <algorithm>
+#include <cmath>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "msd.h"
+
+using namespace msd;
+
+struct msd_model {
+  msd_model_config cfg;
+  std::vector<const uint16_t*> t;  // MSD_N_TENSORS(n_layers) entries
+  float2* rope = nullptr;          // [max_positions][head_dim/2] (cos, sin)
+  int32_t target_wgs = 512;        // split-K sizing target
+  int32_t weights_nt = 0;          // non-temporal weight loads
+  int32_t prof_class = -1;         // instrumentation (msd_set_profile)
+  std::vector<hipEvent_t> prof_begin, prof_end;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+msd_status fail(msd_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define MSD_HIP(call)                                                                    \
+  do {                                                                                   \
+    hipError_t e_ = (call);                                                              \
+    if (e_ != hipSuccess) return fail(MSD_ERR_HIP, std::string(#call) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+inline const uint16_t* T(const msd_model* m, int idx) { return m->t[idx]; }
+inline const uint16_t* LT(const msd_model* m, int l, int slot) {
+  return m->t[MSD_TENSOR_INDEX(l, slot)];
+}
+inline const uint16_t* head_w(const msd_model* m) {
+  return m->cfg.tied_head ? T(m, MSD_T_EMBED) : T(m, MSD_T_LM_HEAD);
+}
+
+inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// split-K factor: enough workgroups to keep HBM busy, >= 4 k-steps per wave
+int splits_for(const msd_model* m, int n_tiles, int K) {
+  const int ks = K / 32;
+  int max_s = ks / 16;
+  if (max_s < 1) max_s = 1;
+  int want = (m->target_wgs + n_tiles - 1) / n_tiles;
+  if (want < 1) want = 1;
+  return want < max_s ? want : max_s;
+}
+
+struct GemmShape {
+  int n_tiles, K, splits;
+};
+
+struct Shapes {
+  GemmShape qkv, o, up, down, head;
+};
+
+Shapes shapes(const msd_model* m) {
+  const msd_model_config& c = m->cfg;
+  Shapes s;
+  s.qkv.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim / kTileN;
+  s.qkv.K = c.d_model;
+  s.o.n_tiles = c.d_model / kTileN;
+  s.o.K = c.n_heads * c.head_dim;
+  s.up.n_tiles = c.act == MSD_ACT_SWIGLU ? c.d_ffn / 32 : c.d_ffn / kTileN;
+  s.up.K = c.d_model;
+  s.down.n_tiles = c.d_model / kTileN;
+  s.down.K = c.d_ffn;
+  s.head.n_tiles = (c.vocab + kTileN - 1) / kTileN;
+  s.head.K = c.d_model;
+  for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head})
+    g->splits = splits_for(m, g->n_tiles, g->K);
+  return s;
+}
+
+struct Layout {
+  size_t x, stats, q, attn, act, partial, counters, part_o, part_ml, tile_ms, tile_top, total;
+  int64_t n_counters;
+  int32_t attn_counter_off;  // in int32 units inside counters
+  int32_t max_chunks;
+};
+
+Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacity) {
+  const msd_model_config& c = m->cfg;
+  const Shapes s = shapes(m);
+  const size_t M = (size_t)batch * n_slots;
+  const int kmax = kappa > 1 ? kappa : 1;
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  L.x = take(M * c.d_model * sizeof(float));
+  L.stats = take((size_t)(c.d_model / kTileN) * M * sizeof(float2));
+  L.q = take(M * c.n_heads * c.head_dim * sizeof(float));
+  L.attn = take(M * c.n_heads * c.head_dim * sizeof(float));
+  L.act = take(M * c.d_ffn * sizeof(float));
+  size_t part = 0;
+  int max_tiles = 0;
+  for (const GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
+    if (g->splits > 1) {
+      const size_t p = (size_t)g->splits * M * g->n_tiles * kTileN * sizeof(float);
+      part = p > part ? p : part;
+      max_tiles = g->n_tiles > max_tiles ? g->n_tiles : max_tiles;
+    }
+  }
+  L.partial = take(part);
+  L.attn_counter_off = max_tiles;
+  L.n_counters = (int64_t)max_tiles + (int64_t)batch * c.n_kv_heads;
+  L.counters = take((size_t)L.n_counters * sizeof(int32_t));
+  L.max_chunks = (capacity + kAttnChunk - 1) / kAttnChunk;
+  const size_t qn = (size_t)(c.n_heads / c.n_kv_heads) * n_slots;
+  const size_t nparts = (size_t)batch * c.n_kv_heads * L.max_chunks * qn;
+  L.part_o = take(nparts * c.head_dim * sizeof(float));
+  L.part_ml = take(nparts * sizeof(float2));
+  L.tile_ms = take((size_t)s.head.n_tiles * M * sizeof(float2));
+  L.tile_top = take((size_t)s.head.n_tiles * M * kmax * sizeof(uint64_t));
+  L.total = off;
+  return L;
+}
+
+msd_status make_topo(const msd_block* blk, Topo* topo) {
+  const int n = blk->n_slots;
+  topo->n_slots = n;
+  topo->max_depth = 0;
+  for (int i = 0; i < kMaxSlots; ++i) {
+    topo->anc[i] = 0;
+    topo->depth[i] = 0;
+    topo->parent[i] = -1;
+  }
+  for (int i = 0; i < n; ++i) {
+    const int p = blk->parent ? blk->parent[i] : i - 1;
+    if (i == 0 && p != -1) return fail(MSD_ERR_SHAPE, "parent[0] must be -1");
+    if (i > 0 && (p < 0 || p >= i)) return fail(MSD_ERR_SHAPE, "parent[i] must lie in [0, i)");
+    topo->parent[i] = p;
+    topo->depth[i] = i == 0 ? 0 : topo->depth[p] + 1;
+    topo->anc[i] = (i == 0 ? 0ull : topo->anc[p]) | (1ull << i);
+    if (topo->depth[i] > topo->max_depth) topo->max_depth = topo->depth[i];
+  }
+  return MSD_OK;
+}
+
+msd_status check_block(const msd_model* m, const msd_block* blk) {
+  if (!m || !blk) return fail(MSD_ERR_INVALID_ARG, "null model or block");
+  if (blk->n_slots < 1 || blk->n_slots > kMaxSlots)
+    return fail(MSD_ERR_SHAPE, "n_slots must lie in [1, 64]");
+  if (blk->batch < 1) return fail(MSD_ERR_SHAPE, "batch must be >= 1");
+  if ((size_t)blk->batch * blk->n_slots > (size_t)kMaxMT * 16)
+    return fail(MSD_ERR_SHAPE, "batch * n_slots must be <= 144");
+  if (!blk->tokens) return fail(MSD_ERR_INVALID_ARG, "null tokens");
+  return MSD_OK;
+}
+
+GemmArgs gemm_base(const msd_model* m, const Shapes& s, const Layout& L, char* ws, int M) {
+  GemmArgs g{};
+  g.M = M;
+  g.partial = reinterpret_cast<float*>(ws + L.partial);
+  g.counters = reinterpret_cast<int32_t*>(ws + L.counters);
+  g.n_heads = m->cfg.n_heads;
+  g.n_kv_heads = m->cfg.n_kv_heads;
+  g.head_dim = m->cfg.head_dim;
+  g.weights_nt = m->weights_nt;
+  (void)s;
+  return g;
+}
+
+void set_shape(GemmArgs& g, const GemmShape& sh, int N) {
+  g.n_tiles = sh.n_tiles;
+  g.K = sh.K;
+  g.splits = sh.splits;
+  g.N = N;
+}
+
+// the pre-norm applied while the GEMM loads A = x
+void set_prenorm(GemmArgs& g, const msd_model* m, const float2* stats, int stats_tiles,
+                 const uint16_t* gain, const uint16_t* shift) {
+  g.a_norm = m->cfg.norm == MSD_NORM_LAYER ? 2 : 1;
+  g.a_stats = stats;
+  g.a_stats_tiles = stats_tiles;
+  g.a_g = gain;
+  g.a_b = m->cfg.norm == MSD_NORM_LAYER ? shift : nullptr;
+  g.a_eps = m->cfg.norm_eps;
+}
+
+// final norm + LM head + per-row merge (used at the early exit and at the end)
+msd_status run_head(const msd_model* m, const Shapes& s, const Layout& L, char* ws, int M,
+                    const float* x, const float2* stats, int stats_tiles, int kappa,
+                    float* logits, int32_t* ids, float* logp, int32_t* argmax, float* lse,
+                    hipStream_t stream) {
+  const msd_model_config& c = m->cfg;
+  GemmArgs g = gemm_base(m, s, L, ws, M);
+  set_shape(g, s.head, c.vocab);
+  g.A = x;
+  set_prenorm(g, m, stats, stats_tiles, T(m, MSD_T_FINAL_G), T(m, MSD_T_FINAL_B));
+  g.map = MAP_PLAIN;
+  g.w0 = head_w(m);
+  g.logits = logits;
+  g.tile_ms = reinterpret_cast<float2*>(ws + L.tile_ms);
+  g.tile_top = reinterpret_cast<uint64_t*>(ws + L.tile_top);
+  g.kappa = kappa;
+  MSD_HIP(launch_gemm(EPI_HEAD, g, stream));
+  HeadMergeArgs hm{g.tile_ms, g.tile_top, s.head.n_tiles, M, kappa, ids, logp, argmax, lse};
+  MSD_HIP(launch_head_merge(hm, stream));
+  return MSD_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+hipError_t prof_mark(const msd_model* m, int kclass, int layer, bool begin, hipStream_t s) {
+  if (m->prof_class != kclass || layer >= (int)m->prof_begin.size()) return hipSuccess;
+  return hipEventRecord(begin ? m->prof_begin[layer] : m->prof_end[layer], s);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* msd_last_error(void) { return g_err.c_str(); }
+
+msd_status msd_model_create(const msd_model_config* cfg, const void* const* tensors,
+                            int32_t n_tensors, msd_model** out) {
+  if (!cfg || !tensors || !out) return fail(MSD_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  const msd_model_config& c = *cfg;
+  if (c.n_layers < 1 || c.d_model < 64 || c.n_heads < 1 || c.n_kv_heads < 1 || c.vocab < 64 ||
+      c.d_ffn < 64)
+    return fail(MSD_ERR_SHAPE, "model sizes out of range");
+  if (c.head_dim != 64 && c.head_dim != 128) return fail(MSD_ERR_SHAPE, "head_dim must be 64 or 128");
+  if (c.n_heads % c.n_kv_heads) return fail(MSD_ERR_SHAPE, "n_heads must be a multiple of n_kv_heads");
+  if (c.d_model % 64 || c.d_ffn % 64) return fail(MSD_ERR_SHAPE, "d_model and d_ffn must be multiples of 64");
+  if (c.vocab % 16) return fail(MSD_ERR_SHAPE, "vocab must be a multiple of 16");
+  if (c.norm != MSD_NORM_RMS && c.norm != MSD_NORM_LAYER) return fail(MSD_ERR_INVALID_ARG, "norm kind");
+  if (c.act != MSD_ACT_SWIGLU && c.act != MSD_ACT_RELU) return fail(MSD_ERR_INVALID_ARG, "act kind");
+  if (c.pos != MSD_POS_ROPE && c.pos != MSD_POS_LEARNED) return fail(MSD_ERR_INVALID_ARG, "pos kind");
+  if (c.max_positions < 1) return fail(MSD_ERR_SHAPE, "max_positions must be >= 1");
+  if (!(c.norm_eps > 0.0f)) return fail(MSD_ERR_INVALID_ARG, "norm_eps must be > 0");
+  if (c.pos == MSD_POS_ROPE && !(c.rope_theta > 0.0f)) return fail(MSD_ERR_INVALID_ARG, "rope_theta must be > 0");
+  if (n_tensors != MSD_N_TENSORS(c.n_layers)) return fail(MSD_ERR_SHAPE, "n_tensors != MSD_N_TENSORS(n_layers)");
+
+  auto need = [&](int idx, const char* what) -> bool {
+    if (!tensors[idx]) {
+      g_err = std::string("missing tensor: ") + what;
+      return false;
+    }
+    if (!aligned16(tensors[idx])) {
+      g_err = std::string("tensor not 16-byte aligned: ") + what;
+      return false;
+    }
+    return true;
+  };
+  const bool ln = c.norm == MSD_NORM_LAYER, bias = c.has_bias != 0;
+  if (!need(MSD_T_EMBED, "embed") || !need(MSD_T_FINAL_G, "final_g")) return MSD_ERR_INVALID_ARG;
+  if (!c.tied_head && !need(MSD_T_LM_HEAD, "lm_head")) return MSD_ERR_INVALID_ARG;
+  if (ln && !need(MSD_T_FINAL_B, "final_b")) return MSD_ERR_INVALID_ARG;
+  if (c.pos == MSD_POS_LEARNED && !need(MSD_T_POS_EMBED, "pos_embed")) return MSD_ERR_INVALID_ARG;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const int b = MSD_TENSOR_INDEX(l, 0);
+    for (int s : {MSD_L_ATTN_G, MSD_L_WQ, MSD_L_WK, MSD_L_WV, MSD_L_WO, MSD_L_MLP_G, MSD_L_W_UP,
+                  MSD_L_W_DOWN})
+      if (!need(b + s, "layer weight")) return MSD_ERR_INVALID_ARG;
+    if (c.act == MSD_ACT_SWIGLU && !need(b + MSD_L_W_GATE, "w_gate")) return MSD_ERR_INVALID_ARG;
+    if (ln && (!need(b + MSD_L_ATTN_B, "attn_b") || !need(b + MSD_L_MLP_B, "mlp_b")))
+      return MSD_ERR_INVALID_ARG;
+    if (bias) {
+      for (int s : {MSD_L_BQ, MSD_L_BK, MSD_L_BV, MSD_L_BO})
+        if (!need(b + s, "attention bias")) return MSD_ERR_INVALID_ARG;
+      if (c.act == MSD_ACT_RELU && (!need(b + MSD_L_B_UP, "b_up") || !need(b + MSD_L_B_DOWN, "b_down")))
+        return MSD_ERR_INVALID_ARG;
+    }
+  }
+
+  msd_model* m = new msd_model();
+  m->cfg = c;
+  m->t.resize(n_tensors);
+  for (int i = 0; i < n_tensors; ++i) m->t[i] = static_cast<const uint16_t*>(tensors[i]);
+  // tensors the model does not use are ignored
+  if (!ln) {
+    m->t[MSD_T_FINAL_B] = nullptr;
+    for (int l = 0; l < c.n_layers; ++l) {
+      m->t[MSD_TENSOR_INDEX(l, MSD_L_ATTN_B)] = nullptr;
+      m->t[MSD_TENSOR_INDEX(l, MSD_L_MLP_B)] = nullptr;
+    }
+  }
+  if (!bias)
+    for (int l = 0; l < c.n_layers; ++l)
+      for (int s : {MSD_L_BQ, MSD_L_BK, MSD_L_BV, MSD_L_BO, MSD_L_B_UP, MSD_L_B_DOWN})
+        m->t[MSD_TENSOR_INDEX(l, s)] = nullptr;
+  if (c.pos != MSD_POS_LEARNED) m->t[MSD_T_POS_EMBED] = nullptr;
+  if (const char* e = getenv("MSD_GEMM_TARGET_WGS")) {
+    const int v = atoi(e);
+    if (v > 0) m->target_wgs = v;
+  }
+  if (const char* e = getenv("MSD_WEIGHTS_NT")) m->weights_nt = atoi(e) != 0;
+
+  // every projection matrix goes fragment-major, in place, through one
+  // temporary buffer as large as the largest matrix
+  {
+    struct Mat {
+      uint16_t* p;
+      int64_t rows;
+      int32_t K;
+    };
+    std::vector<Mat> mats;
+    auto add = [&](const uint16_t* p, int64_t rows, int32_t K) {
+      mats.push_back(Mat{const_cast<uint16_t*>(p), rows, K});
+    };
+    const int qd = c.n_heads * c.head_dim, kd = c.n_kv_heads * c.head_dim;
+    for (int l = 0; l < c.n_layers; ++l) {
+      add(m->t[MSD_TENSOR_INDEX(l, MSD_L_WQ)], qd, c.d_model);
+      add(m->t[MSD_TENSOR_INDEX(l, MSD_L_WK)], kd, c.d_model);
+      add(m->t[MSD_TENSOR_INDEX(l, MSD_L_WV)], kd, c.d_model);
+      add(m->t[MSD_TENSOR_INDEX(l, MSD_L_WO)], c.d_model, qd);
+      if (c.act == MSD_ACT_SWIGLU) add(m->t[MSD_TENSOR_INDEX(l, MSD_L_W_GATE)], c.d_ffn, c.d_model);
+      add(m->t[MSD_TENSOR_INDEX(l, MSD_L_W_UP)], c.d_ffn, c.d_model);
+      add(m->t[MSD_TENSOR_INDEX(l, MSD_L_W_DOWN)], c.d_model, c.d_ffn);
+    }
+    add(c.tied_head ? m->t[MSD_T_EMBED] : m->t[MSD_T_LM_HEAD], c.vocab, c.d_model);
+    size_t biggest = 0;
+    for (const Mat& x : mats) biggest = std::max(biggest, (size_t)x.rows * x.K * 2);
+    void* tmp = nullptr;
+    hipError_t e = hipMalloc(&tmp, biggest);
+    for (size_t i = 0; e == hipSuccess && i < mats.size(); ++i) {
+      const size_t bytes = (size_t)mats[i].rows * mats[i].K * 2;
+      e = hipMemcpyAsync(tmp, mats[i].p, bytes, hipMemcpyDeviceToDevice, 0);
+      if (e == hipSuccess) e = launch_repack(static_cast<uint16_t*>(tmp), mats[i].p, mats[i].rows, mats[i].K, 0);
+    }
+    if (e == hipSuccess) e = hipStreamSynchronize(0);
+    if (tmp) (void)hipFree(tmp);
+    if (e != hipSuccess) {
+      delete m;
+      return fail(MSD_ERR_HIP, std::string("weight repack: ") + hipGetErrorString(e));
+    }
+  }
+
+  if (c.pos == MSD_POS_ROPE) {
+    const int half = c.head_dim / 2;
+    std::vector<float2> tab((size_t)c.max_positions * half);
+    for (int p = 0; p < c.max_positions; ++p)
+      for (int j = 0; j < half; ++j) {
+        const double a = (double)p * std::pow((double)c.rope_theta, -2.0 * j / c.head_dim);
+        tab[(size_t)p * half + j] = make_float2((float)std::cos(a), (float)std::sin(a));
+      }
+    hipError_t e = hipMalloc(&m->rope, tab.size() * sizeof(float2));
+    if (e == hipSuccess) e = hipMemcpy(m->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      if (m->rope) (void)hipFree(m->rope);
+      delete m;
+      return fail(MSD_ERR_HIP, std::string("rotary table: ") + hipGetErrorString(e));
+    }
+  }
+  *out = m;
+  return MSD_OK;
+}
+
+void msd_model_destroy(msd_model* m) {
+  if (!m) return;
+  if (m->rope) (void)hipFree(m->rope);
+  delete m;
+}
+
+size_t msd_workspace_bytes(const msd_model* m, int32_t batch, int32_t n_slots, int32_t kappa,
+                           int32_t capacity) {
+  if (!m || batch < 1 || n_slots < 1 || capacity < 1) return 0;
+  return layout(m, batch, n_slots, kappa, capacity).total;
+}
+
+msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_block* blk,
+                            const msd_ee_request* ee, float* logits, int32_t* argmax, float* lse,
+                            void* ws, size_t ws_bytes, hipStream_t stream) {
+  msd_status st = check_block(m, blk);
+  if (st != MSD_OK) return st;
+  if (!kv || !kv->k || !kv->v || !kv->len || !kv->status) return fail(MSD_ERR_INVALID_ARG, "null kv cache field");
+  if (!argmax) return fail(MSD_ERR_INVALID_ARG, "null argmax");
+  if (blk->batch > kv->batch_cap) return fail(MSD_ERR_SHAPE, "batch exceeds the cache's batch_cap");
+  if (kv->capacity < blk->n_slots) return fail(MSD_ERR_CAPACITY, "cache capacity below n_slots");
+  const msd_model_config& c = m->cfg;
+  if (kv->capacity > c.max_positions) return fail(MSD_ERR_CAPACITY, "cache capacity exceeds max_positions");
+  if (kv->capacity > kMaxAttnChunks * kAttnChunk) return fail(MSD_ERR_CAPACITY, "cache capacity above 32768");
+  int kappa = 1;
+  if (ee) {
+    if (ee->layer < 1 || ee->layer > c.n_layers - 1) return fail(MSD_ERR_INVALID_ARG, "early-exit layer out of [1, n_layers-1]");
+    if (ee->kappa < 1 || ee->kappa > kMaxKappa) return fail(MSD_ERR_INVALID_ARG, "kappa out of [1, 32]");
+    if (!ee->ids || !ee->logp) return fail(MSD_ERR_INVALID_ARG, "null early-exit outputs");
+    kappa = ee->kappa;
+  }
+  Topo topo;
+  st = make_topo(blk, &topo);
+  if (st != MSD_OK) return st;
+  const Layout L = layout(m, blk->batch, blk->n_slots, kappa, kv->capacity);
+  if (!ws || ws_bytes < L.total) return fail(MSD_ERR_WORKSPACE, "workspace too small");
+  const Shapes s = shapes(m);
+  char* w = static_cast<char*>(ws);
+  const int M = blk->batch * blk->n_slots;
+  const int d = c.d_model, qd = c.n_heads * c.head_dim;
+  float* x = reinterpret_cast<float*>(w + L.x);
+  float2* stats = reinterpret_cast<float2*>(w + L.stats);
+  const int resid_tiles = d / kTileN;
+  float* q = reinterpret_cast<float*>(w + L.q);
+  float* att = reinterpret_cast<float*>(w + L.attn);
+  float* act = reinterpret_cast<float*>(w + L.act);
+  int32_t* counters = reinterpret_cast<int32_t*>(w + L.counters);
+  const size_t layer_elems = (size_t)kv->batch_cap * c.n_kv_heads * kv->capacity * c.head_dim;
+
+  EmbedArgs ea{};
+  ea.tokens = blk->tokens;
+  ea.embed = T(m, MSD_T_EMBED);
+  ea.pos_embed = T(m, MSD_T_POS_EMBED);
+  ea.embed_frag = c.tied_head;
+  ea.len = kv->len;
+  ea.M = M;
+  ea.d = d;
+  ea.n_slots = blk->n_slots;
+  ea.max_positions = c.max_positions;
+  ea.vocab = c.vocab;
+  ea.status = kv->status;
+  ea.x = x;
+  ea.stats = stats;
+  ea.zero_i32 = counters;
+  ea.n_zero = L.n_counters;
+  for (int i = 0; i < kMaxSlots; ++i) ea.depth[i] = topo.depth[i];
+  MSD_HIP(launch_embed(ea, stream));
+
+  for (int l = 0; l < c.n_layers; ++l) {
+    uint16_t* kc = static_cast<uint16_t*>(kv->k) + (size_t)l * layer_elems;
+    uint16_t* vc = static_cast<uint16_t*>(kv->v) + (size_t)l * layer_elems;
+
+    // the residual stream's row statistics come from the embedding (layer 0)
+    // or from the previous layer's down projection
+    const int st_tiles = l == 0 ? 1 : resid_tiles;
+    GemmArgs g = gemm_base(m, s, L, w, M);
+    set_shape(g, s.qkv, (c.n_heads + 2 * c.n_kv_heads) * c.head_dim);
+    g.A = x;
+    set_prenorm(g, m, stats, st_tiles, LT(m, l, MSD_L_ATTN_G), LT(m, l, MSD_L_ATTN_B));
+    g.map = MAP_QKV;
+    g.w0 = LT(m, l, MSD_L_WQ);
+    g.w1 = LT(m, l, MSD_L_WK);
+    g.w2 = LT(m, l, MSD_L_WV);
+    g.b0 = LT(m, l, MSD_L_BQ);
+    g.b1 = LT(m, l, MSD_L_BK);
+    g.b2 = LT(m, l, MSD_L_BV);
+    g.out_f32 = q;
+    g.k_cache = kc;
+    g.v_cache = vc;
+    g.len = kv->len;
+    g.status = kv->status;
+    g.capacity = kv->capacity;
+    g.n_slots = blk->n_slots;
+    g.rope = m->rope;
+    g.rope_rows = c.max_positions;
+    for (int i = 0; i < kMaxSlots; ++i) g.depth[i] = topo.depth[i];
+    MSD_HIP(prof_mark(m, MSD_K_QKV, l, true, stream));
+    MSD_HIP(launch_gemm(EPI_QKV, g, stream));
+    MSD_HIP(prof_mark(m, MSD_K_QKV, l, false, stream));
+
+    AttnArgs aa{};
+    aa.q = q;
+    aa.k_cache = kc;
+    aa.v_cache = vc;
+    aa.len = kv->len;
+    aa.status = kv->status;
+    aa.out = att;
+    aa.part_o = reinterpret_cast<float*>(w + L.part_o);
+    aa.part_ml = reinterpret_cast<float*>(w + L.part_ml);
+    aa.batch = blk->batch;
+    aa.n_heads = c.n_heads;
+    aa.n_kv_heads = c.n_kv_heads;
+    aa.capacity = kv->capacity;
+    aa.n_slots = blk->n_slots;
+    aa.max_chunks = L.max_chunks;
+    aa.scale = 1.0f / std::sqrt((float)c.head_dim);
+    aa.topo = topo;
+    MSD_HIP(prof_mark(m, MSD_K_ATTN, l, true, stream));
+    MSD_HIP(launch_attention(c.head_dim, aa, stream));
+    MSD_HIP(prof_mark(m, MSD_K_ATTN, l, false, stream));
+
+    g = gemm_base(m, s, L, w, M);
+    set_shape(g, s.o, d);
+    g.A = att;
+    g.map = MAP_PLAIN;
+    g.w0 = LT(m, l, MSD_L_WO);
+    g.b0 = LT(m, l, MSD_L_BO);
+    g.x = x;
+    g.stats_out = stats;
+    MSD_HIP(prof_mark(m, MSD_K_OPROJ, l, true, stream));
+    MSD_HIP(launch_gemm(EPI_RESID, g, stream));
+    MSD_HIP(prof_mark(m, MSD_K_OPROJ, l, false, stream));
+
+    g = gemm_base(m, s, L, w, M);
+    g.A = x;
+    set_prenorm(g, m, stats, resid_tiles, LT(m, l, MSD_L_MLP_G), LT(m, l, MSD_L_MLP_B));
+    g.out_f32 = act;
+    MSD_HIP(prof_mark(m, MSD_K_FFN_UP, l, true, stream));
+    if (c.act == MSD_ACT_SWIGLU) {
+      set_shape(g, s.up, 2 * c.d_ffn);
+      g.map = MAP_GATEUP;
+      g.w0 = LT(m, l, MSD_L_W_GATE);
+      g.w1 = LT(m, l, MSD_L_W_UP);
+      MSD_HIP(launch_gemm(EPI_SWIGLU, g, stream));
+    } else {
+      set_shape(g, s.up, c.d_ffn);
+      g.map = MAP_PLAIN;
+      g.w0 = LT(m, l, MSD_L_W_UP);
+      g.b0 = LT(m, l, MSD_L_B_UP);
+      MSD_HIP(launch_gemm(EPI_RELU, g, stream));
+    }
+    MSD_HIP(prof_mark(m, MSD_K_FFN_UP, l, false, stream));
+
+    g = gemm_base(m, s, L, w, M);
+    set_shape(g, s.down, d);
+    g.A = act;
+    g.map = MAP_PLAIN;
+    g.w0 = LT(m, l, MSD_L_W_DOWN);
+    g.b0 = LT(m, l, MSD_L_B_DOWN);
+    g.x = x;
+    g.stats_out = stats;
+    MSD_HIP(prof_mark(m, MSD_K_FFN_DOWN, l, true, stream));
+    MSD_HIP(launch_gemm(EPI_RESID, g, stream));
+    MSD_HIP(prof_mark(m, MSD_K_FFN_DOWN, l, false, stream));
+
+    if (ee && l + 1 == ee->layer) {
+      st = run_head(m, s, L, w, M, x, stats, resid_tiles, ee->kappa, nullptr, ee->ids, ee->logp,
+                    nullptr, nullptr, stream);
+      if (st != MSD_OK) return st;
+      if (ee->ready) MSD_HIP(hipEventRecord(ee->ready, stream));
+    }
+  }
+  (void)qd;
+  return run_head(m, s, L, w, M, x, stats, resid_tiles, 1, logits, nullptr, nullptr, argmax, lse,
+                  stream);
+}
+
+msd_status msd_early_exit_topk(const msd_model* m, const float* hidden, int32_t M, int32_t kappa,
+                               int32_t* ids, float* logp, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  if (!m || !hidden || !ids || !logp) return fail(MSD_ERR_INVALID_ARG, "null argument");
+  if (M < 1 || M > kMaxMT * 16) return fail(MSD_ERR_SHAPE, "M must lie in [1, 144]");
+  if (kappa < 1 || kappa > kMaxKappa) return fail(MSD_ERR_INVALID_ARG, "kappa out of [1, 32]");
+  const Layout L = layout(m, 1, M, kappa, 1);
+  if (!ws || ws_bytes < L.total) return fail(MSD_ERR_WORKSPACE, "workspace too small");
+  const Shapes s = shapes(m);
+  char* w = static_cast<char*>(ws);
+  // the head GEMM's split-K counters must start at zero (a kernel, not a
+  // memset node, so the call stays safe under graph capture)
+  MSD_HIP(launch_zero_i32(reinterpret_cast<int32_t*>(w + L.counters), L.n_counters, stream));
+  float2* stats = reinterpret_cast<float2*>(w + L.stats);
+  MSD_HIP(launch_row_stats(hidden, M, m->cfg.d_model, stats, stream));
+  return run_head(m, s, L, w, M, hidden, stats, 1, kappa, nullptr, ids, logp, nullptr, nullptr,
+                  stream);
+}
+
+msd_status msd_accept(const msd_model* m, const msd_block* blk, const float* logits,
+                      const int32_t* argmax, const msd_sampling* smp, int32_t* acc_len,
+                      int32_t* next_tok, int32_t* path, uint32_t* status, void* ws,
+                      size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  msd_status st = check_block(m, blk);
+  if (st != MSD_OK) return st;
+  if (!acc_len || !next_tok || !path) return fail(MSD_ERR_INVALID_ARG, "null output");
+  Topo topo;
+  st = make_topo(blk, &topo);
+  if (st != MSD_OK) return st;
+  AcceptArgs a{};
+  a.mode = smp ? smp->mode : MSD_GREEDY;
+  if (a.mode == MSD_GREEDY) {
+    if (!argmax) return fail(MSD_ERR_INVALID_ARG, "GREEDY needs argmax");
+  } else if (a.mode == MSD_REJECTION || a.mode == MSD_MATCH) {
+    if (!logits) return fail(MSD_ERR_INVALID_ARG, "stochastic acceptance needs logits");
+    if (!(smp->temperature > 0.0f)) return fail(MSD_ERR_INVALID_ARG, "temperature must be > 0");
+    if (!smp->u_sample) return fail(MSD_ERR_INVALID_ARG, "null u_sample");
+    if (a.mode == MSD_REJECTION) {
+      if (smp->n_cand < 1 || smp->n_cand > 64) return fail(MSD_ERR_INVALID_ARG, "n_cand out of [1, 64]");
+      if (!smp->cand_ids || !smp->cand_q || !smp->u_accept)
+        return fail(MSD_ERR_INVALID_ARG, "REJECTION needs cand_ids, cand_q and u_accept");
+    }
+  } else {
+    return fail(MSD_ERR_UNSUPPORTED, "unknown acceptance mode");
+  }
+  a.temperature = smp ? smp->temperature : 1.0f;
+  a.batch = blk->batch;
+  a.n_slots = blk->n_slots;
+  a.vocab = m->cfg.vocab;
+  a.n_cand = smp ? smp->n_cand : 0;
+  a.tokens = blk->tokens;
+  a.logits = logits;
+  a.argmax = argmax;
+  a.cand_ids = smp ? smp->cand_ids : nullptr;
+  a.cand_q = smp ? smp->cand_q : nullptr;
+  a.u_accept = smp ? smp->u_accept : nullptr;
+  a.u_sample = smp ? smp->u_sample : nullptr;
+  a.acc_len = acc_len;
+  a.next_tok = next_tok;
+  a.path = path;
+  a.status = status;
+  a.topo = topo;
+  if (a.mode == MSD_REJECTION && !status) return fail(MSD_ERR_INVALID_ARG, "REJECTION needs a status word");
+  MSD_HIP(launch_accept(a, stream));
+  return MSD_OK;
+}
+
+msd_status msd_kv_commit(const msd_model* m, msd_kv_cache* kv, const msd_block* blk,
+                         const int32_t* acc_len, const int32_t* path, hipStream_t stream) {
+  msd_status st = check_block(m, blk);
+  if (st != MSD_OK) return st;
+  if (!kv || !kv->k || !kv->v || !kv->len) return fail(MSD_ERR_INVALID_ARG, "null kv cache field");
+  if (!acc_len || !path) return fail(MSD_ERR_INVALID_ARG, "null acc_len or path");
+  if (blk->batch > kv->batch_cap) return fail(MSD_ERR_SHAPE, "batch exceeds the cache's batch_cap");
+  Topo topo;
+  st = make_topo(blk, &topo);
+  if (st != MSD_OK) return st;
+  bool chain = true;
+  for (int i = 1; i < blk->n_slots; ++i) chain = chain && topo.parent[i] == i - 1;
+  CommitArgs a{};
+  a.k_cache = static_cast<uint16_t*>(kv->k);
+  a.v_cache = static_cast<uint16_t*>(kv->v);
+  a.len = kv->len;
+  a.acc_len = acc_len;
+  a.path = path;
+  a.n_layers = m->cfg.n_layers;
+  a.batch = blk->batch;
+  a.batch_cap = kv->batch_cap;
+  a.n_kv_heads = m->cfg.n_kv_heads;
+  a.capacity = kv->capacity;
+  a.head_dim = m->cfg.head_dim;
+  a.n_slots = blk->n_slots;
+  a.copy_rows = chain ? 0 : 1;
+  if (blk->n_slots < 2) a.copy_rows = 0;
+  MSD_HIP(launch_commit(a, stream));
+  return MSD_OK;
+}
+
+msd_status msd_set_profile(msd_model* m, int32_t kclass, hipEvent_t* begin, hipEvent_t* end,
+                           int32_t n) {
+  if (!m) return fail(MSD_ERR_INVALID_ARG, "null model");
+  m->prof_begin.clear();
+  m->prof_end.clear();
+  m->prof_class = -1;
+  if (n <= 0) return MSD_OK;
+  if (!begin || !end) return fail(MSD_ERR_INVALID_ARG, "null event arrays");
+  if (kclass < MSD_K_QKV || kclass > MSD_K_FFN_DOWN) return fail(MSD_ERR_INVALID_ARG, "kernel class");
+  m->prof_begin.assign(begin, begin + n);
+  m->prof_end.assign(end, end + n);
+  m->prof_class = kclass;
+  return MSD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,172 @@
+"""Test-side driver: one seeded workload through the HIP library and the oracle.
+
+Only the shared input generator feeds both sides; the oracle never sees a
+byte that the HIP path produced.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional
+
+import numpy as np
+
+import oracle as orc
+from paper_2510_13161_amd import synth
+
+TOL_LOGIT = 2e-2          # max |logit_gpu - logit_oracle| (bf16 operands, fp32 accumulation)
+TIE_MARGIN = 2 * TOL_LOGIT  # decisions closer than this in the oracle are flagged
+
+
+def round_up(x: int, m: int) -> int:
+    return (x + m - 1) // m * m
+
+
+@dataclasses.dataclass
+class GpuResult:
+    logits: Optional[np.ndarray]   # [M, V] fp32
+    argmax: np.ndarray             # [M]
+    lse: np.ndarray                # [M]
+    ee_ids: Optional[np.ndarray]   # [M, kappa]
+    ee_logp: Optional[np.ndarray]
+    acc_len: np.ndarray            # [B]
+    next_tok: np.ndarray           # [B]
+    path: np.ndarray               # [B, n_slots]
+    len_after: np.ndarray          # [B]
+    status: int
+    k_rows: List[np.ndarray]       # per layer [B][Hkv][n_slots][hd] bf16 bits (after verify)
+    v_rows: List[np.ndarray]
+
+
+class GpuCase:
+    """A workload (optionally depth-reduced) resident on the GPU."""
+
+    def __init__(self, w: synth.Workload, n_layers: Optional[int] = None,
+                 capacity: Optional[int] = None, inputs: Optional[synth.StepInputs] = None):
+        import torch
+        from paper_2510_13161_amd import msd
+        self.torch, self.msd = torch, msd
+        self.w = w
+        self.shape = w.model if n_layers is None else w.model.with_layers(n_layers)
+        self.si = inputs if inputs is not None else synth.step_inputs(w)
+        lens = self.si.ctx_len
+        self.capacity = capacity or round_up(int(lens.max()) + w.n_slots, 64)
+        self.dev = synth.device_weights(self.shape, w.seed)
+        maxpos = self.capacity if self.shape.pos == "rope" else self.shape.max_positions
+        self.model = msd.Model(self.shape, self.dev, max_positions=maxpos)
+        self.cache = msd.Cache(self.shape, w.batch, self.capacity)
+        self.cache.len.copy_(torch.from_numpy(lens))
+        synth.device_fill_ctx(self.shape, w.seed, self.cache.k, self.cache.v, self.cache.len)
+        torch.cuda.synchronize()
+
+    def reset_len(self):
+        self.cache.len.copy_(self.torch.from_numpy(self.si.ctx_len))
+        self.cache.status.zero_()
+
+    def run(self, ee: bool = True, want_logits: bool = True, commit: bool = True,
+            mode: Optional[str] = None) -> GpuResult:
+        torch, msd = self.torch, self.msd
+        w, si = self.w, self.si
+        dev = "cuda"
+        B, n = w.batch, w.n_slots
+        M = B * n
+        V = self.shape.vocab
+        mode = mode or w.mode
+        tokens = torch.from_numpy(si.tokens).to(dev)
+        parent = None if w.topology == "chain" else si.parent
+        blk = msd.make_block(tokens, parent)
+        logits = torch.empty((M, V), dtype=torch.float32, device=dev) if want_logits else None
+        argmax = torch.empty(M, dtype=torch.int32, device=dev)
+        lse = torch.empty(M, dtype=torch.float32, device=dev)
+        req = None
+        if ee:
+            ids = torch.empty((M, w.kappa), dtype=torch.int32, device=dev)
+            logp = torch.empty((M, w.kappa), dtype=torch.float32, device=dev)
+            req = msd.EERequest(min(w.ee_layer, self.shape.n_layers - 1), w.kappa, ids.data_ptr(),
+                                logp.data_ptr(), None)
+        nb = msd.workspace_bytes(self.model.handle, B, n, w.kappa if ee else 1, self.capacity)
+        ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+        msd.verify_block(self.model.handle, self.cache.c, blk, req, logits, argmax, lse, ws)
+        # block rows written by the verify pass
+        k_rows, v_rows = [], []
+        for l in range(self.shape.n_layers):
+            kr = np.empty((B, self.shape.n_kv_heads, n, self.shape.head_dim), np.uint16)
+            vr = np.empty_like(kr)
+            for b in range(B):
+                L = int(si.ctx_len[b])
+                kr[b] = self.cache.k[l, b, :, L:L + n].view(torch.int16).cpu().numpy().view(np.uint16)
+                vr[b] = self.cache.v[l, b, :, L:L + n].view(torch.int16).cpu().numpy().view(np.uint16)
+            k_rows.append(kr)
+            v_rows.append(vr)
+        acc = torch.empty(B, dtype=torch.int32, device=dev)
+        nxt = torch.empty(B, dtype=torch.int32, device=dev)
+        path = torch.empty((B, n), dtype=torch.int32, device=dev)
+        smp = None
+        keep = []
+        if mode != "greedy":
+            t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+            cid, cq = t(si.cand_ids), t(si.cand_q)
+            ua, us = t(si.u_accept), t(si.u_sample)
+            keep += [cid, cq, ua, us]
+            smp = msd.Sampling(msd.MODES[mode], float(w.temperature), si.cand_ids.shape[-1],
+                               cid.data_ptr(), cq.data_ptr(), ua.data_ptr(), us.data_ptr())
+        msd.accept(self.model.handle, blk, logits, argmax, smp, acc, nxt, path, self.cache.status)
+        if commit:
+            msd.kv_commit(self.model.handle, self.cache.c, blk, acc, path)
+        torch.cuda.synchronize()
+        return GpuResult(
+            logits=logits.cpu().numpy() if logits is not None else None,
+            argmax=argmax.cpu().numpy(), lse=lse.cpu().numpy(),
+            ee_ids=ids.cpu().numpy() if ee else None, ee_logp=logp.cpu().numpy() if ee else None,
+            acc_len=acc.cpu().numpy(), next_tok=nxt.cpu().numpy(), path=path.cpu().numpy(),
+            len_after=self.cache.len.cpu().numpy(), status=int(self.cache.status.item()),
+            k_rows=k_rows, v_rows=v_rows)
+
+
+@dataclasses.dataclass
+class OracleSeq:
+    logits: np.ndarray
+    ee_ids: Optional[np.ndarray]
+    ee_logp: Optional[np.ndarray]
+    ee_margin: Optional[np.ndarray]
+    blk_k: List[np.ndarray]
+    blk_v: List[np.ndarray]
+    acc: int
+    nxt: int
+    path: np.ndarray
+
+
+def oracle_sequence(shape, w: synth.Workload, si: synth.StepInputs, b: int, ee: bool = True,
+                    weights: Optional[Dict[str, np.ndarray]] = None, mode: Optional[str] = None,
+                    oracle_obj: Optional[orc.Oracle] = None) -> OracleSeq:
+    """The oracle's verification step for sequence b of the workload."""
+    o = oracle_obj or orc.Oracle(shape, weights if weights is not None else synth.host_weights(shape, w.seed))
+    L = int(si.ctx_len[b])
+    cache = {}
+
+    def ctx(l):
+        if l not in cache:
+            cache.clear()
+            cache[l] = (synth.host_ctx(shape, w.seed, l, "k", b, L), synth.host_ctx(shape, w.seed, l, "v", b, L))
+        return cache[l]
+
+    pos = L + orc.depths(si.parent)
+    ee_layer = min(w.ee_layer, shape.n_layers - 1) if ee else None
+    r = o.forward(si.tokens[b], pos, si.parent, ctx, L, ee_layer=ee_layer)
+    ids = logp = marg = None
+    if ee:
+        z_ee = o.head(r.x_ee)
+        ids, logp, _ = orc.Oracle.topk(z_ee, w.kappa)
+        marg = margins(z_ee, w.kappa)
+    mode = mode or w.mode
+    kw = {}
+    if mode != "greedy":
+        kw = dict(cand_ids=si.cand_ids[b], cand_q=si.cand_q[b], u_accept=si.u_accept[b],
+                  u_sample=si.u_sample[b])
+    A, nxt, path = o.accept(si.parent, si.tokens[b], r.logits, mode, w.temperature, **kw)
+    return OracleSeq(r.logits, ids, logp, marg, r.blk_k, r.blk_v, A, nxt, path)
+
+
+def margins(z: np.ndarray, k: int) -> np.ndarray:
+    """Smallest gap among the k+1 largest logits of each row."""
+    part = -np.sort(-z, axis=-1)[..., :k + 1]
+    return np.min(part[..., :-1] - part[..., 1:], axis=-1)

@@ -1,0 +1,170 @@
+"""Parity of the HIP verification step (through the C ABI) against the oracle."""
+import numpy as np
+import pytest
+
+from paper_2510_13161_amd import synth
+from tests import harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _compare(case, gr, seqs, check_ee=True, tol=H.TOL_LOGIT):
+    """Element-wise comparison of one GPU step with the oracle's sequences."""
+    w, si = case.w, case.si
+    n, V = w.n_slots, case.shape.vocab
+    report = {"max_abs": 0.0, "flagged_rows": 0, "flagged_seqs": 0}
+    for b, o in seqs.items():
+        rows = slice(b * n, (b + 1) * n)
+        if gr.logits is not None:
+            err = np.abs(gr.logits[rows] - o.logits)
+            report["max_abs"] = max(report["max_abs"], float(err.max()))
+            assert err.max() <= tol, f"seq {b}: logits max abs {err.max():.3e} > {tol}"
+        lse_ref = np.log(np.exp(o.logits - o.logits.max(-1, keepdims=True)).sum(-1)) + o.logits.max(-1)
+        assert np.max(np.abs(gr.lse[rows] - lse_ref)) <= tol
+        top1 = np.argmax(o.logits, -1)
+        tie = H.margins(o.logits, 1) < H.TIE_MARGIN
+        report["flagged_rows"] += int(tie.sum())
+        assert np.array_equal(gr.argmax[rows][~tie], top1[~tie]), f"seq {b}: argmax differs"
+        if check_ee and o.ee_ids is not None:
+            # rows whose kappa+1 best early-exit logits are closer than the margin are flagged
+            firm = o.ee_margin >= H.TIE_MARGIN
+            report["ee_flagged_rows"] = report.get("ee_flagged_rows", 0) + int((~firm).sum())
+            assert np.array_equal(gr.ee_ids[rows][firm], o.ee_ids[firm]), f"seq {b}: early-exit ids"
+            same = np.all(gr.ee_ids[rows] == o.ee_ids, axis=-1)
+            err = np.abs(gr.ee_logp[rows] - o.ee_logp)[same]
+            assert err.max(initial=0.0) <= tol, f"seq {b}: early-exit logp {err.max():.3e}"
+        # decisions: exact unless the oracle's walk passed a flagged node
+        visited_tie = any(tie[s] for s in o.path)
+        if visited_tie and w.mode == "greedy":
+            report["flagged_seqs"] += 1
+            continue
+        assert gr.acc_len[b] == o.acc, f"seq {b}: accepted length {gr.acc_len[b]} != {o.acc}"
+        assert gr.next_tok[b] == o.nxt, f"seq {b}: next token {gr.next_tok[b]} != {o.nxt}"
+        assert np.array_equal(gr.path[b][:o.acc + 1], o.path)
+        assert np.all(gr.path[b][o.acc + 1:] == -1)
+        assert gr.len_after[b] == si.ctx_len[b] + 1 + o.acc
+        # K/V rows the verify pass wrote at len + slot
+        for l in range(case.shape.n_layers):
+            kg = synth.bf16_bits_to_f32(gr.k_rows[l][b]).astype(np.float64)   # [Hkv][n][hd]
+            vg = synth.bf16_bits_to_f32(gr.v_rows[l][b]).astype(np.float64)
+            ko = np.transpose(o.blk_k[l], (1, 0, 2))
+            vo = np.transpose(o.blk_v[l], (1, 0, 2))
+            scale = max(1.0, float(np.abs(ko).max()))
+            assert np.max(np.abs(kg - ko)) <= tol * scale, f"layer {l} k rows"
+            assert np.max(np.abs(vg - vo)) <= tol * max(1.0, float(np.abs(vo).max())), f"layer {l} v rows"
+    assert gr.status == 0
+    return report
+
+
+def test_device_generator_matches_host():
+    torch = _torch()
+    m = synth.TINY
+    dev = synth.device_weights(m, 0)
+    host = synth.host_weights(m, 0)
+    for name, t in dev.items():
+        d = t.view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(d, host[name]), name
+    k = torch.zeros((1, 2, 4, 160, 64), dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros_like(k)
+    lens = torch.tensor([100, 37], dtype=torch.int32, device="cuda")
+    synth.device_fill_ctx(m, 3, k, v, lens)
+    for b, L in enumerate([100, 37]):
+        got = k[0, b, :, :L].view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, synth.host_ctx(m, 3, 0, "k", b, L))
+
+
+@pytest.fixture(scope="module")
+def tiny_case():
+    _torch()
+    return H.GpuCase(synth.WORKLOADS["tiny_chain"])
+
+
+def test_tiny_chain_step(tiny_case):
+    case = tiny_case
+    case.reset_len()
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, case.w, case.si, 0)
+    rep = _compare(case, gr, {0: o})
+    print("tiny chain:", rep)
+
+
+def test_tiny_planted_acceptance(tiny_case):
+    """Drafts equal to the oracle's greedy continuation up to a planted mismatch:
+    the GPU accepts exactly the prefix token-by-token argmax decoding gives."""
+    import oracle as orc
+    case = tiny_case
+    w = case.w
+    o = orc.Oracle(case.shape, synth.host_weights(case.shape, w.seed))
+    L = int(case.si.ctx_len[0])
+    ctx = lambda l: (synth.host_ctx(case.shape, w.seed, l, "k", 0, L),
+                     synth.host_ctx(case.shape, w.seed, l, "v", 0, L))
+    root = int(case.si.tokens[0, 0])
+    y, zs = o.decode_greedy(root, L, w.gamma + 1, ctx, L)
+    for mism in range(1, w.gamma + 2):
+        drafts = y[:w.gamma].copy()
+        if mism <= w.gamma:
+            drafts[mism - 1] = (drafts[mism - 1] + 1) % case.shape.vocab
+        si = synth.StepInputs(parent=case.si.parent, tokens=np.concatenate([[root], drafts])[None].astype(np.int32),
+                              ctx_len=case.si.ctx_len)
+        case.si = si
+        case.reset_len()
+        gr = case.run(ee=False)
+        want = min(mism - 1, w.gamma)
+        margin = np.min([np.sort(z)[-1] - np.sort(z)[-2] for z in zs[:want + 1]])
+        if margin < H.TIE_MARGIN:
+            continue
+        assert gr.acc_len[0] == want
+        assert gr.next_tok[0] == y[want]
+        assert gr.len_after[0] == L + 1 + want
+
+
+def test_tiny_tree_rejection_and_match():
+    _torch()
+    w = synth.WORKLOADS["14b_tree"].with_model(synth.TINY, ee_layer=1, kappa=4, seed=7, ctx=(96, 96))
+    case = H.GpuCase(w)
+    for mode in ("rejection", "match", "greedy"):
+        case.reset_len()
+        gr = case.run(mode=mode)
+        o = H.oracle_sequence(case.shape, w, case.si, 0, mode=mode)
+        _compare(case, gr, {0: o})
+
+
+def test_depth_reduced_14b_chain():
+    """14B widths (d 5120, GQA 40/8, FFN 13824, vocab 152064) with 2 layers."""
+    _torch()
+    w = synth.WORKLOADS["14b_chain"].with_model(synth.QWEN14B)
+    case = H.GpuCase(w, n_layers=2)
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    rep = _compare(case, gr, {0: o})
+    print("14b L2 chain:", rep)
+
+
+def test_depth_reduced_66b_tree():
+    """66B widths (MHA 72 heads, LayerNorm, learned positions, ReLU, biases, tied head), 2 layers."""
+    _torch()
+    w = synth.WORKLOADS["66b_tree"]
+    case = H.GpuCase(w, n_layers=2)
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    rep = _compare(case, gr, {0: o})
+    print("66b L2 tree:", rep)
+
+
+def test_step_is_deterministic(tiny_case):
+    case = tiny_case
+    case.si = synth.step_inputs(case.w)
+    case.reset_len()
+    a = case.run()
+    case.reset_len()
+    b = case.run()
+    assert np.array_equal(a.logits, b.logits)
+    assert np.array_equal(a.ee_logp, b.ee_logp)
+    assert np.array_equal(a.k_rows[0], b.k_rows[0])
