@@ -67,7 +67,7 @@ def lib():
         P = ctypes.c_void_p
         i32 = ctypes.c_int32
         L.msdo_embed.argtypes = [P, P, i32, P, P, P]
-        L.msdo_layer.argtypes = [P, P, i32, P, P, P, i32, i32, P, P, i32, P, P, P, P]
+        L.msdo_layer.argtypes = [P, P, i32, P, P, P, i32, i32, P, P, i32, P, P, P, P, i32]
         L.msdo_head.argtypes = [P, P, i32, P, P]
         L.msdo_topk.argtypes = [i32, i32, P, i32, P, P, P]
         L.msdo_accept.argtypes = [i32, P, P, i32, P, i32, ctypes.c_double, i32, P, P, P, P,
@@ -107,11 +107,16 @@ class Oracle:
     shape    a ``synth.ModelShape`` (sizes, norm/activation/position kinds)
     weights  dict name -> uint16 bf16 bits for global tensors, and either the
              layer tensors too or ``layer_source(l) -> dict`` to stream them.
+    kv_cache_bf16  the block's keys/values are stored in the KV cache's bf16
+             format before they are attended to (the cache holds the given
+             context in that format); False keeps them at fp64.
     """
 
     def __init__(self, shape, weights: Dict[str, np.ndarray],
-                 layer_source: Optional[Callable[[int], Dict[str, np.ndarray]]] = None):
+                 layer_source: Optional[Callable[[int], Dict[str, np.ndarray]]] = None,
+                 kv_cache_bf16: bool = True):
         self.m = shape
+        self.kv_cache_bf16 = int(kv_cache_bf16)
         self.cfg = _Cfg(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads,
                         shape.head_dim, shape.d_ffn, shape.vocab,
                         int(shape.norm == "layer"), int(shape.act == "relu"),
@@ -192,7 +197,7 @@ class Oracle:
         lib().msdo_layer(ctypes.byref(self.cfg), ctypes.byref(w), n, _p(x), _p(pos), _p(parent),
                          n_ctx, stride, _p(ctx_k), _p(ctx_v), n_extra,
                          _p(extra_k) if n_extra else None, _p(extra_v) if n_extra else None,
-                         _p(blk_k), _p(blk_v))
+                         _p(blk_k), _p(blk_v), self.kv_cache_bf16)
         del keep
         return blk_k, blk_v
 

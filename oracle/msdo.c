@@ -112,6 +112,17 @@ static void rope(double* u, int hd, int pos, double theta) {
 
 static double silu(double z) { return z / (1.0 + exp(-z)); }
 
+/* Nearest value with an 8-bit significand (the bf16 format), ties to even:
+ * the representation of a K/V cache entry. (Range limits of bf16 are far
+ * from the values seen here.) */
+static double to_cache_format(double v) {
+  if (v == 0.0 || !isfinite(v)) return v;
+  int e;
+  frexp(v, &e);                       /* v = f * 2^e, 0.5 <= |f| < 1 */
+  const double scaled = ldexp(v, 8 - e);  /* 8 significant bits left of the point */
+  return ldexp(nearbyint(scaled), e - 8);
+}
+
 void msdo_embed(const msdo_cfg* c, const msdo_global_w* g, int32_t n, const int32_t* tok,
                 const int32_t* pos, double* x) {
   const int d = c->d_model;
@@ -128,7 +139,8 @@ void msdo_embed(const msdo_cfg* c, const msdo_global_w* g, int32_t n, const int3
 void msdo_layer(const msdo_cfg* c, const msdo_layer_w* w, int32_t n, double* x,
                 const int32_t* pos, const int32_t* parent, int32_t n_ctx, int32_t ctx_stride,
                 const uint16_t* ctx_k, const uint16_t* ctx_v, int32_t n_extra,
-                const double* extra_k, const double* extra_v, double* blk_k, double* blk_v) {
+                const double* extra_k, const double* extra_v, double* blk_k, double* blk_v,
+                int32_t kv_cache_bf16) {
   const int d = c->d_model, H = c->n_heads, Hk = c->n_kv_heads, hd = c->head_dim;
   const int qd = H * hd, kd = Hk * hd, F = c->d_ffn;
   const int group = H / Hk;
@@ -154,6 +166,14 @@ void msdo_layer(const msdo_cfg* c, const msdo_layer_w* w, int32_t n, double* x,
     for (int i = 0; i < n; ++i) {
       for (int hh = 0; hh < H; ++hh) rope(q + (size_t)i * qd + hh * hd, hd, pos[i], c->rope_theta);
       for (int hh = 0; hh < Hk; ++hh) rope(blk_k + (size_t)i * kd + hh * hd, hd, pos[i], c->rope_theta);
+    }
+  }
+  /* the block's keys and values enter the KV cache, which stores the same
+   * bf16 format as the given context, before any row attends to them */
+  if (kv_cache_bf16) {
+    for (size_t t = 0; t < (size_t)n * kd; ++t) {
+      blk_k[t] = to_cache_format(blk_k[t]);
+      blk_v[t] = to_cache_format(blk_v[t]);
     }
   }
 

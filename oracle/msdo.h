@@ -78,13 +78,17 @@ void msdo_embed(const msdo_cfg* c, const msdo_global_w* g, int32_t n, const int3
  *                this oracle produced and committed), may be NULL if 0.
  *  blk_k/blk_v   out: the block's own rotated keys / values, fp64
  *                [n][n_kv_heads][head_dim].
+ *  kv_cache_bf16 1: the block's keys / values are stored in the cache's bf16
+ *                format (nearest 8-bit significand, ties to even) before
+ *                any row attends to them; 0: kept at fp64.
  * Key order for row i: context rows, extra rows, then block rows in slot
  * order (positions ascending).
  */
 void msdo_layer(const msdo_cfg* c, const msdo_layer_w* w, int32_t n, double* x,
                 const int32_t* pos, const int32_t* parent, int32_t n_ctx, int32_t ctx_stride,
                 const uint16_t* ctx_k, const uint16_t* ctx_v, int32_t n_extra,
-                const double* extra_k, const double* extra_v, double* blk_k, double* blk_v);
+                const double* extra_k, const double* extra_v, double* blk_k, double* blk_v,
+                int32_t kv_cache_bf16);
 
 /* logits[i][v] = (W_LM norm_f(x_i))_v, [n][V]. */
 void msdo_head(const msdo_cfg* c, const msdo_global_w* g, int32_t n, const double* x,

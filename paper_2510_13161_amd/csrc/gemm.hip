@@ -183,14 +183,22 @@ __device__ void norm_rows(const GemmArgs& a, float2* rowstat) {
   const int T = a.a_stats_tiles;
   const float cnt = (float)a.K / (float)T;
   for (int m = wave; m < a.M; m += nw) {
+    // up to 4 segments per lane, loaded together (T <= 256)
+    float2 st[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int t = lane + 64 * q;
+      st[q] = a.a_stats[(size_t)(t < T ? t : 0) * a.M + m];
+    }
     float sm = 0.0f;
-    for (int t = lane; t < T; t += 64) sm += a.a_stats[(size_t)t * a.M + m].x;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sm += lane + 64 * q < T ? st[q].x : 0.0f;
     const float mean = wave_sum(sm) / (float)T;
     float m2 = 0.0f;
-    for (int t = lane; t < T; t += 64) {
-      const float2 st = a.a_stats[(size_t)t * a.M + m];
-      const float d = st.x - mean;
-      m2 += st.y + cnt * d * d;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float d = st[q].x - mean;
+      m2 += lane + 64 * q < T ? st[q].y + cnt * d * d : 0.0f;
     }
     m2 = wave_sum(m2);
     float mu, sc;
@@ -435,11 +443,24 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     if (tid == 0) s_last = (counter_add(&a.counters[t], 1) == a.splits - 1);
     __syncthreads();
     if (!s_last) return;
+    // splits summed in split order; 8 loads in flight per group (indices past
+    // the last split read split 0 and are masked out)
     const float* src = a.partial + (size_t)t * kTileN;
     for (int i = tid; i < a.M * kTileN; i += blockDim.x) {
       const int m = i / kTileN, c = i - m * kTileN;
+      const float* p = src + (size_t)m * ld + c;
+      const size_t sstride = (size_t)a.M * ld;
       float v = 0.0f;
-      for (int sp = 0; sp < a.splits; ++sp) v += load_coherent(src + ((size_t)sp * a.M + m) * ld + c);
+      for (int sp0 = 0; sp0 < a.splits; sp0 += 8) {
+        float part[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int sp = sp0 + q < a.splits ? sp0 + q : 0;
+          part[q] = load_coherent(p + sp * sstride);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v += sp0 + q < a.splits ? part[q] : 0.0f;
+      }
       red[m * kRedStride + c] = v;
     }
     if (tid == 0) counter_reset(&a.counters[t]);
@@ -453,13 +474,14 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
   else epi_head(a, t, red);
 }
 
-// Activations enter as bf16 hi + lo pairs while the MFMA work stays far below
-// what the weight stream leaves room for (up to 3 row tiles); larger blocks
-// (4..9 row tiles, up to 144 rows) run the 9-tile kernel with single rounding.
+// Activations enter as bf16 hi + lo pairs (two MFMAs per weight tile) at
+// every block size: a single bf16 rounding of the activations loses about
+// three decimal digits per layer, which compounds over a deep target; at 144
+// rows the doubled MFMA work still stays under the weight-stream time.
 template <int MT, int EPI, int NORM>
 hipError_t launch_mt(const GemmArgs& a, hipStream_t s) {
   constexpr int U = MT == 1 ? 4 : (MT <= 3 ? 2 : 1);
-  constexpr bool SPLIT = MT <= 3;
+  constexpr bool SPLIT = true;
   hipLaunchKernelGGL((gemm_kernel<MT, U, EPI, SPLIT, NORM>), dim3(a.n_tiles * a.splits),
                      dim3(256), 0, s, a);
   return hipGetLastError();

@@ -98,8 +98,8 @@ hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
 // ---------------------------------------------------------------------------
 // verify attention
 // ---------------------------------------------------------------------------
-constexpr int kAttnChunk = 256;       // keys per workgroup (64 per wave)
-constexpr int kMaxAttnChunks = 128;   // cache capacity <= 32768 positions
+constexpr int kMaxAttnSpans = 512;    // key spans per (sequence, kv head)
+constexpr int kMaxCapacity = 32768;   // cache positions
 
 struct AttnArgs {
   const float* q;           // fp32 [M][H][hd] (rotated)
@@ -108,9 +108,10 @@ struct AttnArgs {
   const int32_t* len;
   uint32_t* status;
   float* out;               // fp32 [M][H*hd]
-  float* part_o;            // [batch][Hkv][max_chunks][Qn][hd]
-  float* part_ml;           // [batch][Hkv][max_chunks][Qn][2] (max, sum exp)
-  int32_t batch, n_heads, n_kv_heads, capacity, n_slots, max_chunks;
+  float* part_o;            // [batch][Hkv][max_spans][Qn][hd]
+  float* part_ml;           // [batch][Hkv][max_spans][Qn][2] (max, sum exp)
+  int32_t batch, n_heads, n_kv_heads, capacity, n_slots;
+  int32_t span, max_spans;  // keys per wave (multiple of 64), spans per sequence
   float scale;
   Topo topo;
 };

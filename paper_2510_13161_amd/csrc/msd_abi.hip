@@ -88,7 +88,7 @@ struct Layout {
   size_t x, stats, q, attn, act, partial, counters, part_o, part_ml, tile_ms, tile_top, total;
   int64_t n_counters;
   int32_t attn_counter_off;  // in int32 units inside counters
-  int32_t max_chunks;
+  int32_t span, max_spans;
 };
 
 Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacity) {
@@ -121,9 +121,15 @@ Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacit
   L.attn_counter_off = max_tiles;
   L.n_counters = (int64_t)max_tiles + (int64_t)batch * c.n_kv_heads;
   L.counters = take((size_t)L.n_counters * sizeof(int32_t));
-  L.max_chunks = (capacity + kAttnChunk - 1) / kAttnChunk;
+  // attention: keys per wave, doubled from 64 until the (sequence, kv head,
+  // span) items stop exceeding ~2K waves
+  L.span = 64;
+  while ((int64_t)batch * c.n_kv_heads * ((capacity + L.span - 1) / L.span) > 2048 &&
+         L.span < kMaxCapacity)
+    L.span *= 2;
+  L.max_spans = (capacity + L.span - 1) / L.span;
   const size_t qn = (size_t)(c.n_heads / c.n_kv_heads) * n_slots;
-  const size_t nparts = (size_t)batch * c.n_kv_heads * L.max_chunks * qn;
+  const size_t nparts = (size_t)batch * c.n_kv_heads * L.max_spans * qn;
   L.part_o = take(nparts * c.head_dim * sizeof(float));
   L.part_ml = take(nparts * sizeof(float2));
   L.tile_ms = take((size_t)s.head.n_tiles * M * sizeof(float2));
@@ -388,7 +394,7 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
   if (kv->capacity < blk->n_slots) return fail(MSD_ERR_CAPACITY, "cache capacity below n_slots");
   const msd_model_config& c = m->cfg;
   if (kv->capacity > c.max_positions) return fail(MSD_ERR_CAPACITY, "cache capacity exceeds max_positions");
-  if (kv->capacity > kMaxAttnChunks * kAttnChunk) return fail(MSD_ERR_CAPACITY, "cache capacity above 32768");
+  if (kv->capacity > kMaxCapacity) return fail(MSD_ERR_CAPACITY, "cache capacity above 32768");
   int kappa = 1;
   if (ee) {
     if (ee->layer < 1 || ee->layer > c.n_layers - 1) return fail(MSD_ERR_INVALID_ARG, "early-exit layer out of [1, n_layers-1]");
@@ -479,7 +485,8 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
     aa.n_kv_heads = c.n_kv_heads;
     aa.capacity = kv->capacity;
     aa.n_slots = blk->n_slots;
-    aa.max_chunks = L.max_chunks;
+    aa.span = L.span;
+    aa.max_spans = L.max_spans;
     aa.scale = 1.0f / std::sqrt((float)c.head_dim);
     aa.topo = topo;
     MSD_HIP(prof_mark(m, MSD_K_ATTN, l, true, stream));

@@ -61,15 +61,26 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
     for (int q = threadIdx.x; q < (a.d >> 3); q += blockDim.x) {
       const int ks = q >> 2, lane = (tok & 15) + 16 * (q & 3);
       const u32x4 w = *reinterpret_cast<const u32x4*>(grp + (size_t)ks * 512 + lane * 8);
+      u32x4 pw = {0u, 0u, 0u, 0u};
+      if (p) pw = *reinterpret_cast<const u32x4*>(p + q * 8);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int k = q * 8 + 2 * i;
-        x[k] = bf_lo(w[i]) + (p ? bf2f(p[k]) : 0.0f);
-        x[k + 1] = bf_hi(w[i]) + (p ? bf2f(p[k + 1]) : 0.0f);
+        x[k] = bf_lo(w[i]) + bf_lo(pw[i]);
+        x[k + 1] = bf_hi(w[i]) + bf_hi(pw[i]);
       }
     }
   } else {
-    for (int k = threadIdx.x; k < a.d; k += blockDim.x) x[k] = bf2f(e[k]) + (p ? bf2f(p[k]) : 0.0f);
+    for (int q = threadIdx.x; q < (a.d >> 3); q += blockDim.x) {
+      const u32x4 w = *reinterpret_cast<const u32x4*>(e + q * 8);
+      u32x4 pw = {0u, 0u, 0u, 0u};
+      if (p) pw = *reinterpret_cast<const u32x4*>(p + q * 8);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        x[q * 8 + 2 * i] = bf_lo(w[i]) + bf_lo(pw[i]);
+        x[q * 8 + 2 * i + 1] = bf_hi(w[i]) + bf_hi(pw[i]);
+      }
+    }
   }
   __syncthreads();
   row_stats(x, a.d, a.stats + m, sh);
@@ -89,7 +100,9 @@ __device__ __forceinline__ float2 ms_merge(float2 a, float2 b) {
 }
 
 // One workgroup per row: merge the per-tile (max, sum exp) pairs and top-kappa
-// lists produced by the LM-head GEMM epilogue.
+// lists produced by the LM-head GEMM epilogue. KB bounds kappa at compile
+// time so a tile's keys load together; tiles go four at a time.
+template <int KB>
 __global__ __launch_bounds__(256) void head_merge_kernel(HeadMergeArgs a) {
   extern __shared__ uint64_t lists[];  // [256][kappa]
   __shared__ float2 sh_ms[4];
@@ -100,18 +113,34 @@ __global__ __launch_bounds__(256) void head_merge_kernel(HeadMergeArgs a) {
   for (int r = 0; r < K; ++r) mine[r] = 0ull;
 
   float2 acc = make_float2(-INFINITY, 0.0f);
-  for (int t = tid; t < a.n_tiles; t += blockDim.x) {
-    acc = ms_merge(acc, a.tile_ms[(size_t)t * a.M + m]);
-    const uint64_t* top = a.tile_top + ((size_t)t * a.M + m) * K;
-    for (int r = 0; r < K; ++r) {
-      const uint64_t key = top[r];
-      if (key <= mine[K - 1]) break;  // tile lists are sorted, descending
-      int j = K - 1;
-      while (j > 0 && mine[j - 1] < key) {
-        mine[j] = mine[j - 1];
-        --j;
+  for (int t0 = tid; t0 < a.n_tiles; t0 += 4 * blockDim.x) {
+    float2 ms[4];
+    uint64_t keys[4][KB];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int t = t0 + u * blockDim.x;
+      const int tc = t < a.n_tiles ? t : 0;
+      ms[u] = a.tile_ms[(size_t)tc * a.M + m];
+      const uint64_t* top = a.tile_top + ((size_t)tc * a.M + m) * K;
+#pragma unroll
+      for (int r = 0; r < KB; ++r) keys[u][r] = top[r < K ? r : 0];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (t0 + u * blockDim.x >= a.n_tiles) break;
+      acc = ms_merge(acc, ms[u]);
+#pragma unroll
+      for (int r = 0; r < KB; ++r) {
+        if (r >= K) break;
+        const uint64_t key = keys[u][r];
+        if (key <= mine[K - 1]) break;  // tile lists are sorted, descending
+        int j = K - 1;
+        while (j > 0 && mine[j - 1] < key) {
+          mine[j] = mine[j - 1];
+          --j;
+        }
+        mine[j] = key;
       }
-      mine[j] = key;
     }
   }
   // fixed-order reduction of the (max, sum) pairs
@@ -178,7 +207,9 @@ hipError_t launch_row_stats(const float* x, int M, int d, float2* stats, hipStre
 
 hipError_t launch_head_merge(const HeadMergeArgs& a, hipStream_t s) {
   const size_t shmem = (size_t)256 * a.kappa * sizeof(uint64_t);
-  hipLaunchKernelGGL(head_merge_kernel, dim3(a.M), dim3(256), shmem, s, a);
+  if (a.kappa <= 1) hipLaunchKernelGGL(head_merge_kernel<1>, dim3(a.M), dim3(256), shmem, s, a);
+  else if (a.kappa <= 8) hipLaunchKernelGGL(head_merge_kernel<8>, dim3(a.M), dim3(256), shmem, s, a);
+  else hipLaunchKernelGGL(head_merge_kernel<32>, dim3(a.M), dim3(256), shmem, s, a);
   return hipGetLastError();
 }
 

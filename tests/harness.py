@@ -170,3 +170,18 @@ def margins(z: np.ndarray, k: int) -> np.ndarray:
     """Smallest gap among the k+1 largest logits of each row."""
     part = -np.sort(-z, axis=-1)[..., :k + 1]
     return np.min(part[..., :-1] - part[..., 1:], axis=-1)
+
+
+def streaming_oracle(shape, seed: int) -> orc.Oracle:
+    """Oracle whose layer weights are regenerated on the host layer by layer."""
+    glob = synth.host_weights(shape, seed, layers=[], with_globals=True)
+    src = lambda l: synth.host_weights(shape, seed, layers=[l], with_globals=False)
+    return orc.Oracle(shape, glob, layer_source=src)
+
+
+def chain_inputs(si: synth.StepInputs, b: int, slots) -> synth.StepInputs:
+    """The root-to-node chain through `slots` of sequence b as its own block."""
+    slots = list(slots)
+    toks = si.tokens[b, slots][None].astype(np.int32)
+    par = np.arange(-1, len(slots) - 1, dtype=np.int32)
+    return synth.StepInputs(parent=par, tokens=toks, ctx_len=si.ctx_len[b:b + 1].copy())

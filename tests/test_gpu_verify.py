@@ -168,3 +168,85 @@ def test_step_is_deterministic(tiny_case):
     assert np.array_equal(a.logits, b.logits)
     assert np.array_equal(a.ee_logp, b.ee_logp)
     assert np.array_equal(a.k_rows[0], b.k_rows[0])
+
+
+# ---------------------------------------------------------------------------
+# full-depth workloads (the shapes the benchmark times)
+# ---------------------------------------------------------------------------
+def _free(case):
+    import torch
+    del case
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.slow
+def test_full_14b_chain_greedy():
+    """14B-shaped, 48 layers, gamma = 8 chain, ctx 1024, early exit kappa 8 at layer 36."""
+    _torch()
+    w = synth.WORKLOADS["14b_chain"]
+    case = H.GpuCase(w)
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0, oracle_obj=H.streaming_oracle(case.shape, w.seed))
+    rep = _compare(case, gr, {0: o})
+    print("14b full chain:", rep)
+    _free(case)
+
+
+@pytest.mark.slow
+def test_full_14b_tree_rejection():
+    """Branch-complete tree (4 x 6), ctx 4096, rejection sampling at T = 1."""
+    _torch()
+    w = synth.WORKLOADS["14b_tree"]
+    case = H.GpuCase(w)
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0, oracle_obj=H.streaming_oracle(case.shape, w.seed))
+    rep = _compare(case, gr, {0: o})
+    print("14b full tree:", rep)
+    _free(case)
+
+
+@pytest.mark.slow
+def test_full_14b_batch16_sampled_sequences():
+    """16 sequences with contexts in [512, 8192] (M = 144): sequences 0 and the
+    longest are recomputed by the oracle one by one; every sequence's commit
+    and status are checked."""
+    _torch()
+    w = synth.WORKLOADS["14b_batch16"]
+    case = H.GpuCase(w)
+    gr = case.run(ee=True)
+    orc_obj = H.streaming_oracle(case.shape, w.seed)
+    picks = sorted({0, int(np.argmax(case.si.ctx_len))})
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b, oracle_obj=orc_obj) for b in picks}
+    rep = _compare(case, gr, seqs)
+    print("14b batch16:", rep)
+    # every sequence: the commit advanced len by 1 + A, paths are valid chains
+    assert np.array_equal(gr.len_after, case.si.ctx_len + 1 + gr.acc_len)
+    for b in range(w.batch):
+        A = gr.acc_len[b]
+        assert np.array_equal(gr.path[b][:A + 1], np.arange(A + 1))
+    _free(case)
+
+
+@pytest.mark.slow
+def test_full_66b_tree_branch():
+    """66B-shaped, 64 layers (LayerNorm, learned positions, ReLU, biases, tied
+    head), tree 4 x 8, ctx 2048. The oracle scores branch 0 as a chain: a
+    depth-r node holds the token at position t + r (tree node == its chain)."""
+    _torch()
+    w = synth.WORKLOADS["66b_tree"]
+    case = H.GpuCase(w)
+    gr = case.run(ee=True)
+    branch = [0] + list(range(1, 1 + w.gamma))
+    ci = H.chain_inputs(case.si, 0, branch)
+    cw = w.with_model(w.model, topology="chain", branches=1)
+    o = H.oracle_sequence(case.shape, cw, ci, 0, oracle_obj=H.streaming_oracle(case.shape, w.seed))
+    err = np.abs(gr.logits[branch] - o.logits).max()
+    print("66b full branch: max abs", err)
+    assert err <= H.TOL_LOGIT
+    tie = H.margins(o.logits, 1) < H.TIE_MARGIN
+    assert np.array_equal(gr.argmax[branch][~tie], np.argmax(o.logits, -1)[~tie])
+    firm = o.ee_margin >= H.TIE_MARGIN
+    assert np.array_equal(gr.ee_ids[branch][firm], o.ee_ids[firm])
+    assert gr.status == 0
+    _free(case)

@@ -69,7 +69,7 @@ def test_head_closed_form_rmsnorm_and_lm_head():
     w = synth.host_weights(TINY1, 1)
     w["l0.wo"] = zeros(256, 256)
     w["l0.w_down"] = zeros(256, 1024)
-    o = orc.Oracle(TINY1, w)
+    o = orc.Oracle(TINY1, w, kv_cache_bf16=False)
     tok = np.array([3, 4000, 17])
     r = o.forward(tok, np.array([0, 1, 2]), np.array([-1, 0, 1]))
     e = f64(w["embed"])[tok]
@@ -84,10 +84,27 @@ def test_single_row_over_empty_cache_returns_its_value():
     w["l0.wv"] = eye(256, 256)
     w["l0.wo"] = eye(256, 256)
     w["l0.w_down"] = zeros(256, 1024)
-    o = orc.Oracle(TINY1, w)
+    o = orc.Oracle(TINY1, w, kv_cache_bf16=False)
     r = o.forward(np.array([99]), np.array([7]), np.array([-1]))
     e = f64(w["embed"])[[99]]
     assert np.max(np.abs(r.x_final - (e + rms(e)))) < 1e-14
+
+
+def test_block_keys_values_are_stored_in_the_cache_format():
+    """With the cache-format reading the single row's value is the bf16
+    rounding (nearest 8-bit significand, ties to even) of W_v h."""
+    w = synth.host_weights(TINY1, 2)
+    w["l0.wv"] = eye(256, 256)
+    w["l0.wo"] = eye(256, 256)
+    w["l0.w_down"] = zeros(256, 1024)
+    o = orc.Oracle(TINY1, w, kv_cache_bf16=True)
+    r = o.forward(np.array([99]), np.array([7]), np.array([-1]))
+    e = f64(w["embed"])[[99]]
+    want = e + f64(b16(rms(e)))
+    # one bf16 ulp of slack for a float32 tie met on the way to bf16
+    assert np.all(np.abs(r.x_final - want) <= 2.0 ** -8 * np.abs(rms(e)))
+    assert np.array_equal(r.blk_v[0].reshape(-1), f64(b16(rms(e))).reshape(-1)) or \
+        np.max(np.abs(r.blk_v[0].reshape(-1) - rms(e).reshape(-1))) <= 2.0 ** -8 * np.abs(rms(e)).max()
 
 
 def test_uniform_attention_pins_tree_mask_and_gqa_grouping():
@@ -100,7 +117,7 @@ def test_uniform_attention_pins_tree_mask_and_gqa_grouping():
     w["l0.wv"] = eye(128, 256)
     w["l0.wo"] = eye(256, 256)
     w["l0.w_down"] = zeros(256, 1024)
-    o = orc.Oracle(m, w)
+    o = orc.Oracle(m, w, kv_cache_bf16=False)
     n_ctx = 5
     ctx = ctx_fn(m, 3, n_ctx)
     parent = np.array([-1, 0, 1, 0, 3])          # two branches of depth 2
@@ -139,7 +156,7 @@ def test_rotary_causal_attention_matches_library_sdpa():
     for n in ("wq", "wk", "wv", "wo"):
         w["l0." + n] = eye(256, 256)
     w["l0.w_down"] = zeros(256, 1024)
-    o = orc.Oracle(TINY1, w)
+    o = orc.Oracle(TINY1, w, kv_cache_bf16=False)
     tok = np.array([10, 20, 30, 40])
     pos = np.array([5, 6, 7, 8])
     r = o.forward(tok, pos, np.array([-1, 0, 1, 2]))
@@ -163,7 +180,7 @@ def test_swiglu_closed_form():
     w["l0.w_gate"] = eye(1024, 256)
     w["l0.w_up"] = eye(1024, 256)
     w["l0.w_down"] = eye(256, 1024)
-    o = orc.Oracle(TINY1, w)
+    o = orc.Oracle(TINY1, w, kv_cache_bf16=False)
     r = o.forward(np.array([8, 9]), np.array([0, 1]), np.array([-1, 0]))
     e = f64(w["embed"])[[8, 9]]
     h = torch.from_numpy(rms(e))
@@ -182,7 +199,7 @@ def test_layernorm_learned_positions_relu_biases_tied_head():
     w["l0.wo"] = zeros(256, 256)
     w["l0.w_up"] = eye(1024, 256)
     w["l0.w_down"] = eye(256, 1024)
-    o = orc.Oracle(m, w)
+    o = orc.Oracle(m, w, kv_cache_bf16=False)
     tok, pos = np.array([5, 6, 7]), np.array([30, 31, 32])
     r = o.forward(tok, pos, np.array([-1, 0, 1]))
     x1 = f64(w["embed"])[tok] + f64(w["pos_embed"])[pos] + f64(w["l0.bo"])
@@ -250,8 +267,9 @@ def test_tree_node_equals_its_root_to_node_chain(tiny):
 
 def test_rope_relative_position_invariance(tiny):
     """Rotary positions encode offsets only: shifting a block over an empty cache
-    leaves its logits unchanged up to rounding."""
-    o, _ = tiny
+    leaves its logits unchanged up to fp64 rounding (keys kept at fp64: bf16
+    storage of a rotated key depends on its absolute angle)."""
+    o = orc.Oracle(TINY, tiny[1], kv_cache_bf16=False)
     tok = np.array([11, 22, 33, 44, 55])
     par = np.arange(-1, 4)
     a = o.forward(tok, np.arange(5), par)
