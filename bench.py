@@ -10,9 +10,13 @@ tokens), resident in HBM before the timed region.
 
 Prints ONE JSON line: verified draft tokens/s (the metric), ms per step, the
 roofline of the dominant kernel (the FFN up-projection GEMM, timed with HIP
-events around each of its launches in a second, instrumented pass over the
-same number of steps) and the fp64 oracle's throughput on the host cores
-over a bounded sample of the same step.
+events that the library records on its own stream around each of its
+launches inside the timed region), the time from the start of a step to the
+early-exit message, and the fp64 oracle's throughput on the host cores over
+one whole step of sequence 0.
+
+``--copy-calibration BYTES`` instead times a plain device-to-device copy of
+BYTES bytes (the reference kernel that scales the HBM traffic counters).
 """
 from __future__ import annotations
 
@@ -33,10 +37,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="14b_chain")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-profile-pass", action="store_true",
-                    help="skip the instrumented pass (rocprofv3 runs)")
-    ap.add_argument("--cpu-layers", type=int, default=2,
-                    help="decoder layers the oracle times for the CPU baseline sample")
+    ap.add_argument("--no-kernel-events", action="store_true",
+                    help="time the steps without the per-launch HIP events")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
     return ap.parse_args()
 
 
@@ -62,9 +65,31 @@ def ffn_up_bytes(shape, M: int) -> int:
     return n_mats * shape.d_ffn * shape.d_model * 2 + M * shape.d_model * 2 + M * shape.d_ffn * 2
 
 
-def cpu_baseline(shape, w, layers: int) -> dict:
-    """The fp64 oracle on the host: embed + `layers` decoder layers + both heads
-    of sequence 0, scaled to the full depth (the layers are identical in cost)."""
+def measured_traffic():
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary, or None once the GEMM source
+    has changed since those counters were taken."""
+    import hashlib
+    import re
+    root = os.path.dirname(os.path.abspath(__file__))
+    prof = os.path.join(root, "profiles", "ffn_up_gemm_14b_chain_traffic.md")
+    src = os.path.join(root, "paper_2510_13161_amd", "csrc", "gemm.hip")
+    try:
+        text = open(prof).read()
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except OSError:
+        return None
+    m = re.search(r"gemm_source_sha256_16: ([0-9a-f]{16}); traffic_bytes_per_launch: (\d+)", text)
+    if not m or m.group(1) != sha:
+        return None
+    return int(m.group(2))
+
+
+def cpu_baseline(shape, w) -> dict:
+    """The fp64 oracle on the host over one whole verification step of
+    sequence 0: embed, every decoder layer, the early-exit and final heads,
+    top-kappa and acceptance. Layer weights are generated just before their
+    layer runs and dropped after it (only the oracle calls are timed)."""
     import numpy as np
     import oracle as orc
     from paper_2510_13161_amd import synth
@@ -72,32 +97,56 @@ def cpu_baseline(shape, w, layers: int) -> dict:
         orc.build()
     si = synth.step_inputs(w)
     L = int(si.ctx_len[0])
-    sub = shape.with_layers(layers)
-    weights = synth.host_weights(sub, w.seed)
-    o = orc.Oracle(sub, weights)
-    ctx = [(synth.host_ctx(shape, w.seed, l, "k", 0, L), synth.host_ctx(shape, w.seed, l, "v", 0, L))
-           for l in range(layers)]
+    glob = synth.host_weights(shape, w.seed, layers=[], with_globals=True)
+    o = orc.Oracle(shape, glob)
     pos = L + orc.depths(si.parent)
+    timed = 0.0
     t0 = time.perf_counter()
     x = o.embed(si.tokens[0], pos)
-    t1 = time.perf_counter()
-    for l in range(layers):
-        o.layer(l, x, pos, si.parent, ctx[l][0], ctx[l][1], L)
-    t2 = time.perf_counter()
+    timed += time.perf_counter() - t0
+    for l in range(shape.n_layers):
+        lw = synth.host_weights(shape, w.seed, layers=[l], with_globals=False)
+        ck = synth.host_ctx(shape, w.seed, l, "k", 0, L)
+        cv = synth.host_ctx(shape, w.seed, l, "v", 0, L)
+        o.layer_source = lambda _l, lw=lw: lw
+        t0 = time.perf_counter()
+        o.layer(l, x, pos, si.parent, ck, cv, L)
+        if l + 1 == w.ee_layer:
+            orc.Oracle.topk(o.head(x), w.kappa)
+        timed += time.perf_counter() - t0
+        del lw
+    t0 = time.perf_counter()
     z = o.head(x)
-    ids, logp, _ = orc.Oracle.topk(z, w.kappa)
-    t3 = time.perf_counter()
     o.accept(si.parent, si.tokens[0], z)
-    t4 = time.perf_counter()
-    t_step = (t1 - t0) + (t2 - t1) * shape.n_layers / layers + 2 * (t3 - t2) + (t4 - t3)
+    timed += time.perf_counter() - t0
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     per_seq_tokens = w.n_slots - 1
-    return {"value": per_seq_tokens / t_step, "unit": "verified tokens/s", "cores": threads,
+    return {"value": round(per_seq_tokens / timed, 4), "unit": "verified tokens/s", "cores": threads,
             "kind": "oracle",
-            "sample": (f"sequence 0 of workload {w.name}: embed + {layers} of {shape.n_layers} "
-                       f"decoder layers + one head pass (timed {t4 - t0:.2f} s), layer time x "
-                       f"{shape.n_layers}/{layers}, head x2; fp64 C oracle, OpenMP"),
-            "s_per_step": t_step}
+            "sample": (f"one whole step of sequence 0 of {w.name} ({per_seq_tokens} draft tokens): "
+                       f"embed, {shape.n_layers} decoder layers, early-exit and final heads, "
+                       f"top-{w.kappa}, acceptance; fp64 C oracle, OpenMP; {timed:.1f} s of "
+                       "oracle time (weight generation untimed)")}
+
+
+def copy_calibration(nbytes: int) -> None:
+    """A plain HBM copy of known size: its FETCH_SIZE / WRITE_SIZE counters
+    against nbytes give the factor that turns those counters into bytes."""
+    import torch
+    n = nbytes // 4
+    a = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    print(json.dumps({"copy_bytes": 4 * n, "ms": round(ms, 4),
+                      "read_plus_write_gbs": round(8 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
 def main():
@@ -113,11 +162,14 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     w = synth.WORKLOADS[args.workload]
     shape = w.model
     si = synth.step_inputs(w)
     dev = "cuda"
-    total_steps = args.warmup + args.steps * (1 if args.no_profile_pass else 2)
+    total_steps = args.warmup + args.steps
     capacity = int(-(-(int(si.ctx_len.max()) + w.n_slots + total_steps + 8) // 64) * 64)
 
     t0 = time.perf_counter()
@@ -140,6 +192,7 @@ def main():
     lse = torch.empty(M, dtype=torch.float32, device=dev)
     ids = torch.empty((M, w.kappa), dtype=torch.int32, device=dev)
     logp = torch.empty((M, w.kappa), dtype=torch.float32, device=dev)
+    ee_ready = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ee = msd.EERequest(w.ee_layer, w.kappa, ids.data_ptr(), logp.data_ptr(), None)
     ws = torch.empty(msd.workspace_bytes(model.handle, B, n, w.kappa, capacity), dtype=torch.uint8,
                      device=dev)
@@ -162,43 +215,52 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+
+    # HIP events: the library records begin/end around every FFN up-projection
+    # launch on the stream it launches on (one event pair per layer and step),
+    # and the early-exit message's ready event; the step starts are recorded
+    # on the same (current) stream.
+    L = shape.n_layers
+    events = not args.no_kernel_events
+    if events:
+        evb = [[torch.cuda.Event(enable_timing=True) for _ in range(L)] for _ in range(args.steps)]
+        eve = [[torch.cuda.Event(enable_timing=True) for _ in range(L)] for _ in range(args.steps)]
+        starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        for e in [x for r in evb + eve for x in r] + starts + ee_ready:
+            e.record()
+        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record()
-    for _ in range(args.steps):
+    for k in range(args.steps):
+        if events:
+            msd.set_profile(model.handle, msd.MSD_K_FFN_UP, [e.cuda_event for e in evb[k]],
+                            [e.cuda_event for e in eve[k]])
+            ee.ready = ee_ready[k].cuda_event
+            starts[k].record()
         step()
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
+    msd.set_profile(model.handle, msd.MSD_K_FFN_UP, [], [])
+    ee.ready = None
     status = int(cache.status.item())
     if status != 0:
         print(f"bench.py: device status {status}", file=sys.stderr)
         sys.exit(1)
 
-    # second pass: HIP events around each FFN up-projection launch
-    roof = None
-    if not args.no_profile_pass:
-        evb = [torch.cuda.Event(enable_timing=True) for _ in range(shape.n_layers)]
-        eve = [torch.cuda.Event(enable_timing=True) for _ in range(shape.n_layers)]
-        for e in evb + eve:
-            e.record()
-        torch.cuda.synchronize()
-        msd.set_profile(model.handle, msd.MSD_K_FFN_UP, [e.cuda_event for e in evb],
-                        [e.cuda_event for e in eve])
-        dur = []
-        for _ in range(args.steps):
-            step()
-            torch.cuda.synchronize()
-            dur += [b.elapsed_time(e) for b, e in zip(evb, eve)]
-        msd.set_profile(model.handle, msd.MSD_K_FFN_UP, [], [])
+    roof, t_ee = None, None
+    if events:
+        dur = [b.elapsed_time(e) for rb, re_ in zip(evb, eve) for b, e in zip(rb, re_)]
         avg_ms = float(np.mean(dur))
         per_launch = ffn_up_bytes(shape, M)
         achieved = per_launch / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                 "kernel": "gemm_kernel<EPI_SWIGLU> (FFN gate+up projection)",
                 "bytes_per_launch": per_launch, "avg_launch_us": round(avg_ms * 1e3, 2),
                 "launches": len(dur)}
+        t_ee = float(np.median([s_.elapsed_time(r) for s_, r in zip(starts, ee_ready)]))
 
     ctx_mean = float(si.ctx_len.mean()) + (args.warmup + args.steps)  # len grows by 1 per step
     sb = step_bytes(shape, w, ctx_mean)
@@ -209,19 +271,20 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded random-init weights, random cached K/V and draft tokens)",
-        "config": {"workload": w.name, "model": shape.name, "n_layers": shape.n_layers,
-                   "d_model": shape.d_model, "batch": w.batch, "n_slots": n,
+        "config": {"workload": w.name,
+                   "shape": (f"{shape.n_layers}L d{shape.d_model} {shape.n_heads}/{shape.n_kv_heads}"
+                             f"x{shape.head_dim} F{shape.d_ffn} V{shape.vocab}"),
+                   "batch": w.batch, "n_slots": n,
                    "topology": w.topology, "ctx": list(w.ctx), "ee_layer": w.ee_layer,
                    "kappa": w.kappa, "acceptance": w.mode},
         "step_bytes": sb["total"], "step_hbm_gbs": round(step_gbs, 1),
         "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
         "roofline": roof,
+        "ms_to_early_exit": None if t_ee is None else round(t_ee, 4),
         "setup_s": round(t_setup, 2),
     }
     if not args.no_cpu_baseline:
-        cb = cpu_baseline(shape, w, args.cpu_layers)
-        cb.pop("s_per_step")
-        out["cpu_baseline"] = cb
+        out["cpu_baseline"] = cpu_baseline(shape, w)
     print(json.dumps(out), flush=True)
 
 

@@ -17,7 +17,7 @@ struct msd_model {
   msd_model_config cfg;
   std::vector<const uint16_t*> t;  // MSD_N_TENSORS(n_layers) entries
   float2* rope = nullptr;          // [max_positions][head_dim/2] (cos, sin)
-  int32_t target_wgs = 512;        // split-K sizing target
+  int32_t target_wgs = 384;        // split-K sizing target
   int32_t weights_nt = 0;          // non-temporal weight loads
   int32_t prof_class = -1;         // instrumentation (msd_set_profile)
   std::vector<hipEvent_t> prof_begin, prof_end;
