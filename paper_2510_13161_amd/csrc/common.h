@@ -198,6 +198,47 @@ __device__ __forceinline__ void counter_reset(int32_t* c) {
   __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// 8-byte variants of the coherent hand-off accesses (two floats at a time).
+__device__ __forceinline__ void store_coherent2(float* p, float a, float b) {
+  const uint64_t v = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 load_coherent2(const float* p) {
+  const uint64_t v = __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<float*>(p)),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+}
+
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+// Pairwise combination of (count, mean, M2) summaries (Chan, Golub & LeVeque):
+// n = na + nb, d = mb - ma, mean = ma + d nb / n, M2 = M2a + M2b + d^2 na nb / n.
+__device__ __forceinline__ void chan_combine(float& n, float& mean, float& m2, float nb, float mb,
+                                             float m2b) {
+  const float nt = n + nb;
+  if (nt <= 0.0f) return;
+  const float d = mb - mean;
+  mean += d * (nb / nt);
+  m2 += m2b + d * d * (n * nb / nt);
+  n = nt;
+}
+
+// Activation image: the split-bf16 MFMA operand form of an activation matrix
+// [M][K] (M padded to 16 MT rows). Element order [K/32][MT][2][64][8]: k-step
+// ks, row tile mt, part (0 = hi, 1 = lo), lane l = row 16 mt + l%16 and
+// columns 32 ks + 8 (l/16) .. +8. One k-step of one row tile is 1 KB of hi and
+// 1 KB of lo: exactly the B operand of one MFMA 16x16x32 per part. Rows past
+// M are zero.
+__device__ __forceinline__ size_t img_offset(int ks, int mt, int MT, int lane) {
+  return ((size_t)(ks * MT + mt) * 2) * 512 + (size_t)lane * 8;
+}
+// Eight values as the hi and lo words of one image lane.
+__device__ __forceinline__ void split8_words(const float (&v)[8], u32x4& h, u32x4& l) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    h[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
+    l[i] = pack_bf16x2(v[2 * i] - bf_lo(h[i]), v[2 * i + 1] - bf_hi(h[i]));
+  }
+}
 
 }  // namespace msd

@@ -1,38 +1,37 @@
-// Skinny weight-streaming GEMM for the verification pass: Y = A W^T with
-// A = the block's rows (M = batch * n_slots <= 144, fp32 activations) and W a
-// bf16 weight matrix [N][K] read exactly once. This is where the verify step
-// spends its bytes: every projection of every layer plus the two LM-head
-// passes.
+// Skinny weight-streaming GEMM for the verification pass: Y = norm(X) W^T with
+// X = the block's rows (M = batch * n_slots <= 144) and W a bf16 weight
+// matrix [N][K] read exactly once. This is where the verify step spends its
+// bytes: every projection of every layer plus the two LM-head passes.
 //
 // Mapping (gfx950, wave64, MFMA 16x16x32 bf16 -> fp32):
-//  * a workgroup (4 waves) owns a 64-column output tile and a contiguous
-//    slice of K (split-K over `splits` workgroups per tile);
-//  * inside the workgroup the slice is cut in 4 k-ranges, one per wave; each
-//    wave holds the full 64 columns (4 MFMA column tiles) for MT row tiles;
-//  * weights are stored fragment-major (one 1 KB MFMA B operand after the
-//    other along K, per 16-row group) and streamed straight from HBM into
-//    the MFMA with 16-byte loads, two batches of U k-steps in flight per
-//    wave; the small A operand is L2-resident;
-//  * the pre-norm of the block (RMSNorm or LayerNorm) is applied while A is
-//    loaded, from per-row statistics the producing kernel left behind, and A
-//    enters the MFMA as bf16 hi + lo parts (two MFMAs per weight tile, about
-//    16-bit activations) while that costs nothing against the weight stream;
-//  * the 4 waves' tiles are summed in LDS in a fixed order; with split-K each
-//    workgroup publishes its tile with coherent stores and the last to arrive
-//    sums all splits in split order and runs the epilogue. No floating-point
-//    atomics: results are bit-reproducible.
+//  * a workgroup of NW waves owns a 64-column output tile and one of
+//    `splits` contiguous slices of K; its waves cut the slice in NW k-ranges;
+//  * weights are stored fragment-major (1 KB MFMA operands one after the
+//    other along K, per 16-row group) and each wave keeps D k-steps of them
+//    in flight, straight from HBM into the MFMA;
+//  * the input is an activation image: X (times the pre-norm gain) already
+//    split into bf16 hi + lo parts in MFMA operand order by the kernel that
+//    produced it, so the loop is loads and MFMAs only (two MFMAs per weight
+//    fragment, about 16-bit activations against the exact bf16 weights);
+//  * operands are swapped (D = W X^T): each lane ends with 4 consecutive
+//    output columns of one row, which makes the epilogues vector-friendly;
+//  * the waves' tiles are summed in LDS in a fixed order; with split-K wave 0
+//    publishes the tile with coherent stores and the last workgroup of the
+//    tile to arrive sums all splits in split order. No floating-point
+//    atomics: results are bit-reproducible;
+//  * the row-wise pre-norm is applied after the product (its per-row scale
+//    commutes with W), from (mean, M2) summaries the producer left behind;
+//  * epilogues (residual + statistics, RoPE + KV append, SwiGLU / ReLU, LM
+//    head statistics) write the next GEMM's activation image directly.
 #include "kernels.h"
 
 namespace msd {
 namespace {
 
-constexpr int kRedStride = kTileN + 4;  // LDS row stride (floats), breaks bank aliasing
-
 // Weights live in the fragment-major layout (see repack_kernel): the 16-row
 // group G of a matrix is a contiguous run of K/32 fragments of 1 KB, fragment
-// ks holding rows 16G..16G+15 x columns 32ks..32ks+31 in MFMA B-operand order
-// (lane l: row 16G + l%16, columns 32ks + 8(l/16) .. +8). A wave's four
-// column tiles are therefore four sequential HBM streams.
+// ks holding rows 16G..16G+15 x columns 32ks..32ks+31 in MFMA operand order
+// (lane l: row 16G + l%16, columns 32ks + 8(l/16) .. +8).
 // Returns the lane's pointer into fragment 0 of the group feeding sub-tile j.
 __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t, int j, int lane) {
   const size_t run = (size_t)(a.K >> 5) * 512;  // elements per 16-row group
@@ -64,240 +63,378 @@ __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t,
   return base + (size_t)grp * run + lane * 8;
 }
 
-// ---------------------------------------------------------------------------
-// epilogues: the reduced tile is red[m * kRedStride + c], m < M, c < 64
-// ---------------------------------------------------------------------------
+// Logical output column (index into biases and LayerNorm column sums) of
+// value r of sub-tile j in lane group q of tile t.
+__device__ __forceinline__ int out_col(const GemmArgs& a, int t, int j, int q, int r) {
+  if (a.map == MAP_QKV) {
+    const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
+    const int hh = t / tph, gi = t - hh * tph;
+    const int dim = (j < 2 ? 0 : half) + gi * 32 + 16 * (j & 1) + 4 * q + r;
+    return hh * hd + dim;
+  }
+  if (a.map == MAP_GATEUP) {
+    const int f = 32 * t + 16 * (j & 1) + 4 * q + r;
+    return j < 2 ? f : (a.N >> 1) + f;
+  }
+  return kTileN * t + 16 * j + 4 * q + r;
+}
 
-// x += y (+ bias); also the (mean, M2) of the 64 updated values of every row,
-// from which the next pre-norm is built (Chan et al. pairwise combination).
-__device__ void epi_resid(const GemmArgs& a, int t, const float* red) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const int n = t * kTileN + lane;
-  const bool valid = n < a.N;
-  for (int m = wave; m < a.M; m += nw) {
-    float v = 0.0f;
-    if (valid) {
-      v = red[m * kRedStride + lane];
-      if (a.b0) v += bf2f(a.b0[n]);
-      float* xp = a.x + (size_t)m * a.N + n;
-      v += *xp;
-      *xp = v;
+// Per-row (mu, r) of the pre-norm, for the lane's row 16 mt + l%16: the four
+// lanes of a row each combine a quarter of the producer's 64-column
+// summaries (loads issued together), then the quarters are combined in lane
+// order so that all four lanes hold identical bits.
+template <int MT>
+__device__ void row_norm(const GemmArgs& a, float (&mu)[MT], float (&rs)[MT]) {
+  constexpr int kMaxPer = 40;  // summaries per lane: K <= 40 * 4 * 64 = 10240
+  const int lane = threadIdx.x & 63, q = lane >> 4, r16 = lane & 15;
+  const RowNorm& nm = a.norm;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    mu[mt] = 0.0f;
+    rs[mt] = 1.0f;
+  }
+  if (nm.kind == 0) return;
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = 16 * mt + r16;
+    const int mm = m < a.M ? m : 0;
+    float2 st[kMaxPer];
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+      const int tt = q + 4 * i;
+      st[i] = nm.stats[(size_t)(tt < nm.tiles ? tt : 0) * a.M + mm];
+    }
+    float n = 0.0f, mean = 0.0f, m2 = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i)
+      if (q + 4 * i < nm.tiles) chan_combine(n, mean, m2, (float)kTileN, st[i].x, st[i].y);
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float n2 = __shfl_xor(n, o), mean2 = __shfl_xor(mean, o), m22 = __shfl_xor(m2, o);
+      if (lane & o) {  // combine as (lower lane, higher lane) in both lanes
+        float nn = n2, me = mean2, mm2 = m22;
+        chan_combine(nn, me, mm2, n, mean, m2);
+        n = nn;
+        mean = me;
+        m2 = mm2;
+      } else {
+        chan_combine(n, mean, m2, n2, mean2, m22);
+      }
+    }
+    const float var = m2 / (float)a.K;
+    if (nm.kind == 1) {
+      rs[mt] = 1.0f / sqrtf(var + mean * mean + nm.eps);
+    } else {
+      rs[mt] = 1.0f / sqrtf(var + nm.eps);
+      mu[mt] = mean;
+    }
+  }
+}
+
+// normalised value of an accumulator entry
+__device__ __forceinline__ float normed(const GemmArgs& a, float acc, float mu, float rs, int col) {
+  if (a.norm.kind == 2) return rs * acc - rs * mu * a.norm.col_g[col] + a.norm.col_b[col];
+  return a.norm.kind == 1 ? rs * acc : acc;
+}
+
+// make this wave's LDS writes visible to its own later LDS reads
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+constexpr int kScr = kTileN + 4;  // scratch row stride (floats)
+
+// Image of 32 consecutive columns [c0, c0 + 32) of a 16-row tile held in
+// scratch[16][kScr], times an optional gain, written as image k-step ks.
+__device__ __forceinline__ void scratch_to_image(const float* scr, int c0, const uint16_t* gain,
+                                                 int gcol0, int M, int mt, int MT, int ks,
+                                                 uint16_t* img) {
+  const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
+  const float* src = scr + r16 * kScr + c0 + 8 * q;
+  const float4 v0 = *reinterpret_cast<const float4*>(src);
+  const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
+  float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+  if (gain) {
+    const u32x4 gw = *reinterpret_cast<const u32x4*>(gain + gcol0 + 8 * q);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] *= bf_lo(gw[i]);
+      v[2 * i + 1] *= bf_hi(gw[i]);
+    }
+  }
+  const bool valid = 16 * mt + r16 < M;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = valid ? v[e] : 0.0f;
+  u32x4 h, l;
+  split8_words(v, h, l);
+  uint16_t* dst = img + img_offset(ks, mt, MT, lane);
+  *reinterpret_cast<u32x4*>(dst) = h;
+  *reinterpret_cast<u32x4*>(dst + 512) = l;
+}
+
+// ---------------------------------------------------------------------------
+// epilogues (wave 0 of the finishing workgroup; acc = the whole tile)
+// lane l, value [mt][j][r]: row 16 mt + l%16, column 64 t + 16 j + 4 (l/16) + r
+// ---------------------------------------------------------------------------
+template <int MT>
+__device__ void epi_resid(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4], float* scr) {
+  const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = 16 * mt + r16;
+    const bool valid = m < a.M;
+    const int mm = valid ? m : 0;
+    float v[4][4];
+    float sum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n0 = kTileN * t + 16 * j + 4 * q;
+      float4* xp = reinterpret_cast<float4*>(a.x + (size_t)mm * a.N + n0);
+      const float4 xv = *xp;
+      float bb[4] = {0.f, 0.f, 0.f, 0.f};
+      if (a.b0) {
+        const u32x2 bw = *reinterpret_cast<const u32x2*>(a.b0 + n0);
+        bb[0] = bf_lo(bw[0]);
+        bb[1] = bf_hi(bw[0]);
+        bb[2] = bf_lo(bw[1]);
+        bb[3] = bf_hi(bw[1]);
+      }
+      const float xs[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[j][r] = valid ? xs[r] + (acc[mt][j][r] + bb[r]) : 0.0f;
+        sum += v[j][r];
+      }
+      if (valid) *xp = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
     }
     if (a.stats_out) {
-      const float cnt = (float)min(kTileN, a.N - t * kTileN);
-      const float mean = wave_sum(valid ? v : 0.0f) / cnt;
-      const float dv = valid ? v - mean : 0.0f;
-      const float m2 = wave_sum(dv * dv);
-      if (lane == 0) a.stats_out[(size_t)t * a.M + m] = make_float2(mean, m2);
+      sum += __shfl_xor(sum, 16);
+      sum += __shfl_xor(sum, 32);
+      const float mean = sum * (1.0f / kTileN);
+      float m2 = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float dv = v[j][r] - mean;
+          m2 += dv * dv;
+        }
+      m2 += __shfl_xor(m2, 16);
+      m2 += __shfl_xor(m2, 32);
+      if (q == 0 && valid) a.stats_out[(size_t)t * a.M + m] = make_float2(mean, m2);
+    }
+    if (a.img_out[0].img || a.img_out[1].img) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<float4*>(scr + r16 * kScr + 16 * j + 4 * q) =
+            make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+      wave_lds_sync();
+#pragma unroll
+      for (int o = 0; o < 2; ++o) {
+        if (!a.img_out[o].img) continue;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          scratch_to_image(scr, 32 * h, a.img_out[o].gain, kTileN * t + 32 * h, a.M, mt, a.MT,
+                           2 * t + h, a.img_out[o].img);
+      }
+      wave_lds_sync();
     }
   }
 }
 
-__device__ void epi_swiglu(const GemmArgs& a, int t, const float* red) {
-  const int F = a.N >> 1;
-  for (int i = threadIdx.x; i < a.M * 32; i += blockDim.x) {
-    const int m = i >> 5, c = i & 31;
-    const float g = red[m * kRedStride + c], u = red[m * kRedStride + 32 + c];
-    a.out_f32[(size_t)m * F + t * 32 + c] = silu(g) * u;
+template <int MT>
+__device__ void epi_swiglu(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4], float* scr,
+                           const float (&mu)[MT], const float (&rs)[MT]) {
+  const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
+  for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      float act[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float g = normed(a, acc[mt][j][r], mu[mt], rs[mt], out_col(a, t, j, q, r));
+        const float u = normed(a, acc[mt][j + 2][r], mu[mt], rs[mt], out_col(a, t, j + 2, q, r));
+        act[r] = silu(g) * u;
+      }
+      *reinterpret_cast<float4*>(scr + r16 * kScr + 16 * j + 4 * q) =
+          make_float4(act[0], act[1], act[2], act[3]);
+    }
+    wave_lds_sync();
+    scratch_to_image(scr, 0, nullptr, 0, a.M, mt, a.MT, t, a.act_img);
+    wave_lds_sync();
   }
 }
 
-__device__ void epi_relu(const GemmArgs& a, int t, const float* red) {
-  for (int i = threadIdx.x; i < a.M * kTileN; i += blockDim.x) {
-    const int m = i / kTileN, c = i - m * kTileN, n = t * kTileN + c;
-    if (n >= a.N) continue;
-    float v = red[m * kRedStride + c];
-    if (a.b0) v += bf2f(a.b0[n]);
-    a.out_f32[(size_t)m * a.N + n] = fmaxf(v, 0.0f);
+template <int MT>
+__device__ void epi_relu(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4], float* scr,
+                         const float (&mu)[MT], const float (&rs)[MT]) {
+  const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
+  for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float v[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int col = out_col(a, t, j, q, r);
+        float y = normed(a, acc[mt][j][r], mu[mt], rs[mt], col);
+        if (a.b0) y += bf2f(a.b0[col]);
+        v[r] = fmaxf(y, 0.0f);
+      }
+      *reinterpret_cast<float4*>(scr + r16 * kScr + 16 * j + 4 * q) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      scratch_to_image(scr, 32 * h, nullptr, 0, a.M, mt, a.MT, 2 * t + h, a.act_img);
+    wave_lds_sync();
   }
 }
 
-__device__ void epi_qkv(const GemmArgs& a, int t, const float* red) {
+template <int MT>
+__device__ void epi_qkv(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4],
+                        const float (&mu)[MT], const float (&rs)[MT]) {
+  const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
   const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
   const int H = a.n_heads, Hk = a.n_kv_heads;
   const int hh = t / tph, gi = t - hh * tph;
   const int which = hh < H ? 0 : (hh < H + Hk ? 1 : 2);
   const int hloc = hh - (which == 0 ? 0 : (which == 1 ? H : H + Hk));
   const uint16_t* bias = which == 0 ? a.b0 : (which == 1 ? a.b1 : a.b2);
-  for (int i = threadIdx.x; i < a.M * 32; i += blockDim.x) {
-    const int m = i >> 5, p = i & 31;
-    const int col_lo = gi * 32 + p, col_hi = half + gi * 32 + p;
-    float lo = red[m * kRedStride + p], hi = red[m * kRedStride + 32 + p];
-    if (bias) {
-      lo += bf2f(bias[hloc * hd + col_lo]);
-      hi += bf2f(bias[hloc * hd + col_hi]);
-    }
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = 16 * mt + r16;
+    if (m >= a.M) continue;
     const int b = m / a.n_slots, slot = m - b * a.n_slots;
     const int L = a.len[b];
     if (L + a.n_slots > a.capacity) {
-      if (p == 0) atomicOr(a.status, 1u);
+      if (q == 0 && slot == 0) atomicOr(a.status, 1u);
       continue;
     }
     const int pos = L + a.depth[slot];
-    if (which < 2 && a.rope) {
-      const float2 cs = a.rope[(size_t)pos * half + col_lo];
-      const float rlo = lo * cs.x - hi * cs.y;
-      const float rhi = hi * cs.x + lo * cs.y;
-      lo = rlo;
-      hi = rhi;
-    }
-    if (which == 0) {
-      float* q = a.out_f32 + ((size_t)m * H + hloc) * hd;
-      q[col_lo] = lo;
-      q[col_hi] = hi;
-    } else {
-      uint16_t* cache = which == 1 ? a.k_cache : a.v_cache;
-      uint16_t* row = cache + (((size_t)b * Hk + hloc) * a.capacity + L + slot) * hd;
-      row[col_lo] = f2bf(lo);
-      row[col_hi] = f2bf(hi);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int dlo = gi * 32 + 16 * j + 4 * q, dhi = half + dlo;
+      float lo[4], hi[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        lo[r] = normed(a, acc[mt][j][r], mu[mt], rs[mt], hh * hd + dlo + r);
+        hi[r] = normed(a, acc[mt][j + 2][r], mu[mt], rs[mt], hh * hd + dhi + r);
+        if (bias) {
+          lo[r] += bf2f(bias[hloc * hd + dlo + r]);
+          hi[r] += bf2f(bias[hloc * hd + dhi + r]);
+        }
+      }
+      if (which < 2 && a.rope) {
+        const float2* cs = a.rope + (size_t)pos * half + dlo;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float2 c = cs[r];
+          const float rl = lo[r] * c.x - hi[r] * c.y;
+          const float rh = hi[r] * c.x + lo[r] * c.y;
+          lo[r] = rl;
+          hi[r] = rh;
+        }
+      }
+      if (which == 0) {
+        float* qp = a.q_out + ((size_t)m * H + hloc) * hd;
+        *reinterpret_cast<float4*>(qp + dlo) = make_float4(lo[0], lo[1], lo[2], lo[3]);
+        *reinterpret_cast<float4*>(qp + dhi) = make_float4(hi[0], hi[1], hi[2], hi[3]);
+      } else {
+        uint16_t* cache = which == 1 ? a.k_cache : a.v_cache;
+        uint16_t* row = cache + (((size_t)b * Hk + hloc) * a.capacity + L + slot) * hd;
+        const u32x2 wl = {pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
+        const u32x2 wh = {pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
+        *reinterpret_cast<u32x2*>(row + dlo) = wl;
+        *reinterpret_cast<u32x2*>(row + dhi) = wh;
+      }
     }
   }
 }
 
 // Per row of the tile: logits out, (max, sum exp), top-kappa rank keys.
-__device__ void epi_head(const GemmArgs& a, int t, const float* red) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const int n = t * kTileN + lane;
-  const bool valid = n < a.N;
-  for (int m = wave; m < a.M; m += nw) {
-    const float v = red[m * kRedStride + lane];
-    if (a.logits && valid) a.logits[(size_t)m * a.N + n] = v;
-    const float mx = wave_max(valid ? v : -INFINITY);
-    const float se = wave_sum(valid ? expf(v - mx) : 0.0f);
-    if (lane == 0) a.tile_ms[(size_t)t * a.M + m] = make_float2(mx, se);
-    uint64_t key = valid ? rank_key(v, n) : 0ull;
-    uint64_t* top = a.tile_top + ((size_t)t * a.M + m) * a.kappa;
-    for (int r = 0; r < a.kappa; ++r) {
-      const uint64_t best = wave_max_u64(key);
-      if (key == best) key = 0ull;
-      if (lane == 0) top[r] = best;
+template <int MT>
+__device__ void epi_head(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4],
+                         const float (&mu)[MT], const float (&rs)[MT]) {
+  const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = 16 * mt + r16;
+    const bool valid = m < a.M;
+    float v[4][4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n0 = kTileN * t + 16 * j + 4 * q;
+      const bool cv = kTileN * t + 16 * j < a.N;  // N % 16 == 0: whole groups
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[j][r] = cv ? normed(a, acc[mt][j][r], mu[mt], rs[mt], cv ? n0 + r : 0) : -INFINITY;
+        mx = fmaxf(mx, v[j][r]);
+      }
+      if (a.logits && valid && cv)
+        *reinterpret_cast<float4*>(a.logits + (size_t)m * a.N + n0) =
+            make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    float se = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) se += v[j][r] == -INFINITY ? 0.0f : expf(v[j][r] - mx);
+    se += __shfl_xor(se, 16);
+    se += __shfl_xor(se, 32);
+    if (q == 0 && valid) a.tile_ms[(size_t)t * a.M + m] = make_float2(mx, se);
+    uint64_t key[4][4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        key[j][r] = v[j][r] == -INFINITY ? 0ull : rank_key(v[j][r], kTileN * t + 16 * j + 4 * q + r);
+    uint64_t* top = a.tile_top + ((size_t)t * a.M + (valid ? m : 0)) * a.kappa;
+    for (int rr = 0; rr < a.kappa; ++rr) {
+      uint64_t best = 0ull;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) best = key[j][r] > best ? key[j][r] : best;
+      uint64_t o = __shfl_xor(best, 16);
+      best = o > best ? o : best;
+      o = __shfl_xor(best, 32);
+      best = o > best ? o : best;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) key[j][r] = key[j][r] == best ? 0ull : key[j][r];
+      if (q == 0 && valid) top[rr] = best;
     }
   }
 }
 
-// Per-row (mu, scale) of the fused pre-norm from the producer's per-segment
-// (mean, M2) pairs: mean = average of segment means; M2 = sum M2_t +
-// cnt * sum (mean_t - mean)^2. RMSNorm uses E[x^2] = M2/K + mean^2.
-__device__ void norm_rows(const GemmArgs& a, float2* rowstat) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const int T = a.a_stats_tiles;
-  const float cnt = (float)a.K / (float)T;
-  for (int m = wave; m < a.M; m += nw) {
-    // up to 4 segments per lane, loaded together (T <= 256)
-    float2 st[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int t = lane + 64 * q;
-      st[q] = a.a_stats[(size_t)(t < T ? t : 0) * a.M + m];
-    }
-    float sm = 0.0f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) sm += lane + 64 * q < T ? st[q].x : 0.0f;
-    const float mean = wave_sum(sm) / (float)T;
-    float m2 = 0.0f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float d = st[q].x - mean;
-      m2 += lane + 64 * q < T ? st[q].y + cnt * d * d : 0.0f;
-    }
-    m2 = wave_sum(m2);
-    float mu, sc;
-    if (a.a_norm == 2) {
-      mu = mean;
-      sc = 1.0f / sqrtf(m2 / (float)a.K + a.a_eps);
-    } else {
-      mu = 0.0f;
-      sc = 1.0f / sqrtf(m2 / (float)a.K + mean * mean + a.a_eps);
-    }
-    if (lane == 0) rowstat[m] = make_float2(mu, sc);
-  }
-}
-
-// Raw A-operand data of one MFMA k-step for one row tile: 8 fp32 values of
-// the row, and for a fused pre-norm the 8 matching gains (and shifts).
-struct ARaw {
-  u32x4 x0, x1, g, b;
+template <int MT>
+struct KStep {
+  bf16x8 w[4];
+  bf16x8 ah[MT], al[MT];
 };
 
-template <int MT, int U, int EPI, bool SPLIT, int NORM>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
-  __shared__ float red[MT * 16 * kRedStride];
-  __shared__ float2 rowstat[MT * 16];
-  __shared__ int s_last;
+template <int MT, int NW, int EPI>
+__global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
+  constexpr int D = MT == 1 ? (NW == 8 ? 4 : 8) : (MT <= 3 ? 4 : 2);  // k-steps in flight per wave
+  constexpr int RCH = MT < 3 ? MT : 3;  // row tiles per LDS reduction round
+  __shared__ floatx4 red[NW][RCH * 4][kWave];
+  __shared__ __attribute__((aligned(16))) float scr[16 * kScr];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int r16 = lane & 15, g = lane >> 4;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int t = blockIdx.x / a.splits, s = blockIdx.x - t * a.splits;
   const int KS = a.K >> 5;
-  const int ks_b = (int)((int64_t)KS * s / a.splits);
-  const int ks_e = (int)((int64_t)KS * (s + 1) / a.splits);
-  const int nks = ks_e - ks_b;
-  const int kb = ks_b + (nks * wave) / 4, ke = ks_b + (nks * (wave + 1)) / 4;
+  const int kb0 = (int)((int64_t)KS * s / a.splits), ke0 = (int)((int64_t)KS * (s + 1) / a.splits);
+  const int nk = ke0 - kb0;
+  const int kb = kb0 + nk * wave / NW, ke = kb0 + nk * (wave + 1) / NW;
+  const int n = ke - kb;
 
   const uint16_t* wp[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) wp[j] = weight_frag(a, t, j, lane);
-  // rows past M read row 0 (always valid) and are zeroed after the load:
-  // no divergent branch around loads, so the compiler keeps them in flight
-  const float* ap[MT];
-  float amask[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = mt * 16 + r16;
-    amask[mt] = m < a.M ? 1.0f : 0.0f;
-    ap[mt] = a.A + (size_t)(m < a.M ? m : 0) * a.K + g * 8;
-  }
-  const uint16_t* gp = NORM ? a.a_g + g * 8 : nullptr;
-  const uint16_t* bp = NORM == 2 ? a.a_b + g * 8 : nullptr;
-
-  bf16x8 w0[U][4], w1[U][4];
-  auto issue_w = [&](bf16x8 (&w)[U][4], int ks) {
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) w[u][j] = load16(wp[j] + (size_t)(ks + u) * 512);
-  };
-  auto issue_a = [&](ARaw (&r)[U][MT], int ks) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const size_t ko = (size_t)(ks + u) * 32;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        r[u][mt].x0 = *reinterpret_cast<const u32x4*>(ap[mt] + ko);
-        r[u][mt].x1 = *reinterpret_cast<const u32x4*>(ap[mt] + ko + 4);
-      }
-      if constexpr (NORM != 0) {
-        const u32x4 gv = *reinterpret_cast<const u32x4*>(gp + ko);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) r[u][mt].g = gv;
-      }
-      if constexpr (NORM == 2) {
-        const u32x4 bv = *reinterpret_cast<const u32x4*>(bp + ko);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) r[u][mt].b = bv;
-      }
-    }
-  };
-
-  // the weight stream of batch 0 goes out before the pre-norm statistics
-  const int nb = (ke - kb) / U;
-  if (nb > 0) issue_w(w0, kb);
-
-  if constexpr (NORM != 0) {
-    norm_rows(a, rowstat);
-    lds_barrier();
-  }
-  float mu[MT], sc[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    mu[mt] = 0.0f;
-    sc[mt] = amask[mt];
-    if constexpr (NORM != 0) {
-      const float2 st = rowstat[(mt * 16 + r16) < a.M ? mt * 16 + r16 : 0];
-      mu[mt] = st.x;
-      sc[mt] = st.y * amask[mt];
-    }
-  }
+  const uint16_t* ap = a.a_img + lane * 8;
 
   floatx4 acc[MT][4];
 #pragma unroll
@@ -305,242 +442,211 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // A operand = (x - mu) * sc * g + b (pre-norm) or x * mask, then split into
-  // bf16 hi + lo (two MFMAs per weight tile) or rounded once.
-  auto compute = [&](const bf16x8 (&w)[U][4], const ARaw (&r)[U][MT]) {
+  KStep<MT> st[D];
+  auto issue = [&](KStep<MT>& x, int k) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int j = 0; j < 4; ++j) x.w[j] = load16(wp[j] + (size_t)k * 512);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        float v[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          v[i] = __uint_as_float(r[u][mt].x0[i]);
-          v[4 + i] = __uint_as_float(r[u][mt].x1[i]);
-        }
-        if constexpr (NORM != 0) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const uint32_t gw = r[u][mt].g[i];
-            v[2 * i] = (v[2 * i] - mu[mt]) * sc[mt] * bf_lo(gw);
-            v[2 * i + 1] = (v[2 * i + 1] - mu[mt]) * sc[mt] * bf_hi(gw);
-            if constexpr (NORM == 2) {
-              const uint32_t bw = r[u][mt].b[i];
-              v[2 * i] += bf_lo(bw) * amask[mt];
-              v[2 * i + 1] += bf_hi(bw) * amask[mt];
-            }
-          }
-        } else {
-#pragma unroll
-          for (int i = 0; i < 8; ++i) v[i] *= amask[mt];
-        }
-        bf16x8 hi, lo;
-        if constexpr (SPLIT) split_vals(v, hi, lo);
-        else hi = round_vals(v);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          acc[mt][j] = mfma16x16x32(hi, w[u][j], acc[mt][j]);
-          if constexpr (SPLIT) acc[mt][j] = mfma16x16x32(lo, w[u][j], acc[mt][j]);
-        }
-      }
+    for (int mt = 0; mt < MT; ++mt) {
+      const uint16_t* p = ap + (size_t)(k * MT + mt) * 1024;
+      x.ah[mt] = load16(p);
+      x.al[mt] = load16(p + 512);
+    }
   };
-
-  // software pipeline: A of batch i, weights of batch i+1, then the MFMAs of
-  // batch i; in-order completion lets the wait for A(i) leave W(i+1) in flight
-  int i = 0;
-  for (; i + 2 < nb; i += 2) {
-    ARaw r[U][MT];
-    issue_a(r, kb + i * U);
-    issue_w(w1, kb + (i + 1) * U);
-    compute(w0, r);
-    issue_a(r, kb + (i + 1) * U);
-    issue_w(w0, kb + (i + 2) * U);
-    compute(w1, r);
-  }
-  if (nb - i == 2) {
-    ARaw r[U][MT];
-    issue_a(r, kb + i * U);
-    issue_w(w1, kb + (i + 1) * U);
-    compute(w0, r);
-    issue_a(r, kb + (i + 1) * U);
-    compute(w1, r);
-  } else if (nb - i == 1) {
-    ARaw r[U][MT];
-    issue_a(r, kb + i * U);
-    compute(w0, r);
-  }
-  // k-steps left over from whole batches, one batch-sized step at a time
-  for (int ks = kb + nb * U; ks < ke; ++ks) {
-    bf16x8 w[1][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) w[0][j] = load16(wp[j] + (size_t)ks * 512);
-    ARaw r[1][MT];
+  for (int d = 0; d < D; ++d)
+    if (d < n) issue(st[d], kb + d);
+  for (int i0 = 0; i0 < n; i0 += D) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      r[0][mt].x0 = *reinterpret_cast<const u32x4*>(ap[mt] + (size_t)ks * 32);
-      r[0][mt].x1 = *reinterpret_cast<const u32x4*>(ap[mt] + (size_t)ks * 32 + 4);
-      if constexpr (NORM != 0) r[0][mt].g = *reinterpret_cast<const u32x4*>(gp + (size_t)ks * 32);
-      if constexpr (NORM == 2) r[0][mt].b = *reinterpret_cast<const u32x4*>(bp + (size_t)ks * 32);
-    }
+    for (int d = 0; d < D; ++d) {
+      const int i = i0 + d;
+      if (i < n) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      float v[8];
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        v[q] = __uint_as_float(r[0][mt].x0[q]);
-        v[4 + q] = __uint_as_float(r[0][mt].x1[q]);
-      }
-      if constexpr (NORM != 0) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          v[2 * q] = (v[2 * q] - mu[mt]) * sc[mt] * bf_lo(r[0][mt].g[q]);
-          v[2 * q + 1] = (v[2 * q + 1] - mu[mt]) * sc[mt] * bf_hi(r[0][mt].g[q]);
-          if constexpr (NORM == 2) {
-            v[2 * q] += bf_lo(r[0][mt].b[q]) * amask[mt];
-            v[2 * q + 1] += bf_hi(r[0][mt].b[q]) * amask[mt];
+          for (int j = 0; j < 4; ++j) {
+            acc[mt][j] = mfma16x16x32(st[d].w[j], st[d].ah[mt], acc[mt][j]);
+            acc[mt][j] = mfma16x16x32(st[d].w[j], st[d].al[mt], acc[mt][j]);
           }
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) v[q] *= amask[mt];
-      }
-      bf16x8 hi, lo;
-      if constexpr (SPLIT) split_vals(v, hi, lo);
-      else hi = round_vals(v);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        acc[mt][j] = mfma16x16x32(hi, w[0][j], acc[mt][j]);
-        if constexpr (SPLIT) acc[mt][j] = mfma16x16x32(lo, w[0][j], acc[mt][j]);
+        if (i + D < n) issue(st[d], kb + i + D);
       }
     }
   }
 
-  // fixed-order sum of the 4 waves' tiles in LDS
-  for (int w = 0; w < 4; ++w) {
-    if (wave == w) {
+  // fixed-order sum of the waves' tiles
+  if constexpr (NW > 1) {
+    for (int m0 = 0; m0 < MT; m0 += RCH) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int c = 0; c < RCH; ++c)
+        if (m0 + c < MT)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+          for (int j = 0; j < 4; ++j) red[wave][c * 4 + j][lane] = acc[m0 + c][j];
+      __syncthreads();
+      if (wave == 0) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int idx = (mt * 16 + 4 * g + r) * kRedStride + 16 * j + r16;
-            red[idx] = (w == 0 ? 0.0f : red[idx]) + acc[mt][j][r];
-          }
+        for (int c = 0; c < RCH; ++c)
+          if (m0 + c < MT)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              floatx4 v = red[0][c * 4 + j][lane];
+#pragma unroll
+              for (int w = 1; w < NW; ++w) v += red[w][c * 4 + j][lane];
+              acc[m0 + c][j] = v;
+            }
+      }
+      __syncthreads();
     }
-    __syncthreads();
+    if (wave != 0) return;
   }
 
   if (a.splits > 1) {
-    const size_t ld = (size_t)a.n_tiles * kTileN;
-    float* dst = a.partial + (size_t)s * a.M * ld + (size_t)t * kTileN;
-    for (int i = tid; i < a.M * kTileN; i += blockDim.x) {
-      const int m = i / kTileN, c = i - m * kTileN;
-      store_coherent(dst + (size_t)m * ld + c, red[m * kRedStride + c]);
-    }
-    drain_stores();
-    __syncthreads();
-    if (tid == 0) s_last = (counter_add(&a.counters[t], 1) == a.splits - 1);
-    __syncthreads();
-    if (!s_last) return;
-    // splits summed in split order; 8 loads in flight per group (indices past
-    // the last split read split 0 and are masked out)
-    const float* src = a.partial + (size_t)t * kTileN;
-    for (int i = tid; i < a.M * kTileN; i += blockDim.x) {
-      const int m = i / kTileN, c = i - m * kTileN;
-      const float* p = src + (size_t)m * ld + c;
-      const size_t sstride = (size_t)a.M * ld;
-      float v = 0.0f;
-      for (int sp0 = 0; sp0 < a.splits; sp0 += 8) {
-        float part[8];
+    // publish this split's tile; the last split to arrive sums all of them
+    float* slot = a.partial + ((size_t)t * a.splits + s) * (MT * 1024) + lane * 4;
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const int sp = sp0 + q < a.splits ? sp0 + q : 0;
-          part[q] = load_coherent(p + sp * sstride);
-        }
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int q = 0; q < 8; ++q) v += sp0 + q < a.splits ? part[q] : 0.0f;
+      for (int j = 0; j < 4; ++j) {
+        float* p = slot + (mt * 4 + j) * 256;
+        store_coherent2(p, acc[mt][j][0], acc[mt][j][1]);
+        store_coherent2(p + 2, acc[mt][j][2], acc[mt][j][3]);
       }
-      red[m * kRedStride + c] = v;
+    drain_stores();
+    int old = 0;
+    if (lane == 0) old = counter_add(&a.counters[t], 1);
+    old = __shfl(old, 0);
+    if (old != a.splits - 1) return;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const float* base = a.partial + (size_t)t * a.splits * (MT * 1024) + lane * 4;
+    for (int sp0 = 0; sp0 < a.splits; sp0 += 2) {
+      // two splits' tiles in flight, summed in split order
+      floatx4 part[2][MT][4];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int sp = sp0 + u < a.splits ? sp0 + u : sp0;
+        const float* src = base + (size_t)sp * (MT * 1024);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float* p = src + (mt * 4 + j) * 256;
+            const float2 v01 = load_coherent2(p), v23 = load_coherent2(p + 2);
+            part[u][mt][j] = floatx4{v01.x, v01.y, v23.x, v23.y};
+          }
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+        if (sp0 + u < a.splits)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[mt][j] += part[u][mt][j];
     }
-    if (tid == 0) counter_reset(&a.counters[t]);
-    __syncthreads();
+    if (lane == 0) counter_reset(&a.counters[t]);
   }
 
-  if constexpr (EPI == EPI_QKV) epi_qkv(a, t, red);
-  else if constexpr (EPI == EPI_RESID) epi_resid(a, t, red);
-  else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, t, red);
-  else if constexpr (EPI == EPI_RELU) epi_relu(a, t, red);
-  else epi_head(a, t, red);
+  if constexpr (EPI == EPI_RESID) {
+    epi_resid<MT>(a, t, acc, scr);
+  } else {
+    float mu[MT], rs[MT];
+    row_norm<MT>(a, mu, rs);
+    if constexpr (EPI == EPI_QKV) epi_qkv<MT>(a, t, acc, mu, rs);
+    else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<MT>(a, t, acc, scr, mu, rs);
+    else if constexpr (EPI == EPI_RELU) epi_relu<MT>(a, t, acc, scr, mu, rs);
+    else epi_head<MT>(a, t, acc, mu, rs);
+  }
 }
 
-// Activations enter as bf16 hi + lo pairs (two MFMAs per weight tile) at
-// every block size: a single bf16 rounding of the activations loses about
-// three decimal digits per layer, which compounds over a deep target; at 144
-// rows the doubled MFMA work still stays under the weight-stream time.
-template <int MT, int EPI, int NORM>
-hipError_t launch_mt(const GemmArgs& a, hipStream_t s) {
-  constexpr int U = MT == 1 ? 4 : (MT <= 3 ? 2 : 1);
-  constexpr bool SPLIT = true;
-  hipLaunchKernelGGL((gemm_kernel<MT, U, EPI, SPLIT, NORM>), dim3(a.n_tiles * a.splits),
-                     dim3(256), 0, s, a);
+template <int MT, int NW, int EPI>
+hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((gemm_kernel<MT, NW, EPI>), dim3(a.n_tiles * a.splits), dim3(64 * NW), 0, s, a);
   return hipGetLastError();
 }
 
-template <int EPI, int NORM>
-hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  const int mt = (a.M + 15) / 16;
-  if (mt == 1) return launch_mt<1, EPI, NORM>(a, s);
-  if (mt == 2) return launch_mt<2, EPI, NORM>(a, s);
-  if (mt == 3) return launch_mt<3, EPI, NORM>(a, s);
-  if (mt <= 9) return launch_mt<9, EPI, NORM>(a, s);
-  return hipErrorInvalidValue;
-}
-
 template <int EPI>
-hipError_t launch_norm_kind(const GemmArgs& a, hipStream_t s) {
-  if (a.a_norm == 1) return launch_epi<EPI, 1>(a, s);
-  if (a.a_norm == 2) return launch_epi<EPI, 2>(a, s);
-  return launch_epi<EPI, 0>(a, s);
+hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
+  switch (a.MT) {
+    case 1: return a.waves == 8 ? launch_cfg<1, 8, EPI>(a, s) : launch_cfg<1, 4, EPI>(a, s);
+    case 2: return launch_cfg<2, 4, EPI>(a, s);
+    case 3: return launch_cfg<3, 4, EPI>(a, s);
+    case 9: return launch_cfg<9, 4, EPI>(a, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
-// Row-major [R][K] (src) -> fragment-major (dst), R % 16 == 0, K % 32 == 0:
-// 16 bytes per thread, dst written sequentially.
-__global__ void repack_kernel(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
-                              int64_t rows, int32_t K) {
-  const int64_t ks_n = K >> 5;
-  const int64_t n16 = rows * (int64_t)K / 8;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16;
+// Row-major [rows][K] -> fragment-major: fragment (G, ks) holds rows
+// 16G..16G+15, columns 32ks..32ks+31, lane l taking row 16G + l%16 and
+// columns 32ks + 8(l/16) .. +8 (16 bytes); dst is written sequentially.
+__global__ __launch_bounds__(256) void repack_kernel(const uint16_t* __restrict__ src,
+                                                     uint16_t* __restrict__ dst, int64_t rows,
+                                                     int32_t K) {
+  const int64_t KS = K >> 5;
+  const int64_t total = (rows >> 4) * KS * 64;  // 16-byte lane chunks
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const int lane = (int)(i & 63);
-    const int64_t frag = i >> 6;
-    const int64_t grp = frag / ks_n, ks = frag - grp * ks_n;
-    const int64_t row = grp * 16 + (lane & 15);
-    const int64_t col = ks * 32 + 8 * (lane >> 4);
-    reinterpret_cast<u32x4*>(dst)[i] = *reinterpret_cast<const u32x4*>(src + row * K + col);
+    const int64_t lanes = i & 63, frag = i >> 6;
+    const int64_t G = frag / KS, ks = frag - G * KS;
+    const int64_t row = 16 * G + (lanes & 15), col = 32 * ks + 8 * (lanes >> 4);
+    *reinterpret_cast<u32x4*>(dst + i * 8) = *reinterpret_cast<const u32x4*>(src + row * K + col);
+  }
+}
+
+// c[n] = sum_k W[n][k] g[k] and e[n] = sum_k W[n][k] b[k] of a row-major bf16
+// matrix; one wave per row, fp64 accumulation.
+__global__ __launch_bounds__(256) void colsum_kernel(const uint16_t* w, int64_t rows, int32_t K,
+                                                     const uint16_t* g, const uint16_t* b, float* c,
+                                                     float* e) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  double sg = 0.0, sb = 0.0;
+  for (int k = lane; k < K; k += 64) {
+    const double wv = bf2f(w[row * K + k]);
+    sg += wv * bf2f(g[k]);
+    if (b) sb += wv * bf2f(b[k]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    sg += __shfl_xor(sg, o);
+    sb += __shfl_xor(sb, o);
+  }
+  if (lane == 0) {
+    c[row] = (float)sg;
+    if (e) e[row] = (float)sb;
   }
 }
 
 }  // namespace
 
-hipError_t launch_repack(const uint16_t* src, uint16_t* dst, int64_t rows, int32_t K,
-                         hipStream_t s) {
-  const int64_t n16 = rows * (int64_t)K / 8;
-  int64_t grid = (n16 + 255) / 256;
-  if (grid > 65536) grid = 65536;
-  hipLaunchKernelGGL(repack_kernel, dim3((int)grid), dim3(256), 0, s, src, dst, rows, K);
+hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
+  if (a.n_tiles < 1 || a.splits < 1 || a.K % 32 || a.M < 1 || a.M > 16 * a.MT) return hipErrorInvalidValue;
+  if (a.splits > 1 && (!a.partial || !a.counters)) return hipErrorInvalidValue;
+  switch (epi) {
+    case EPI_QKV: return launch_epi<EPI_QKV>(a, s);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, s);
+    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, s);
+    case EPI_RELU: return launch_epi<EPI_RELU>(a, s);
+    case EPI_HEAD: return launch_epi<EPI_HEAD>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_repack(const uint16_t* src, uint16_t* dst, int64_t rows, int32_t K, hipStream_t s) {
+  if (rows % 16 || K % 32) return hipErrorInvalidValue;
+  const int64_t total = (rows >> 4) * (K >> 5) * 64;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(repack_kernel, dim3((unsigned)blocks), dim3(256), 0, s, src, dst, rows, K);
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
-  switch (epi) {
-    case EPI_QKV: return launch_norm_kind<EPI_QKV>(a, s);
-    case EPI_RESID: return launch_epi<EPI_RESID, 0>(a, s);
-    case EPI_SWIGLU: return launch_norm_kind<EPI_SWIGLU>(a, s);
-    case EPI_RELU: return launch_norm_kind<EPI_RELU>(a, s);
-    case EPI_HEAD: return launch_norm_kind<EPI_HEAD>(a, s);
-    default: return hipErrorInvalidValue;
-  }
+hipError_t launch_colsum(const uint16_t* w, int64_t rows, int32_t K, const uint16_t* g,
+                         const uint16_t* b, float* c, float* e, hipStream_t s) {
+  hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, w, rows, K,
+                     g, b, c, e);
+  return hipGetLastError();
 }
 
 }  // namespace msd

@@ -8,98 +8,124 @@
 namespace msd {
 
 // ---------------------------------------------------------------------------
-// skinny weight-streaming GEMM: Y[M][N] = X[M][K] W^T, W [N][K] bf16
+// skinny weight-streaming GEMM: Y[M][N] = norm(X)[M][K] W^T, W [N][K] bf16
 // ---------------------------------------------------------------------------
 enum GemmMap : int32_t {
-  MAP_PLAIN = 0,   // output column n <- row n of w0 (rows >= n0 are padding)
+  MAP_PLAIN = 0,   // output column n <- row n of w0 (rows >= N are padding)
   MAP_QKV = 1,     // 64-wide tiles hold 32 rotary pairs of one q/k/v head
   MAP_GATEUP = 2,  // 64-wide tiles: 32 rows of w0 (gate) then the same 32 of w1 (up)
 };
 
 enum GemmEpi : int32_t {
   EPI_QKV = 0,     // (+bias) rotary, q -> q buffer, k/v -> cache slots
-  EPI_RESID = 1,   // x[m][n] += y (+bias)
-  EPI_SWIGLU = 2,  // act[m][f] = silu(gate) * up
-  EPI_RELU = 3,    // act[m][n] = relu(y + bias)
+  EPI_RESID = 1,   // x[m][n] += y (+bias), row statistics, images of x
+  EPI_SWIGLU = 2,  // act = silu(gate) * up -> activation image
+  EPI_RELU = 3,    // act = relu(y + bias) -> activation image
   EPI_HEAD = 4,    // logits (+ per-tile max / sum-exp / top-kappa)
 };
 
-constexpr int kTileN = 64;   // output columns per workgroup tile
+constexpr int kTileN = 64;   // output columns per tile
 constexpr int kMaxMT = 9;    // up to 144 rows (9 MFMA row tiles)
 
+// Pre-norm of the GEMM input, applied after the product: the input image
+// holds x * g (the norm gain folded in by its producer), so
+//   RMSNorm:   y = r * (W (x g))                    r = 1 / sqrt(mean x^2 + eps)
+//   LayerNorm: y = r * (W (x g)) - r mu c + e       r = 1 / sqrt(var x + eps)
+// with c = W g and e = W b per output column, and (mu, var) rebuilt from the
+// producer's per-64-column (mean, M2) summaries.
+struct RowNorm {
+  int32_t kind;            // 0 none, 1 RMSNorm, 2 LayerNorm
+  const float2* stats;     // [tiles][M] (mean, M2) over 64-column tiles
+  int32_t tiles;           // = K / 64
+  float eps;
+  const float* col_g;      // LayerNorm: c [N]
+  const float* col_b;      // LayerNorm: e [N]
+};
+
+// An activation image an epilogue writes, with an optional per-column gain.
+struct ImageOut {
+  uint16_t* img;
+  const uint16_t* gain;
+};
+
 struct GemmArgs {
-  const float* A;      // fp32 activations [M][K]
-  int32_t M, K, N;     // N = logical output columns (padding masked)
-  int32_t n_tiles, splits;
+  const uint16_t* a_img;   // input image [K/32][MT][2][64][8]
+  int32_t M, MT, K, N;     // N = logical output columns (padding masked)
+  int32_t n_tiles, splits, waves;
   int32_t map;
   const uint16_t* w0;
   const uint16_t* w1;
   const uint16_t* w2;
   int32_t n_heads, n_kv_heads, head_dim;  // MAP_QKV
-  float* partial;      // [splits][M][n_tiles*64] fp32 (splits > 1)
-  int32_t* counters;   // [n_tiles], zero on entry, left zero on exit
-  // epilogues
-  const uint16_t* b0;  // bias of w0 (q / plain / up)
-  const uint16_t* b1;  // bias of w1 (k)
-  const uint16_t* b2;  // bias of w2 (v)
-  float* x;            // EPI_RESID residual [M][N]
-  float* out_f32;      // EPI_QKV q [M][H*hd]; EPI_SWIGLU / EPI_RELU act [M][F]
-  uint16_t* k_cache;   // EPI_QKV this layer's [batch_cap][Hkv][cap][hd]
+  float* partial;          // [n_tiles][splits][MT * 1024] (splits > 1)
+  int32_t* counters;       // [n_tiles], zero on entry, left zero on exit
+  RowNorm norm;
+  const uint16_t* b0;      // bias of w0 (q / plain / up)
+  const uint16_t* b1;      // bias of w1 (k)
+  const uint16_t* b2;      // bias of w2 (v)
+  // EPI_RESID
+  float* x;                // residual [M][N]
+  float2* stats_out;       // [n_tiles][M] (mean, M2) of the updated rows
+  ImageOut img_out[2];     // images of the updated x (K = N)
+  // EPI_QKV
+  float* q_out;            // [M][H * hd]
+  uint16_t* k_cache;       // this layer's [batch_cap][Hkv][cap][hd]
   uint16_t* v_cache;
-  const int32_t* len;  // committed lengths [batch]
+  const int32_t* len;      // committed lengths [batch]
   uint32_t* status;
   int32_t capacity, n_slots;
-  const float2* rope;  // [max_positions][hd/2] (cos, sin), or null
+  const float2* rope;      // [max_positions][hd/2] (cos, sin), or null
   int32_t rope_rows;
-  // pre-norm fused into the A load: 0 none, 1 RMSNorm, 2 LayerNorm, from the
-  // producer's per-segment (mean, M2) of each row: a_stats [a_stats_tiles][M]
-  int32_t a_norm, a_stats_tiles;
-  const float2* a_stats;
-  const uint16_t* a_g;
-  const uint16_t* a_b;
-  float a_eps;
-  float2* stats_out;   // EPI_RESID: [n_tiles][M] (mean, M2) of the updated rows
-  int32_t weights_nt;  // stream weights with non-temporal loads
-  float* logits;       // EPI_HEAD [M][N] or null
-  float2* tile_ms;     // EPI_HEAD [n_tiles][M] (max, sum exp)
-  uint64_t* tile_top;  // EPI_HEAD [n_tiles][M][kappa] rank keys
-  int32_t kappa;
   int32_t depth[kMaxSlots];
+  // EPI_SWIGLU / EPI_RELU
+  uint16_t* act_img;       // image of the activation (K = d_ffn)
+  // EPI_HEAD
+  float* logits;           // [M][N] or null
+  float2* tile_ms;         // [n_tiles][M] (max, sum exp)
+  uint64_t* tile_top;      // [n_tiles][M][kappa] rank keys
+  int32_t kappa;
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
 // row-major [rows][K] -> fragment-major weight layout (src and dst distinct)
 hipError_t launch_repack(const uint16_t* src, uint16_t* dst, int64_t rows, int32_t K,
                          hipStream_t s);
+// c[n] = sum_k W[n][k] g[k] (and e with b) for a row-major bf16 matrix, fp64
+// accumulation, fp32 out; b may be null.
+hipError_t launch_colsum(const uint16_t* w, int64_t rows, int32_t K, const uint16_t* g,
+                         const uint16_t* b, float* c, float* e, hipStream_t s);
 
 // ---------------------------------------------------------------------------
-// embedding / norms
+// block rows -> residual, statistics and image
 // ---------------------------------------------------------------------------
-struct EmbedArgs {
+struct RowsArgs {
+  // source of row m: hidden[m] (fp32, if non-null) or E[tokens[m]] (+ P[pos])
+  const float* hidden;
   const int32_t* tokens;   // [M]
   const uint16_t* embed;   // [V][d]
   const uint16_t* pos_embed;
   int32_t embed_frag;      // the table is stored fragment-major (tied LM head)
   const int32_t* len;
-  int32_t M, d, n_slots, max_positions, vocab;
+  int32_t M, MT, d, n_slots, max_positions, vocab;
   uint32_t* status;        // MSD_DEV_TOKEN on an id outside [0, vocab)
-  float* x;                // [M][d]
-  float2* stats;           // [M] (mean, M2) of each embedded row
+  float* x;                // [M][d] (may be null with hidden)
+  float2* stats;           // [d/64][M] (mean, M2)
+  ImageOut img;            // image of the rows (K = d)
+  uint16_t* zero_img;      // another image whose padding rows are cleared
+  int32_t zero_img_k;
   int32_t* zero_i32;       // counters to clear
   int64_t n_zero;
   int32_t depth[kMaxSlots];
 };
-hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
-
-// (mean, M2) of each row of x [M][d] (one segment per row)
-hipError_t launch_row_stats(const float* x, int M, int d, float2* stats, hipStream_t s);
+hipError_t launch_rows(const RowsArgs& a, hipStream_t s);
 hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // verify attention
 // ---------------------------------------------------------------------------
-constexpr int kMaxAttnSpans = 512;    // key spans per (sequence, kv head)
+constexpr int kMaxAttnChunks = 128;   // key chunks per (sequence, kv head)
 constexpr int kMaxCapacity = 32768;   // cache positions
+constexpr int kAttnChunk = 256;       // keys per workgroup chunk (4 waves x 64)
 
 struct AttnArgs {
   const float* q;           // fp32 [M][H][hd] (rotated)
@@ -107,11 +133,13 @@ struct AttnArgs {
   const uint16_t* v_cache;
   const int32_t* len;
   uint32_t* status;
-  float* out;               // fp32 [M][H*hd]
-  float* part_o;            // [batch][Hkv][max_spans][Qn][hd]
-  float* part_ml;           // [batch][Hkv][max_spans][Qn][2] (max, sum exp)
+  uint16_t* out_img;        // image of the output (K = H * hd)
+  int32_t MT;
+  float* part_o;            // [batch][Hkv][chunks][Qn][hd]
+  float* part_ml;           // [batch][Hkv][chunks][Qn][2] (max, sum exp)
+  int32_t* counters;        // [batch][Hkv]
   int32_t batch, n_heads, n_kv_heads, capacity, n_slots;
-  int32_t span, max_spans;  // keys per wave (multiple of 64), spans per sequence
+  int32_t max_chunks;
   float scale;
   Topo topo;
 };

@@ -17,8 +17,12 @@ struct msd_model {
   msd_model_config cfg;
   std::vector<const uint16_t*> t;  // MSD_N_TENSORS(n_layers) entries
   float2* rope = nullptr;          // [max_positions][head_dim/2] (cos, sin)
-  int32_t target_wgs = 384;        // split-K sizing target
-  int32_t weights_nt = 0;          // non-temporal weight loads
+  float* colsums = nullptr;        // LayerNorm column sums c = W g, e = W b (model create)
+  std::vector<const float*> qkv_c, qkv_e, up_c, up_e;
+  const float* head_c = nullptr;
+  const float* head_e = nullptr;
+  int32_t target_wgs = 240;        // split-K sizing target (workgroups per GEMM)
+  int32_t waves = 8;               // GEMM waves per workgroup for one row tile
   int32_t prof_class = -1;         // instrumentation (msd_set_profile)
   std::vector<hipEvent_t> prof_begin, prof_end;
 };
@@ -48,26 +52,34 @@ inline const uint16_t* head_w(const msd_model* m) {
 
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// split-K factor: enough workgroups to keep HBM busy, >= 4 k-steps per wave
-int splits_for(const msd_model* m, int n_tiles, int K) {
+// Row tiles of the kernels for M rows: 1, 2 or 3, else the 9-tile variant.
+inline int row_tiles(int M) {
+  const int mt = (M + 15) / 16;
+  return mt <= 3 ? mt : kMaxMT;
+}
+
+// Split-K factor: about target_wgs workgroups per GEMM, each wave keeping at
+// least 2 k-steps.
+int splits_for(const msd_model* m, int n_tiles, int K, int waves) {
   const int ks = K / 32;
-  int max_s = ks / 16;
+  int max_s = ks / (2 * waves);
   if (max_s < 1) max_s = 1;
-  int want = (m->target_wgs + n_tiles - 1) / n_tiles;
+  int want = (m->target_wgs + n_tiles / 2) / n_tiles;
   if (want < 1) want = 1;
   return want < max_s ? want : max_s;
 }
 
 struct GemmShape {
-  int n_tiles, K, splits;
+  int n_tiles, K, splits, waves;
 };
 
 struct Shapes {
   GemmShape qkv, o, up, down, head;
 };
 
-Shapes shapes(const msd_model* m) {
+Shapes shapes(const msd_model* m, int M) {
   const msd_model_config& c = m->cfg;
+  const int waves = row_tiles(M) == 1 ? m->waves : 4;
   Shapes s;
   s.qkv.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim / kTileN;
   s.qkv.K = c.d_model;
@@ -79,40 +91,51 @@ Shapes shapes(const msd_model* m) {
   s.down.K = c.d_ffn;
   s.head.n_tiles = (c.vocab + kTileN - 1) / kTileN;
   s.head.K = c.d_model;
-  for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head})
-    g->splits = splits_for(m, g->n_tiles, g->K);
+  for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
+    g->waves = waves;
+    g->splits = splits_for(m, g->n_tiles, g->K, waves);
+  }
   return s;
 }
 
 struct Layout {
-  size_t x, stats, q, attn, act, partial, counters, part_o, part_ml, tile_ms, tile_top, total;
+  size_t x, stats, q, img_x, img_h, img_f, img_attn, img_act, partial, counters, part_o, part_ml,
+      tile_ms, tile_top, total;
   int64_t n_counters;
   int32_t attn_counter_off;  // in int32 units inside counters
-  int32_t span, max_spans;
+  int32_t MT, max_chunks;
 };
+
+// image bytes of an [M][K] activation
+inline size_t img_bytes(int K, int MT) { return (size_t)(K / 32) * MT * 1024 * sizeof(uint16_t); }
 
 Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacity) {
   const msd_model_config& c = m->cfg;
-  const Shapes s = shapes(m);
-  const size_t M = (size_t)batch * n_slots;
+  const int M = batch * n_slots;
+  const Shapes s = shapes(m, M);
   const int kmax = kappa > 1 ? kappa : 1;
+  const int qd = c.n_heads * c.head_dim;
   Layout L{};
+  L.MT = row_tiles(M);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off += align_up(bytes);
     return o;
   };
-  L.x = take(M * c.d_model * sizeof(float));
+  L.x = take((size_t)M * c.d_model * sizeof(float));
   L.stats = take((size_t)(c.d_model / kTileN) * M * sizeof(float2));
-  L.q = take(M * c.n_heads * c.head_dim * sizeof(float));
-  L.attn = take(M * c.n_heads * c.head_dim * sizeof(float));
-  L.act = take(M * c.d_ffn * sizeof(float));
+  L.q = take((size_t)M * qd * sizeof(float));
+  L.img_x = take(img_bytes(c.d_model, L.MT));
+  L.img_h = take(img_bytes(c.d_model, L.MT));
+  L.img_f = take(img_bytes(c.d_model, L.MT));
+  L.img_attn = take(img_bytes(qd, L.MT));
+  L.img_act = take(img_bytes(c.d_ffn, L.MT));
   size_t part = 0;
   int max_tiles = 0;
   for (const GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
     if (g->splits > 1) {
-      const size_t p = (size_t)g->splits * M * g->n_tiles * kTileN * sizeof(float);
+      const size_t p = (size_t)g->n_tiles * g->splits * L.MT * 1024 * sizeof(float);
       part = p > part ? p : part;
       max_tiles = g->n_tiles > max_tiles ? g->n_tiles : max_tiles;
     }
@@ -121,15 +144,9 @@ Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacit
   L.attn_counter_off = max_tiles;
   L.n_counters = (int64_t)max_tiles + (int64_t)batch * c.n_kv_heads;
   L.counters = take((size_t)L.n_counters * sizeof(int32_t));
-  // attention: keys per wave, doubled from 64 until the (sequence, kv head,
-  // span) items stop exceeding ~2K waves
-  L.span = 64;
-  while ((int64_t)batch * c.n_kv_heads * ((capacity + L.span - 1) / L.span) > 2048 &&
-         L.span < kMaxCapacity)
-    L.span *= 2;
-  L.max_spans = (capacity + L.span - 1) / L.span;
+  L.max_chunks = (capacity + kAttnChunk - 1) / kAttnChunk;
   const size_t qn = (size_t)(c.n_heads / c.n_kv_heads) * n_slots;
-  const size_t nparts = (size_t)batch * c.n_kv_heads * L.max_spans * qn;
+  const size_t nparts = (size_t)batch * c.n_kv_heads * L.max_chunks * qn;
   L.part_o = take(nparts * c.head_dim * sizeof(float));
   L.part_ml = take(nparts * sizeof(float2));
   L.tile_ms = take((size_t)s.head.n_tiles * M * sizeof(float2));
@@ -170,47 +187,43 @@ msd_status check_block(const msd_model* m, const msd_block* blk) {
   return MSD_OK;
 }
 
-GemmArgs gemm_base(const msd_model* m, const Shapes& s, const Layout& L, char* ws, int M) {
+GemmArgs gemm_base(const msd_model* m, const Layout& L, char* ws, int M, const GemmShape& sh, int N) {
   GemmArgs g{};
   g.M = M;
+  g.MT = L.MT;
+  g.K = sh.K;
+  g.N = N;
+  g.n_tiles = sh.n_tiles;
+  g.splits = sh.splits;
+  g.waves = sh.waves;
   g.partial = reinterpret_cast<float*>(ws + L.partial);
   g.counters = reinterpret_cast<int32_t*>(ws + L.counters);
   g.n_heads = m->cfg.n_heads;
   g.n_kv_heads = m->cfg.n_kv_heads;
   g.head_dim = m->cfg.head_dim;
-  g.weights_nt = m->weights_nt;
-  (void)s;
   return g;
 }
 
-void set_shape(GemmArgs& g, const GemmShape& sh, int N) {
-  g.n_tiles = sh.n_tiles;
-  g.K = sh.K;
-  g.splits = sh.splits;
-  g.N = N;
-}
-
-// the pre-norm applied while the GEMM loads A = x
-void set_prenorm(GemmArgs& g, const msd_model* m, const float2* stats, int stats_tiles,
-                 const uint16_t* gain, const uint16_t* shift) {
-  g.a_norm = m->cfg.norm == MSD_NORM_LAYER ? 2 : 1;
-  g.a_stats = stats;
-  g.a_stats_tiles = stats_tiles;
-  g.a_g = gain;
-  g.a_b = m->cfg.norm == MSD_NORM_LAYER ? shift : nullptr;
-  g.a_eps = m->cfg.norm_eps;
+// the pre-norm of a GEMM's input, applied in its epilogue
+RowNorm prenorm(const msd_model* m, const float2* stats, const float* col_g, const float* col_b) {
+  RowNorm n{};
+  n.kind = m->cfg.norm == MSD_NORM_LAYER ? 2 : 1;
+  n.stats = stats;
+  n.tiles = m->cfg.d_model / kTileN;
+  n.eps = m->cfg.norm_eps;
+  n.col_g = col_g;
+  n.col_b = col_b;
+  return n;
 }
 
 // final norm + LM head + per-row merge (used at the early exit and at the end)
 msd_status run_head(const msd_model* m, const Shapes& s, const Layout& L, char* ws, int M,
-                    const float* x, const float2* stats, int stats_tiles, int kappa,
-                    float* logits, int32_t* ids, float* logp, int32_t* argmax, float* lse,
-                    hipStream_t stream) {
+                    const float2* stats, int kappa, float* logits, int32_t* ids, float* logp,
+                    int32_t* argmax, float* lse, hipStream_t stream) {
   const msd_model_config& c = m->cfg;
-  GemmArgs g = gemm_base(m, s, L, ws, M);
-  set_shape(g, s.head, c.vocab);
-  g.A = x;
-  set_prenorm(g, m, stats, stats_tiles, T(m, MSD_T_FINAL_G), T(m, MSD_T_FINAL_B));
+  GemmArgs g = gemm_base(m, L, ws, M, s.head, c.vocab);
+  g.a_img = reinterpret_cast<const uint16_t*>(ws + L.img_f);
+  g.norm = prenorm(m, stats, m->head_c, m->head_e);
   g.map = MAP_PLAIN;
   g.w0 = head_w(m);
   g.logits = logits;
@@ -309,7 +322,66 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
     const int v = atoi(e);
     if (v > 0) m->target_wgs = v;
   }
-  if (const char* e = getenv("MSD_WEIGHTS_NT")) m->weights_nt = atoi(e) != 0;
+  if (const char* e = getenv("MSD_GEMM_WAVES")) {
+    const int v = atoi(e);
+    if (v == 4 || v == 8) m->waves = v;
+  }
+
+  // LayerNorm models: column sums c = W g and e = W b of every matrix that
+  // consumes a LayerNorm output (q/k/v, the FFN up projections, the LM head),
+  // from the row-major weights before they are rearranged
+  if (ln) {
+    const int qd = c.n_heads * c.head_dim, kd = c.n_kv_heads * c.head_dim;
+    const size_t n_qkv = (size_t)qd + 2 * kd;
+    const size_t n_up = (size_t)(c.act == MSD_ACT_SWIGLU ? 2 : 1) * c.d_ffn;
+    const size_t per_layer = 2 * (n_qkv + n_up);
+    const size_t total = per_layer * c.n_layers + 2 * (size_t)c.vocab;
+    hipError_t e = hipMalloc(&m->colsums, total * sizeof(float));
+    float* p = m->colsums;
+    for (int l = 0; e == hipSuccess && l < c.n_layers; ++l) {
+      float* qc = p;
+      float* qe = p + n_qkv;
+      float* uc = p + 2 * n_qkv;
+      float* ue = uc + n_up;
+      p += per_layer;
+      m->qkv_c.push_back(qc);
+      m->qkv_e.push_back(qe);
+      m->up_c.push_back(uc);
+      m->up_e.push_back(ue);
+      const uint16_t* ag = LT(m, l, MSD_L_ATTN_G);
+      const uint16_t* ab = LT(m, l, MSD_L_ATTN_B);
+      const uint16_t* mg = LT(m, l, MSD_L_MLP_G);
+      const uint16_t* mb = LT(m, l, MSD_L_MLP_B);
+      e = launch_colsum(LT(m, l, MSD_L_WQ), qd, c.d_model, ag, ab, qc, qe, 0);
+      if (e == hipSuccess) e = launch_colsum(LT(m, l, MSD_L_WK), kd, c.d_model, ag, ab, qc + qd, qe + qd, 0);
+      if (e == hipSuccess)
+        e = launch_colsum(LT(m, l, MSD_L_WV), kd, c.d_model, ag, ab, qc + qd + kd, qe + qd + kd, 0);
+      if (c.act == MSD_ACT_SWIGLU) {
+        if (e == hipSuccess) e = launch_colsum(LT(m, l, MSD_L_W_GATE), c.d_ffn, c.d_model, mg, mb, uc, ue, 0);
+        if (e == hipSuccess)
+          e = launch_colsum(LT(m, l, MSD_L_W_UP), c.d_ffn, c.d_model, mg, mb, uc + c.d_ffn, ue + c.d_ffn, 0);
+      } else if (e == hipSuccess) {
+        e = launch_colsum(LT(m, l, MSD_L_W_UP), c.d_ffn, c.d_model, mg, mb, uc, ue, 0);
+      }
+    }
+    if (e == hipSuccess) {
+      m->head_c = p;
+      m->head_e = p + c.vocab;
+      e = launch_colsum(head_w(m), c.vocab, c.d_model, T(m, MSD_T_FINAL_G), T(m, MSD_T_FINAL_B), p,
+                        p + c.vocab, 0);
+    }
+    if (e == hipSuccess) e = hipStreamSynchronize(0);
+    if (e != hipSuccess) {
+      if (m->colsums) (void)hipFree(m->colsums);
+      delete m;
+      return fail(MSD_ERR_HIP, std::string("layer-norm column sums: ") + hipGetErrorString(e));
+    }
+  } else {
+    m->qkv_c.assign(c.n_layers, nullptr);
+    m->qkv_e.assign(c.n_layers, nullptr);
+    m->up_c.assign(c.n_layers, nullptr);
+    m->up_e.assign(c.n_layers, nullptr);
+  }
 
   // every projection matrix goes fragment-major, in place, through one
   // temporary buffer as large as the largest matrix
@@ -346,6 +418,7 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
     if (e == hipSuccess) e = hipStreamSynchronize(0);
     if (tmp) (void)hipFree(tmp);
     if (e != hipSuccess) {
+      if (m->colsums) (void)hipFree(m->colsums);
       delete m;
       return fail(MSD_ERR_HIP, std::string("weight repack: ") + hipGetErrorString(e));
     }
@@ -363,6 +436,7 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
     if (e == hipSuccess) e = hipMemcpy(m->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       if (m->rope) (void)hipFree(m->rope);
+      if (m->colsums) (void)hipFree(m->colsums);
       delete m;
       return fail(MSD_ERR_HIP, std::string("rotary table: ") + hipGetErrorString(e));
     }
@@ -374,6 +448,7 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
 void msd_model_destroy(msd_model* m) {
   if (!m) return;
   if (m->rope) (void)hipFree(m->rope);
+  if (m->colsums) (void)hipFree(m->colsums);
   delete m;
 }
 
@@ -407,49 +482,53 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
   if (st != MSD_OK) return st;
   const Layout L = layout(m, blk->batch, blk->n_slots, kappa, kv->capacity);
   if (!ws || ws_bytes < L.total) return fail(MSD_ERR_WORKSPACE, "workspace too small");
-  const Shapes s = shapes(m);
-  char* w = static_cast<char*>(ws);
   const int M = blk->batch * blk->n_slots;
+  const Shapes s = shapes(m, M);
+  char* w = static_cast<char*>(ws);
   const int d = c.d_model, qd = c.n_heads * c.head_dim;
   float* x = reinterpret_cast<float*>(w + L.x);
   float2* stats = reinterpret_cast<float2*>(w + L.stats);
-  const int resid_tiles = d / kTileN;
   float* q = reinterpret_cast<float*>(w + L.q);
-  float* att = reinterpret_cast<float*>(w + L.attn);
-  float* act = reinterpret_cast<float*>(w + L.act);
+  uint16_t* img_x = reinterpret_cast<uint16_t*>(w + L.img_x);
+  uint16_t* img_h = reinterpret_cast<uint16_t*>(w + L.img_h);
+  uint16_t* img_f = reinterpret_cast<uint16_t*>(w + L.img_f);
+  uint16_t* img_attn = reinterpret_cast<uint16_t*>(w + L.img_attn);
+  uint16_t* img_act = reinterpret_cast<uint16_t*>(w + L.img_act);
   int32_t* counters = reinterpret_cast<int32_t*>(w + L.counters);
   const size_t layer_elems = (size_t)kv->batch_cap * c.n_kv_heads * kv->capacity * c.head_dim;
 
-  EmbedArgs ea{};
-  ea.tokens = blk->tokens;
-  ea.embed = T(m, MSD_T_EMBED);
-  ea.pos_embed = T(m, MSD_T_POS_EMBED);
-  ea.embed_frag = c.tied_head;
-  ea.len = kv->len;
-  ea.M = M;
-  ea.d = d;
-  ea.n_slots = blk->n_slots;
-  ea.max_positions = c.max_positions;
-  ea.vocab = c.vocab;
-  ea.status = kv->status;
-  ea.x = x;
-  ea.stats = stats;
-  ea.zero_i32 = counters;
-  ea.n_zero = L.n_counters;
-  for (int i = 0; i < kMaxSlots; ++i) ea.depth[i] = topo.depth[i];
-  MSD_HIP(launch_embed(ea, stream));
+  // block rows: residual, statistics and the first attention input image;
+  // also clears the counters and the padding rows of the attention image
+  RowsArgs ra{};
+  ra.tokens = blk->tokens;
+  ra.embed = T(m, MSD_T_EMBED);
+  ra.pos_embed = T(m, MSD_T_POS_EMBED);
+  ra.embed_frag = c.tied_head;
+  ra.len = kv->len;
+  ra.M = M;
+  ra.MT = L.MT;
+  ra.d = d;
+  ra.n_slots = blk->n_slots;
+  ra.max_positions = c.max_positions;
+  ra.vocab = c.vocab;
+  ra.status = kv->status;
+  ra.x = x;
+  ra.stats = stats;
+  ra.img = ImageOut{img_x, LT(m, 0, MSD_L_ATTN_G)};
+  ra.zero_img = img_attn;
+  ra.zero_img_k = qd;
+  ra.zero_i32 = counters;
+  ra.n_zero = L.n_counters;
+  for (int i = 0; i < kMaxSlots; ++i) ra.depth[i] = topo.depth[i];
+  MSD_HIP(launch_rows(ra, stream));
 
   for (int l = 0; l < c.n_layers; ++l) {
     uint16_t* kc = static_cast<uint16_t*>(kv->k) + (size_t)l * layer_elems;
     uint16_t* vc = static_cast<uint16_t*>(kv->v) + (size_t)l * layer_elems;
 
-    // the residual stream's row statistics come from the embedding (layer 0)
-    // or from the previous layer's down projection
-    const int st_tiles = l == 0 ? 1 : resid_tiles;
-    GemmArgs g = gemm_base(m, s, L, w, M);
-    set_shape(g, s.qkv, (c.n_heads + 2 * c.n_kv_heads) * c.head_dim);
-    g.A = x;
-    set_prenorm(g, m, stats, st_tiles, LT(m, l, MSD_L_ATTN_G), LT(m, l, MSD_L_ATTN_B));
+    GemmArgs g = gemm_base(m, L, w, M, s.qkv, qd + 2 * c.n_kv_heads * c.head_dim);
+    g.a_img = img_x;
+    g.norm = prenorm(m, stats, m->qkv_c[l], m->qkv_e[l]);
     g.map = MAP_QKV;
     g.w0 = LT(m, l, MSD_L_WQ);
     g.w1 = LT(m, l, MSD_L_WK);
@@ -457,7 +536,7 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
     g.b0 = LT(m, l, MSD_L_BQ);
     g.b1 = LT(m, l, MSD_L_BK);
     g.b2 = LT(m, l, MSD_L_BV);
-    g.out_f32 = q;
+    g.q_out = q;
     g.k_cache = kc;
     g.v_cache = vc;
     g.len = kv->len;
@@ -477,47 +556,46 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
     aa.v_cache = vc;
     aa.len = kv->len;
     aa.status = kv->status;
-    aa.out = att;
+    aa.out_img = img_attn;
+    aa.MT = L.MT;
     aa.part_o = reinterpret_cast<float*>(w + L.part_o);
     aa.part_ml = reinterpret_cast<float*>(w + L.part_ml);
+    aa.counters = counters + L.attn_counter_off;
     aa.batch = blk->batch;
     aa.n_heads = c.n_heads;
     aa.n_kv_heads = c.n_kv_heads;
     aa.capacity = kv->capacity;
     aa.n_slots = blk->n_slots;
-    aa.span = L.span;
-    aa.max_spans = L.max_spans;
+    aa.max_chunks = L.max_chunks;
     aa.scale = 1.0f / std::sqrt((float)c.head_dim);
     aa.topo = topo;
     MSD_HIP(prof_mark(m, MSD_K_ATTN, l, true, stream));
     MSD_HIP(launch_attention(c.head_dim, aa, stream));
     MSD_HIP(prof_mark(m, MSD_K_ATTN, l, false, stream));
 
-    g = gemm_base(m, s, L, w, M);
-    set_shape(g, s.o, d);
-    g.A = att;
+    g = gemm_base(m, L, w, M, s.o, d);
+    g.a_img = img_attn;
     g.map = MAP_PLAIN;
     g.w0 = LT(m, l, MSD_L_WO);
     g.b0 = LT(m, l, MSD_L_BO);
     g.x = x;
     g.stats_out = stats;
+    g.img_out[0] = ImageOut{img_h, LT(m, l, MSD_L_MLP_G)};
     MSD_HIP(prof_mark(m, MSD_K_OPROJ, l, true, stream));
     MSD_HIP(launch_gemm(EPI_RESID, g, stream));
     MSD_HIP(prof_mark(m, MSD_K_OPROJ, l, false, stream));
 
-    g = gemm_base(m, s, L, w, M);
-    g.A = x;
-    set_prenorm(g, m, stats, resid_tiles, LT(m, l, MSD_L_MLP_G), LT(m, l, MSD_L_MLP_B));
-    g.out_f32 = act;
+    g = gemm_base(m, L, w, M, s.up, c.act == MSD_ACT_SWIGLU ? 2 * c.d_ffn : c.d_ffn);
+    g.a_img = img_h;
+    g.norm = prenorm(m, stats, m->up_c[l], m->up_e[l]);
+    g.act_img = img_act;
     MSD_HIP(prof_mark(m, MSD_K_FFN_UP, l, true, stream));
     if (c.act == MSD_ACT_SWIGLU) {
-      set_shape(g, s.up, 2 * c.d_ffn);
       g.map = MAP_GATEUP;
       g.w0 = LT(m, l, MSD_L_W_GATE);
       g.w1 = LT(m, l, MSD_L_W_UP);
       MSD_HIP(launch_gemm(EPI_SWIGLU, g, stream));
     } else {
-      set_shape(g, s.up, c.d_ffn);
       g.map = MAP_PLAIN;
       g.w0 = LT(m, l, MSD_L_W_UP);
       g.b0 = LT(m, l, MSD_L_B_UP);
@@ -525,28 +603,28 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
     }
     MSD_HIP(prof_mark(m, MSD_K_FFN_UP, l, false, stream));
 
-    g = gemm_base(m, s, L, w, M);
-    set_shape(g, s.down, d);
-    g.A = act;
+    const bool ee_here = ee && l + 1 == ee->layer;
+    g = gemm_base(m, L, w, M, s.down, d);
+    g.a_img = img_act;
     g.map = MAP_PLAIN;
     g.w0 = LT(m, l, MSD_L_W_DOWN);
     g.b0 = LT(m, l, MSD_L_B_DOWN);
     g.x = x;
     g.stats_out = stats;
+    if (l + 1 < c.n_layers) g.img_out[0] = ImageOut{img_x, LT(m, l + 1, MSD_L_ATTN_G)};
+    if (ee_here || l + 1 == c.n_layers) g.img_out[1] = ImageOut{img_f, T(m, MSD_T_FINAL_G)};
     MSD_HIP(prof_mark(m, MSD_K_FFN_DOWN, l, true, stream));
     MSD_HIP(launch_gemm(EPI_RESID, g, stream));
     MSD_HIP(prof_mark(m, MSD_K_FFN_DOWN, l, false, stream));
 
-    if (ee && l + 1 == ee->layer) {
-      st = run_head(m, s, L, w, M, x, stats, resid_tiles, ee->kappa, nullptr, ee->ids, ee->logp,
-                    nullptr, nullptr, stream);
+    if (ee_here) {
+      st = run_head(m, s, L, w, M, stats, ee->kappa, nullptr, ee->ids, ee->logp, nullptr, nullptr,
+                    stream);
       if (st != MSD_OK) return st;
       if (ee->ready) MSD_HIP(hipEventRecord(ee->ready, stream));
     }
   }
-  (void)qd;
-  return run_head(m, s, L, w, M, x, stats, resid_tiles, 1, logits, nullptr, nullptr, argmax, lse,
-                  stream);
+  return run_head(m, s, L, w, M, stats, 1, logits, nullptr, nullptr, argmax, lse, stream);
 }
 
 msd_status msd_early_exit_topk(const msd_model* m, const float* hidden, int32_t M, int32_t kappa,
@@ -555,17 +633,28 @@ msd_status msd_early_exit_topk(const msd_model* m, const float* hidden, int32_t 
   if (!m || !hidden || !ids || !logp) return fail(MSD_ERR_INVALID_ARG, "null argument");
   if (M < 1 || M > kMaxMT * 16) return fail(MSD_ERR_SHAPE, "M must lie in [1, 144]");
   if (kappa < 1 || kappa > kMaxKappa) return fail(MSD_ERR_INVALID_ARG, "kappa out of [1, 32]");
+  if (!aligned16(hidden)) return fail(MSD_ERR_INVALID_ARG, "hidden must be 16-byte aligned");
   const Layout L = layout(m, 1, M, kappa, 1);
   if (!ws || ws_bytes < L.total) return fail(MSD_ERR_WORKSPACE, "workspace too small");
-  const Shapes s = shapes(m);
+  const Shapes s = shapes(m, M);
   char* w = static_cast<char*>(ws);
-  // the head GEMM's split-K counters must start at zero (a kernel, not a
-  // memset node, so the call stays safe under graph capture)
-  MSD_HIP(launch_zero_i32(reinterpret_cast<int32_t*>(w + L.counters), L.n_counters, stream));
   float2* stats = reinterpret_cast<float2*>(w + L.stats);
-  MSD_HIP(launch_row_stats(hidden, M, m->cfg.d_model, stats, stream));
-  return run_head(m, s, L, w, M, hidden, stats, 1, kappa, nullptr, ids, logp, nullptr, nullptr,
-                  stream);
+  // statistics and final-norm image of the given rows; clears the head
+  // GEMM's split-K counters (a kernel, not a memset node, so the call stays
+  // safe under graph capture)
+  RowsArgs ra{};
+  ra.hidden = hidden;
+  ra.M = M;
+  ra.MT = L.MT;
+  ra.d = m->cfg.d_model;
+  ra.n_slots = M;
+  ra.vocab = m->cfg.vocab;
+  ra.stats = stats;
+  ra.img = ImageOut{reinterpret_cast<uint16_t*>(w + L.img_f), T(m, MSD_T_FINAL_G)};
+  ra.zero_i32 = reinterpret_cast<int32_t*>(w + L.counters);
+  ra.n_zero = L.n_counters;
+  MSD_HIP(launch_rows(ra, stream));
+  return run_head(m, s, L, w, M, stats, kappa, nullptr, ids, logp, nullptr, nullptr, stream);
 }
 
 msd_status msd_accept(const msd_model* m, const msd_block* blk, const float* logits,

@@ -1,94 +1,127 @@
-// Row-wise kernels of the verification pass: embedding gather (with the row
-// statistics the first pre-norm needs) and the per-row merge of the LM-head
-// tiles (top-kappa, argmax, logsumexp).
+// Row-wise kernels of the verification pass: the block rows (embedding gather
+// or a given residual) as residual, 64-column statistics and activation
+// image; the per-row merge of the LM-head tiles (top-kappa, argmax,
+// logsumexp).
 #include "kernels.h"
 
 namespace msd {
 namespace {
 
-// Fixed-order block sum (256 threads): butterfly inside each wave, then the
-// four wave sums in wave order. Same result for the same inputs, always.
-__device__ float block_sum(float v, float* sh) {
-  v = wave_sum(v);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) sh[wave] = v;
-  __syncthreads();
-  float r = 0.0f;
-  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) r += sh[w];
-  return r;
-}
-
-// (mean, M2) of one row, two passes, fixed-order block sums.
-__device__ void row_stats(const float* x, int d, float2* out, float* sh) {
-  float s = 0.0f;
-  for (int k = threadIdx.x; k < d; k += blockDim.x) s += x[k];
-  const float mean = block_sum(s, sh) / (float)d;
-  float v = 0.0f;
-  for (int k = threadIdx.x; k < d; k += blockDim.x) {
-    const float c = x[k] - mean;
-    v += c * c;
+// Zero the image lanes of padding row m (K columns).
+__device__ void zero_image_row(uint16_t* img, int K, int m, int MT) {
+  const int mt = m >> 4, r16 = m & 15;
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  for (int i = threadIdx.x; i < (K >> 5) * 4; i += blockDim.x) {
+    const int ks = i >> 2, g = i & 3;
+    uint16_t* dst = img + img_offset(ks, mt, MT, 16 * g + r16);
+    *reinterpret_cast<u32x4*>(dst) = z;
+    *reinterpret_cast<u32x4*>(dst + 512) = z;
   }
-  const float m2 = block_sum(v, sh);
-  if (threadIdx.x == 0) *out = make_float2(mean, m2);
 }
 
-__global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
-  __shared__ float sh[8];
+// One workgroup per row (16 MT of them; rows past M only clear their image
+// lanes). Thread tt owns columns [64 tt, 64 tt + 64) of the row: it gathers
+// them (embedding row, plus the learned position row, or a given fp32 hidden
+// row), stores the fp32 residual, the (mean, M2) of its 64 values (two
+// passes in registers) and its two image k-steps (values times the gain of
+// the next pre-norm, split into bf16 hi + lo).
+__global__ __launch_bounds__(256) void rows_kernel(RowsArgs a) {
   const int m = blockIdx.x;
-  // clear the split-K / merge counters of this pass
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.n_zero;
        i += (int64_t)gridDim.x * blockDim.x)
     a.zero_i32[i] = 0;
-  int tok = a.tokens[m];
-  if (tok < 0 || tok >= a.vocab) {
-    if (threadIdx.x == 0) atomicOr(a.status, 4u);
-    tok = 0;
+  if (m >= a.M) {
+    if (a.img.img) zero_image_row(a.img.img, a.d, m, a.MT);
+    if (a.zero_img) zero_image_row(a.zero_img, a.zero_img_k, m, a.MT);
+    return;
   }
-  const uint16_t* e = a.embed + (size_t)tok * a.d;
-  const uint16_t* p = nullptr;
-  if (a.pos_embed) {
-    const int b = m / a.n_slots, slot = m - b * a.n_slots;
-    int pos = a.len[b] + a.depth[slot];
-    if (pos >= a.max_positions) pos = a.max_positions - 1;  // flagged by the cache check
-    p = a.pos_embed + (size_t)pos * a.d;
-  }
-  float* x = a.x + (size_t)m * a.d;
-  if (a.embed_frag) {
-    // row tok of a fragment-major table: 8 consecutive columns per 16 bytes
-    const size_t run = (size_t)(a.d >> 5) * 512;
-    const uint16_t* grp = a.embed + (size_t)(tok >> 4) * run;
-    for (int q = threadIdx.x; q < (a.d >> 3); q += blockDim.x) {
-      const int ks = q >> 2, lane = (tok & 15) + 16 * (q & 3);
-      const u32x4 w = *reinterpret_cast<const u32x4*>(grp + (size_t)ks * 512 + lane * 8);
-      u32x4 pw = {0u, 0u, 0u, 0u};
-      if (p) pw = *reinterpret_cast<const u32x4*>(p + q * 8);
+  const int tt = threadIdx.x;
+  if (tt >= (a.d >> 6)) return;
+  float v[64];
+  if (a.hidden) {
+    const float4* src = reinterpret_cast<const float4*>(a.hidden + (size_t)m * a.d + 64 * tt);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int k = q * 8 + 2 * i;
-        x[k] = bf_lo(w[i]) + bf_lo(pw[i]);
-        x[k + 1] = bf_hi(w[i]) + bf_hi(pw[i]);
-      }
+    for (int i = 0; i < 16; ++i) {
+      const float4 f = src[i];
+      v[4 * i] = f.x;
+      v[4 * i + 1] = f.y;
+      v[4 * i + 2] = f.z;
+      v[4 * i + 3] = f.w;
     }
   } else {
-    for (int q = threadIdx.x; q < (a.d >> 3); q += blockDim.x) {
-      const u32x4 w = *reinterpret_cast<const u32x4*>(e + q * 8);
-      u32x4 pw = {0u, 0u, 0u, 0u};
-      if (p) pw = *reinterpret_cast<const u32x4*>(p + q * 8);
+    int tok = a.tokens[m];
+    if (tok < 0 || tok >= a.vocab) {
+      if (tt == 0) atomicOr(a.status, 4u);
+      tok = 0;
+    }
+    const uint16_t* p = nullptr;
+    if (a.pos_embed) {
+      const int b = m / a.n_slots, slot = m - b * a.n_slots;
+      int pos = a.len[b] + a.depth[slot];
+      if (pos >= a.max_positions) pos = a.max_positions - 1;  // flagged by the cache check
+      p = a.pos_embed + (size_t)pos * a.d;
+    }
+    u32x4 w[8], pw[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int col = 64 * tt + 8 * c;
+      if (a.embed_frag) {
+        // row tok of a fragment-major table: 8 consecutive columns per 16 bytes
+        const size_t run = (size_t)(a.d >> 5) * 512;
+        const int ks = col >> 5, lane = (tok & 15) + 16 * ((col >> 3) & 3);
+        w[c] = *reinterpret_cast<const u32x4*>(a.embed + (size_t)(tok >> 4) * run + (size_t)ks * 512 +
+                                               lane * 8);
+      } else {
+        w[c] = *reinterpret_cast<const u32x4*>(a.embed + (size_t)tok * a.d + col);
+      }
+      pw[c] = p ? *reinterpret_cast<const u32x4*>(p + col) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        x[q * 8 + 2 * i] = bf_lo(w[i]) + bf_lo(pw[i]);
-        x[q * 8 + 2 * i + 1] = bf_hi(w[i]) + bf_hi(pw[i]);
+        v[8 * c + 2 * i] = bf_lo(w[c][i]) + bf_lo(pw[c][i]);
+        v[8 * c + 2 * i + 1] = bf_hi(w[c][i]) + bf_hi(pw[c][i]);
       }
-    }
   }
-  __syncthreads();
-  row_stats(x, a.d, a.stats + m, sh);
-}
-
-__global__ __launch_bounds__(256) void row_stats_kernel(const float* x, int d, float2* stats) {
-  __shared__ float sh[8];
-  row_stats(x + (size_t)blockIdx.x * d, d, stats + blockIdx.x, sh);
+  if (a.x) {
+    float4* dst = reinterpret_cast<float4*>(a.x + (size_t)m * a.d + 64 * tt);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) dst[i] = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+  }
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 64; ++i) sum += v[i];
+  const float mean = sum * (1.0f / 64.0f);
+  float m2 = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 64; ++i) {
+    const float dv = v[i] - mean;
+    m2 += dv * dv;
+  }
+  a.stats[(size_t)tt * a.M + m] = make_float2(mean, m2);
+  if (a.img.img) {
+    const int mt = m >> 4, r16 = m & 15;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float e8[8];
+        const int c0 = 32 * h + 8 * g;
+        u32x4 gw = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};  // bf16 ones
+        if (a.img.gain) gw = *reinterpret_cast<const u32x4*>(a.img.gain + 64 * tt + c0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          e8[2 * i] = v[c0 + 2 * i] * bf_lo(gw[i]);
+          e8[2 * i + 1] = v[c0 + 2 * i + 1] * bf_hi(gw[i]);
+        }
+        u32x4 hw, lw;
+        split8_words(e8, hw, lw);
+        uint16_t* dst = a.img.img + img_offset(2 * tt + h, mt, a.MT, 16 * g + r16);
+        *reinterpret_cast<u32x4*>(dst) = hw;
+        *reinterpret_cast<u32x4*>(dst + 512) = lw;
+      }
+  }
 }
 
 // (max, sum exp) pair merge: the pair describes sum_i exp(v_i) = s * exp(m).
@@ -195,13 +228,9 @@ hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(embed_kernel, dim3(a.M), dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_row_stats(const float* x, int M, int d, float2* stats, hipStream_t s) {
-  hipLaunchKernelGGL(row_stats_kernel, dim3(M), dim3(256), 0, s, x, d, stats);
+hipError_t launch_rows(const RowsArgs& a, hipStream_t s) {
+  if (a.d % 64 || a.d > 64 * 256 || a.M < 1 || a.M > 16 * a.MT) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rows_kernel, dim3(16 * a.MT), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
