@@ -4,24 +4,24 @@
 // registers). GQA: query head h reads kv head h / (H / H_kv).
 //
 // Flash-decoding over 256-key chunks: a workgroup owns one (sequence, kv
-// head, chunk) and each of its 4 waves one 64-key block of the chunk. A wave
-// loads its block's K (as MFMA operands) and V (staged transposed in its own
-// LDS) once, then serves every query tile of the kv head's group:
+// head, chunk) and each of its 4 waves one 64-key block. A wave loads its
+// block's K as MFMA operands and V rows into its own LDS (16-byte writes, read
+// back transposed two bytes at a time with conflict-free strides) once, then
+// serves the kv head's GQA query tiles, up to three per pass:
 //   S^T[key][query] = K Q^T        MFMA 16x16x32; Q (fp32) as bf16 hi + lo;
 //   block softmax statistics       one query per lane column: 2 shuffles;
-//   O[query][d] = P V              P stays in registers as the MFMA operand.
+//   O[query][d] += P V             P stays in registers as the MFMA operand.
 // The 4 waves' (max, sum, output) are merged in LDS in wave order. A chunk
 // that covers the whole sequence writes the normalised output straight into
 // the output-projection's activation image; otherwise chunks publish their
-// partials and the last chunk to arrive merges them in chunk order. All
-// statistics in fp32; no floating-point atomics.
+// partials and a second kernel merges them in chunk order. All statistics
+// in fp32; no floating-point atomics.
 #include "kernels.h"
 
 namespace msd {
 namespace {
 
-constexpr int kVtStride = 64 + 8;  // bf16 per LDS row of V^T (64 keys + pad)
-constexpr int kQG = 2;             // query tiles per pass
+constexpr int kQG = 3;  // query tiles per pass (one pass for G * n_slots <= 48)
 
 // image write of 8 consecutive output dims [8 c8, 8 c8 + 8) of query qg
 template <int HD>
@@ -40,14 +40,25 @@ __device__ __forceinline__ void write_out(const AttnArgs& a, int b, int kvh, int
 }
 
 template <int HD>
+struct AttnLds {
+  static constexpr int kVS = HD + 4;  // bf16 per LDS row of V (one key), conflict-free strides
+  static constexpr int kOS = HD + 4;  // floats per LDS row of a wave's output
+  static constexpr int kVBytes = 64 * kVS * 2;
+  static constexpr int kOBytes = kQG * 16 * kOS * 4;
+  static constexpr int kRegion = kVBytes > kOBytes ? kVBytes : kOBytes;
+};
+
+template <int HD>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+  using Lds = AttnLds<HD>;
   constexpr int KSTEPS = HD / 32;
   constexpr int DSUB = HD / 16;
   constexpr int C8 = HD / 8;
-  __shared__ __attribute__((aligned(16))) uint16_t vt_all[4][HD][kVtStride];
+  constexpr int VIT = HD / 8;    // 16-byte V chunks per lane per 64-key block
+  constexpr int KPI = 512 / HD;  // keys per V chunk iteration
+  __shared__ __attribute__((aligned(16))) unsigned char region_all[4][Lds::kRegion];
   __shared__ float ml_sh[4][kQG * 16][2];
-  __shared__ __attribute__((aligned(16))) float o_sh[4][kQG * 16][HD + 4];
-  __shared__ int s_last;
+  __shared__ __attribute__((aligned(16))) uint16_t qs[kQG * KSTEPS * 2 * 512];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
@@ -61,7 +72,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
   const int nch = (T + kAttnChunk - 1) / kAttnChunk;
   if (c >= nch) return;
-  uint16_t (*vt)[kVtStride] = vt_all[wave];
+  uint16_t* vs = reinterpret_cast<uint16_t*>(region_all[wave]);  // [64 keys][kVS]
+  float* os = reinterpret_cast<float*>(region_all[wave]);        // [48 queries][kOS]
   const int G = a.n_heads / a.n_kv_heads;
   const int Qn = G * ns;
   const int QT = (Qn + 15) >> 4;
@@ -69,12 +81,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const uint16_t* kbase = a.k_cache + row0 * HD;
   const uint16_t* vbase = a.v_cache + row0 * HD;
   const int k0 = c * kAttnChunk + 64 * wave;
-  const int key_hi = min(T, k0 + 64);  // keys [k0, key_hi) of this wave (maybe none)
+  const int key_hi = min(T, k0 + 64);  // this wave's keys [k0, key_hi), maybe none
 
-  // this wave's K fragments and V^T, loaded once (rows clamped to a valid
-  // key and masked afterwards, so no load waits behind a divergent branch)
-  constexpr int VIT = HD / 8;    // 16-byte V chunks per lane
-  constexpr int KPI = 512 / HD;  // keys per iteration
+  // K fragments and V rows first (rows past the last key clamped to a valid
+  // row; their scores are masked), so that their round trip overlaps the
+  // query staging below
   u32x4 vraw[VIT];
 #pragma unroll
   for (int it = 0; it < VIT; ++it) {
@@ -89,73 +100,96 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk) kf[j][kk] = load16(kbase + (size_t)pos * HD + kk * 32 + g * 8);
   }
-#pragma unroll
-  for (int it = 0; it < VIT; ++it) {
-    const int key = it * KPI + lane / (HD / 8);
-    const int d0 = (lane % (HD / 8)) * 8;
-    const bool live = k0 + key < key_hi;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t w = vraw[it][e >> 1];
-      vt[d0 + e][key] = live ? (uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu)) : (uint16_t)0;
-    }
-  }
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // this wave's V^T is in LDS
-  __builtin_amdgcn_wave_barrier();
+  bf16x8 vb[2][DSUB];
 
   for (int qt0 = 0; qt0 < QT; qt0 += kQG) {
-    bf16x8 qh[kQG][KSTEPS], ql[kQG][KSTEPS];
-    uint64_t anc[kQG];
-    u32x4 qraw[kQG][KSTEPS][2];
-    float qmask[kQG];
-#pragma unroll
-    for (int q = 0; q < kQG; ++q) {
-      const int qv = (qt0 + q) * 16 + r16;
+    // the pass's query tiles as split-bf16 MFMA operands, shared by the
+    // 4 waves through LDS: qs[tile][k-step][hi / lo][lane][8]
+    for (int x = tid; x < kQG * KSTEPS * 64; x += blockDim.x) {
+      const int q = x / (KSTEPS * 64), kk = (x / 64) % KSTEPS, l = x & 63;
+      const int qv = (qt0 + q) * 16 + (l & 15);
       const bool qok = qv < Qn;
       const int gq = qok ? qv / ns : 0;
       const int slot = qok ? qv - gq * ns : 0;
-      const float* qp = a.q + ((size_t)(b * ns + slot) * a.n_heads + kvh * G + gq) * HD + g * 8;
+      const float* qp = a.q + ((size_t)(b * ns + slot) * a.n_heads + kvh * G + gq) * HD + kk * 32 + (l >> 4) * 8;
+      const u32x4 r0 = *reinterpret_cast<const u32x4*>(qp);
+      const u32x4 r1 = *reinterpret_cast<const u32x4*>(qp + 4);
+      const float qm = qok ? 1.0f : 0.0f;
+      float v[8];
 #pragma unroll
-      for (int kk = 0; kk < KSTEPS; ++kk) {
-        qraw[q][kk][0] = *reinterpret_cast<const u32x4*>(qp + kk * 32);
-        qraw[q][kk][1] = *reinterpret_cast<const u32x4*>(qp + kk * 32 + 4);
+      for (int i = 0; i < 4; ++i) {
+        v[i] = __uint_as_float(r0[i]) * qm;
+        v[4 + i] = __uint_as_float(r1[i]) * qm;
       }
-      qmask[q] = qok ? 1.0f : 0.0f;
-      anc[q] = qok ? a.topo.anc[slot] : 0ull;
+      u32x4 hw, lw;
+      split8_words(v, hw, lw);
+      uint16_t* dst = qs + (size_t)((q * KSTEPS + kk) * 2) * 512 + l * 8;
+      *reinterpret_cast<u32x4*>(dst) = hw;
+      *reinterpret_cast<u32x4*>(dst + 512) = lw;
     }
+    if (qt0 == 0) {
+      // V rows into the wave's LDS as they are (16-byte writes), read back as
+      // P V operands: lane l takes dim 16 ds + l%16 of keys 32 kb + 4 g + e
+      // and 32 kb + 16 + 4 g + e (e < 4), the k order of P below
 #pragma unroll
-    for (int q = 0; q < kQG; ++q)
-#pragma unroll
-      for (int kk = 0; kk < KSTEPS; ++kk) {
-        float v[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          v[i] = __uint_as_float(qraw[q][kk][0][i]) * qmask[q];
-          v[4 + i] = __uint_as_float(qraw[q][kk][1][i]) * qmask[q];
-        }
-        split_vals(v, qh[q][kk], ql[q][kk]);
+      for (int it = 0; it < VIT; ++it) {
+        const int key = it * KPI + lane / (HD / 8);
+        *reinterpret_cast<u32x4*>(vs + key * Lds::kVS + (lane % (HD / 8)) * 8) = vraw[it];
       }
+    }
+    __syncthreads();
+    if (qt0 == 0) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int ds = 0; ds < DSUB; ++ds) {
+          const uint16_t* col = vs + 16 * ds + r16;
+          uint16_t e8[8];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            e8[e] = col[(32 * kb + 4 * g + e) * Lds::kVS];
+            e8[4 + e] = col[(32 * kb + 16 + 4 * g + e) * Lds::kVS];
+          }
+          u32x4 w;
+#pragma unroll
+          for (int x = 0; x < 4; ++x) w[x] = (uint32_t)e8[2 * x] | ((uint32_t)e8[2 * x + 1] << 16);
+          vb[kb][ds] = __builtin_bit_cast(bf16x8, w);
+        }
+    }
 
+    float run_m[kQG], run_l[kQG];
+    floatx4 o[kQG][DSUB];
 #pragma unroll
     for (int q = 0; q < kQG; ++q) {
+      run_m[q] = -INFINITY;
+      run_l[q] = 0.0f;
+#pragma unroll
+      for (int ds = 0; ds < DSUB; ++ds) o[q][ds] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int q = 0; q < kQG; ++q) {
+      const int qv = (qt0 + q) * 16 + r16;
+      if ((qt0 + q) * 16 >= Qn) break;
+      const uint64_t anc = qv < Qn ? a.topo.anc[qv % ns] : 0ull;
       floatx4 sc[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         sc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; ++kk) {
-          sc[j] = mfma16x16x32(kf[j][kk], qh[q][kk], sc[j]);
-          sc[j] = mfma16x16x32(kf[j][kk], ql[q][kk], sc[j]);
+          const uint16_t* qf = qs + (size_t)((q * KSTEPS + kk) * 2) * 512 + lane * 8;
+          sc[j] = mfma16x16x32(kf[j][kk], load16(qf), sc[j]);
+          sc[j] = mfma16x16x32(kf[j][kk], load16(qf + 512), sc[j]);
         }
       }
-      // lane holds S^T[key 16j + 4g + r][query r16]: scale, mask, block max
+      // lane holds S^T[key 16j + 4g + r][query r16]: scale, mask, softmax
       float mx = -INFINITY;
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int pos = k0 + 16 * j + 4 * g + r;
-          const bool vis = pos < key_hi && (pos < L || ((anc[q] >> (pos - L)) & 1ull));
+          const bool vis = pos < key_hi && (pos < L || ((anc >> (pos - L)) & 1ull));
           sc[j][r] = vis ? sc[j][r] * a.scale : -INFINITY;
           mx = fmaxf(mx, sc[j][r]);
         }
@@ -172,60 +206,61 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         }
       ls += __shfl_xor(ls, 16);
       ls += __shfl_xor(ls, 32);
-      floatx4 o[DSUB];
-#pragma unroll
-      for (int ds = 0; ds < DSUB; ++ds) o[ds] = floatx4{0.f, 0.f, 0.f, 0.f};
+      run_l[q] = ls;
+      run_m[q] = mx;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         // P as bf16 hi + lo (k order: keys 4g+r of the two 16-key tiles)
         u32x4 ph, pl;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float p0 = sc[2 * kb + (i >> 1)][2 * (i & 1)];
-          const float p1 = sc[2 * kb + (i >> 1)][2 * (i & 1) + 1];
-          ph[i] = pack_bf16x2(p0, p1);
-          pl[i] = pack_bf16x2(p0 - bf_lo(ph[i]), p1 - bf_hi(ph[i]));
+        for (int x = 0; x < 4; ++x) {
+          const float p0 = sc[2 * kb + (x >> 1)][2 * (x & 1)];
+          const float p1 = sc[2 * kb + (x >> 1)][2 * (x & 1) + 1];
+          ph[x] = pack_bf16x2(p0, p1);
+          pl[x] = pack_bf16x2(p0 - bf_lo(ph[x]), p1 - bf_hi(ph[x]));
         }
         const bf16x8 pah = __builtin_bit_cast(bf16x8, ph);
         const bf16x8 pal = __builtin_bit_cast(bf16x8, pl);
 #pragma unroll
         for (int ds = 0; ds < DSUB; ++ds) {
-          const uint16_t* vrow = &vt[ds * 16 + r16][32 * kb];
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + 4 * g);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16 + 4 * g);
-          const u32x4 vw = {lo[0], lo[1], hi[0], hi[1]};
-          const bf16x8 vb = __builtin_bit_cast(bf16x8, vw);
-          o[ds] = mfma16x16x32(pah, vb, o[ds]);
-          o[ds] = mfma16x16x32(pal, vb, o[ds]);
+          o[q][ds] = mfma16x16x32(pah, vb[kb][ds], o[q][ds]);
+          o[q][ds] = mfma16x16x32(pal, vb[kb][ds], o[q][ds]);
         }
       }
-      // publish to LDS: o D layout rows (queries) 4g + r, column (dim) 16 ds + r16
+    }
+
+    // publish the wave's (max, sum, output) to its LDS region: every wave's
+    // V reads are done once all have passed this barrier
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kQG; ++q) {
 #pragma unroll
       for (int ds = 0; ds < DSUB; ++ds)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) o_sh[wave][q * 16 + 4 * g + r][ds * 16 + r16] = o[ds][r];
+        for (int r = 0; r < 4; ++r) os[(q * 16 + 4 * g + r) * Lds::kOS + ds * 16 + r16] = o[q][ds][r];
       if (g == 0) {
-        ml_sh[wave][q * 16 + r16][0] = mx;
-        ml_sh[wave][q * 16 + r16][1] = ls;
+        ml_sh[wave][q * 16 + r16][0] = run_m[q];
+        ml_sh[wave][q * 16 + r16][1] = run_l[q];
       }
     }
     __syncthreads();
     // merge the 4 waves (wave order), then output or publish the chunk
-    for (int i = tid; i < kQG * 16 * C8; i += blockDim.x) {
-      const int ql = i / C8, c8 = i - ql * C8;
-      const int qg = qt0 * 16 + ql;
+    for (int x = tid; x < kQG * 16 * C8; x += blockDim.x) {
+      const int qloc = x / C8, c8 = x - qloc * C8;
+      const int qg = qt0 * 16 + qloc;
       if (qg >= Qn) continue;
       float M = -INFINITY;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][ql][0]);
+      for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
       float S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        const float mw = ml_sh[w][ql][0];
+        const float mw = ml_sh[w][qloc][0];
         const float f = mw == -INFINITY ? 0.0f : expf(mw - M);
-        S += ml_sh[w][ql][1] * f;
-        const float4 v0 = *reinterpret_cast<const float4*>(&o_sh[w][ql][8 * c8]);
-        const float4 v1 = *reinterpret_cast<const float4*>(&o_sh[w][ql][8 * c8 + 4]);
+        S += ml_sh[w][qloc][1] * f;
+        const float* src = reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 8 * c8;
+        const float4 v0 = *reinterpret_cast<const float4*>(src);
+        const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
         o8[0] += f * v0.x;
         o8[1] += f * v0.y;
         o8[2] += f * v0.z;
@@ -243,61 +278,64 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       } else {
         const size_t pidx = (((size_t)b * a.n_kv_heads + kvh) * a.max_chunks + c) * Qn + qg;
         float* po = a.part_o + pidx * HD + 8 * c8;
-#pragma unroll
-        for (int e = 0; e < 8; e += 2) store_coherent2(po + e, o8[e], o8[e + 1]);
-        if (c8 == 0) store_coherent2(a.part_ml + 2 * pidx, M, S);
+        *reinterpret_cast<float4*>(po) = make_float4(o8[0], o8[1], o8[2], o8[3]);
+        *reinterpret_cast<float4*>(po + 4) = make_float4(o8[4], o8[5], o8[6], o8[7]);
+        if (c8 == 0) reinterpret_cast<float2*>(a.part_ml)[pidx] = make_float2(M, S);
       }
     }
     __syncthreads();
   }
-  if (nch == 1) return;
+}
 
-  // chunk hand-off: the last chunk of this (sequence, kv head) merges all
-  drain_stores();
-  __syncthreads();
-  int32_t* ctr = a.counters + (size_t)b * a.n_kv_heads + kvh;
-  if (tid == 0) s_last = counter_add(ctr, 1) == nch - 1;
-  __syncthreads();
-  if (!s_last) return;
+// Merge of the chunk partials of sequences that span more than one chunk:
+// one thread per (sequence, kv head, query, 8 output dims), chunks in order.
+template <int HD>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+  constexpr int C8 = HD / 8;
+  const int G = a.n_heads / a.n_kv_heads, ns = a.n_slots, Qn = G * ns;
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t per_seq = (int64_t)a.n_kv_heads * Qn * C8;
+  if (x >= (int64_t)a.batch * per_seq) return;
+  const int b = (int)(x / per_seq);
+  int64_t rem = x - b * per_seq;
+  const int kvh = (int)(rem / ((int64_t)Qn * C8));
+  rem -= (int64_t)kvh * Qn * C8;
+  const int qg = (int)(rem / C8), c8 = (int)(rem - (int64_t)qg * C8);
+  const int T = a.len[b] + ns;
+  if (T > a.capacity) return;
+  const int nch = (T + kAttnChunk - 1) / kAttnChunk;
+  if (nch == 1) return;  // the chunk kernel wrote the output directly
   const size_t base = ((size_t)b * a.n_kv_heads + kvh) * a.max_chunks;
-  for (int i = tid; i < Qn * C8; i += blockDim.x) {
-    const int qg = i / C8, c8 = i - qg * C8;
-    float M = -INFINITY, S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int c0 = 0; c0 < nch; c0 += 4) {
-      float pm[4], ps[4], pv[4][8];
+  float M = -INFINITY, S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int c0 = 0; c0 < nch; c0 += 4) {
+    float2 ml[4];
+    float4 v0[4], v1[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int cc = c0 + u < nch ? c0 + u : c0;
-        const size_t pidx = (base + cc) * Qn + qg;
-        const float2 ml = load_coherent2(a.part_ml + 2 * pidx);
-        pm[u] = ml.x;
-        ps[u] = ml.y;
-        const float* po = a.part_o + pidx * HD + 8 * c8;
-#pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const float2 v = load_coherent2(po + e);
-          pv[u][e] = v.x;
-          pv[u][e + 1] = v.y;
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (c0 + u >= nch || pm[u] == -INFINITY) continue;
-        const float Mn = fmaxf(M, pm[u]);
-        const float fa = M == -INFINITY ? 0.0f : expf(M - Mn);
-        const float fb = expf(pm[u] - Mn);
-        S = S * fa + ps[u] * fb;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o8[e] = o8[e] * fa + pv[u][e] * fb;
-        M = Mn;
-      }
+    for (int u = 0; u < 4; ++u) {
+      const int cc = c0 + u < nch ? c0 + u : c0;
+      const size_t pidx = (base + cc) * Qn + qg;
+      ml[u] = reinterpret_cast<const float2*>(a.part_ml)[pidx];
+      const float* po = a.part_o + pidx * HD + 8 * c8;
+      v0[u] = *reinterpret_cast<const float4*>(po);
+      v1[u] = *reinterpret_cast<const float4*>(po + 4);
     }
-    const float inv = S > 0.0f ? 1.0f / S : 0.0f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o8[e] *= inv;
-    write_out<HD>(a, b, kvh, qg, c8, o8);
+    for (int u = 0; u < 4; ++u) {
+      if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
+      const float Mn = fmaxf(M, ml[u].x);
+      const float fa = M == -INFINITY ? 0.0f : expf(M - Mn);
+      const float fb = expf(ml[u].x - Mn);
+      S = S * fa + ml[u].y * fb;
+      const float pv[8] = {v0[u].x, v0[u].y, v0[u].z, v0[u].w, v1[u].x, v1[u].y, v1[u].z, v1[u].w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o8[e] = o8[e] * fa + pv[e] * fb;
+      M = Mn;
+    }
   }
-  if (tid == 0) counter_reset(ctr);
+  const float inv = S > 0.0f ? 1.0f / S : 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o8[e] *= inv;
+  write_out<HD>(a, b, kvh, qg, c8, o8);
 }
 
 }  // namespace
@@ -305,9 +343,18 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s) {
   if (a.max_chunks > kMaxAttnChunks || a.max_chunks < 1) return hipErrorInvalidValue;
   const dim3 grid(a.max_chunks, a.n_kv_heads, a.batch);
-  if (head_dim == 128) hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, s, a);
-  else if (head_dim == 64) hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, s, a);
-  else return hipErrorInvalidValue;
+  const int64_t items = (int64_t)a.batch * a.n_kv_heads * (a.n_heads / a.n_kv_heads) * a.n_slots *
+                        (head_dim / 8);
+  const dim3 mgrid((unsigned)((items + 255) / 256));
+  if (head_dim == 128) {
+    hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, s, a);
+    if (a.max_chunks > 1) hipLaunchKernelGGL(attn_merge_kernel<128>, mgrid, dim3(256), 0, s, a);
+  } else if (head_dim == 64) {
+    hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, s, a);
+    if (a.max_chunks > 1) hipLaunchKernelGGL(attn_merge_kernel<64>, mgrid, dim3(256), 0, s, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -125,7 +125,7 @@ hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
 // ---------------------------------------------------------------------------
 constexpr int kMaxAttnChunks = 128;   // key chunks per (sequence, kv head)
 constexpr int kMaxCapacity = 32768;   // cache positions
-constexpr int kAttnChunk = 256;       // keys per workgroup chunk (4 waves x 64)
+constexpr int kAttnChunk = 256;       // keys per workgroup (4 waves x 64)
 
 struct AttnArgs {
   const float* q;           // fp32 [M][H][hd] (rotated)
@@ -137,9 +137,8 @@ struct AttnArgs {
   int32_t MT;
   float* part_o;            // [batch][Hkv][chunks][Qn][hd]
   float* part_ml;           // [batch][Hkv][chunks][Qn][2] (max, sum exp)
-  int32_t* counters;        // [batch][Hkv]
   int32_t batch, n_heads, n_kv_heads, capacity, n_slots;
-  int32_t max_chunks;
+  int32_t max_chunks;       // 256-key chunks of the longest sequence
   float scale;
   Topo topo;
 };

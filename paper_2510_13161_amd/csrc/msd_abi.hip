@@ -102,7 +102,6 @@ struct Layout {
   size_t x, stats, q, img_x, img_h, img_f, img_attn, img_act, partial, counters, part_o, part_ml,
       tile_ms, tile_top, total;
   int64_t n_counters;
-  int32_t attn_counter_off;  // in int32 units inside counters
   int32_t MT, max_chunks;
 };
 
@@ -141,8 +140,7 @@ Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacit
     }
   }
   L.partial = take(part);
-  L.attn_counter_off = max_tiles;
-  L.n_counters = (int64_t)max_tiles + (int64_t)batch * c.n_kv_heads;
+  L.n_counters = max_tiles;
   L.counters = take((size_t)L.n_counters * sizeof(int32_t));
   L.max_chunks = (capacity + kAttnChunk - 1) / kAttnChunk;
   const size_t qn = (size_t)(c.n_heads / c.n_kv_heads) * n_slots;
@@ -560,7 +558,6 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
     aa.MT = L.MT;
     aa.part_o = reinterpret_cast<float*>(w + L.part_o);
     aa.part_ml = reinterpret_cast<float*>(w + L.part_ml);
-    aa.counters = counters + L.attn_counter_off;
     aa.batch = blk->batch;
     aa.n_heads = c.n_heads;
     aa.n_kv_heads = c.n_kv_heads;
