@@ -151,11 +151,14 @@ struct HeadMergeArgs {
   const float2* tile_ms;
   const uint64_t* tile_top;
   int32_t n_tiles, M, kappa;
+  float2* part_ms;     // [M][parts] (parts = head_parts(n_tiles))
+  uint64_t* part_top;  // [M][parts][kappa]
   int32_t* ids;    // [M][kappa] or null
   float* logp;     // [M][kappa] or null
   int32_t* argmax; // [M] or null
   float* lse;      // [M] or null
 };
+int head_parts(int n_tiles);  // 256 tiles per part, at most 64 parts
 hipError_t launch_head_merge(const HeadMergeArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------

@@ -100,7 +100,7 @@ Shapes shapes(const msd_model* m, int M) {
 
 struct Layout {
   size_t x, stats, q, img_x, img_h, img_f, img_attn, img_act, partial, counters, part_o, part_ml,
-      tile_ms, tile_top, total;
+      tile_ms, tile_top, head_ms, head_top, total;
   int64_t n_counters;
   int32_t MT, max_chunks;
 };
@@ -149,6 +149,9 @@ Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacit
   L.part_ml = take(nparts * sizeof(float2));
   L.tile_ms = take((size_t)s.head.n_tiles * M * sizeof(float2));
   L.tile_top = take((size_t)s.head.n_tiles * M * kmax * sizeof(uint64_t));
+  const int parts = head_parts(s.head.n_tiles);
+  L.head_ms = take((size_t)parts * M * sizeof(float2));
+  L.head_top = take((size_t)parts * M * kmax * sizeof(uint64_t));
   L.total = off;
   return L;
 }
@@ -229,7 +232,17 @@ msd_status run_head(const msd_model* m, const Shapes& s, const Layout& L, char* 
   g.tile_top = reinterpret_cast<uint64_t*>(ws + L.tile_top);
   g.kappa = kappa;
   MSD_HIP(launch_gemm(EPI_HEAD, g, stream));
-  HeadMergeArgs hm{g.tile_ms, g.tile_top, s.head.n_tiles, M, kappa, ids, logp, argmax, lse};
+  HeadMergeArgs hm{g.tile_ms,
+                   g.tile_top,
+                   s.head.n_tiles,
+                   M,
+                   kappa,
+                   reinterpret_cast<float2*>(ws + L.head_ms),
+                   reinterpret_cast<uint64_t*>(ws + L.head_top),
+                   ids,
+                   logp,
+                   argmax,
+                   lse};
   MSD_HIP(launch_head_merge(hm, stream));
   return MSD_OK;
 }
@@ -259,6 +272,7 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
   if (c.n_heads % c.n_kv_heads) return fail(MSD_ERR_SHAPE, "n_heads must be a multiple of n_kv_heads");
   if (c.d_model % 64 || c.d_ffn % 64) return fail(MSD_ERR_SHAPE, "d_model and d_ffn must be multiples of 64");
   if (c.vocab % 16) return fail(MSD_ERR_SHAPE, "vocab must be a multiple of 16");
+  if (head_parts((c.vocab + kTileN - 1) / kTileN) > 64) return fail(MSD_ERR_SHAPE, "vocab must be <= 1048576");
   if (c.norm != MSD_NORM_RMS && c.norm != MSD_NORM_LAYER) return fail(MSD_ERR_INVALID_ARG, "norm kind");
   if (c.act != MSD_ACT_SWIGLU && c.act != MSD_ACT_RELU) return fail(MSD_ERR_INVALID_ARG, "act kind");
   if (c.pos != MSD_POS_ROPE && c.pos != MSD_POS_LEARNED) return fail(MSD_ERR_INVALID_ARG, "pos kind");

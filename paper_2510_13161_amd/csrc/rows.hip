@@ -132,51 +132,27 @@ __device__ __forceinline__ float2 ms_merge(float2 a, float2 b) {
   return make_float2(b.x, b.y + a.y * expf(a.x - b.x));
 }
 
-// One workgroup per row: merge the per-tile (max, sum exp) pairs and top-kappa
-// lists produced by the LM-head GEMM epilogue. KB bounds kappa at compile
-// time so a tile's keys load together; tiles go four at a time.
+// kappa best keys of a wave: every lane holds a descending list v[0..KB);
+// kappa rounds of shuffle argmax over the list heads (keys are unique). The
+// result is the same in every lane.
 template <int KB>
-__global__ __launch_bounds__(256) void head_merge_kernel(HeadMergeArgs a) {
-  extern __shared__ uint64_t lists[];  // [256][kappa]
-  __shared__ float2 sh_ms[4];
-  __shared__ uint64_t sh_key[4];
-  const int m = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int K = a.kappa;
-  uint64_t* mine = lists + (size_t)tid * K;
-  for (int r = 0; r < K; ++r) mine[r] = 0ull;
-
-  float2 acc = make_float2(-INFINITY, 0.0f);
-  for (int t0 = tid; t0 < a.n_tiles; t0 += 4 * blockDim.x) {
-    float2 ms[4];
-    uint64_t keys[4][KB];
+__device__ __forceinline__ void wave_topk(uint64_t (&v)[KB], int K, uint64_t (&out)[KB]) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int t = t0 + u * blockDim.x;
-      const int tc = t < a.n_tiles ? t : 0;
-      ms[u] = a.tile_ms[(size_t)tc * a.M + m];
-      const uint64_t* top = a.tile_top + ((size_t)tc * a.M + m) * K;
+  for (int r = 0; r < KB; ++r) {
+    out[r] = 0ull;
+    if (r >= K) continue;
+    const uint64_t best = wave_max_u64(v[0]);
+    const bool pop = v[0] == best && best != 0ull;
 #pragma unroll
-      for (int r = 0; r < KB; ++r) keys[u][r] = top[r < K ? r : 0];
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (t0 + u * blockDim.x >= a.n_tiles) break;
-      acc = ms_merge(acc, ms[u]);
-#pragma unroll
-      for (int r = 0; r < KB; ++r) {
-        if (r >= K) break;
-        const uint64_t key = keys[u][r];
-        if (key <= mine[K - 1]) break;  // tile lists are sorted, descending
-        int j = K - 1;
-        while (j > 0 && mine[j - 1] < key) {
-          mine[j] = mine[j - 1];
-          --j;
-        }
-        mine[j] = key;
-      }
-    }
+    for (int x = 0; x < KB - 1; ++x) v[x] = pop ? v[x + 1] : v[x];
+    if (pop) v[KB - 1] = 0ull;
+    out[r] = best;
   }
-  // fixed-order reduction of the (max, sum) pairs
+}
+
+// (max, sum) pairs of a wave, combined in a fixed butterfly order.
+__device__ __forceinline__ float2 wave_ms(float2 acc) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     float2 other;
@@ -184,32 +160,83 @@ __global__ __launch_bounds__(256) void head_merge_kernel(HeadMergeArgs a) {
     other.y = __shfl_xor(acc.y, o);
     acc = (lane & o) ? ms_merge(other, acc) : ms_merge(acc, other);
   }
-  if (lane == 0) sh_ms[wave] = acc;
-  __syncthreads();
-  float2 tot = sh_ms[0];
-  for (int w = 1; w < 4; ++w) tot = ms_merge(tot, sh_ms[w]);
-  const float lse = tot.x + logf(tot.y);
+  return acc;
+}
 
-  // kappa rounds of block-wide argmax over the heads of the per-thread lists
-  int head = 0;
-  for (int r = 0; r < K; ++r) {
-    const uint64_t cand = head < K ? mine[head] : 0ull;
-    const uint64_t wbest = wave_max_u64(cand);
-    if (lane == 0) sh_key[wave] = wbest;
-    __syncthreads();
-    uint64_t best = sh_key[0];
-    for (int w = 1; w < 4; ++w) best = sh_key[w] > best ? sh_key[w] : best;
-    __syncthreads();
-    if (cand == best && best != 0ull) ++head;
-    if (tid == 0) {
-      const int id = best ? key_id(best) : -1;
-      const float v = best ? key_val(best) : -INFINITY;
-      if (a.ids) a.ids[(size_t)m * K + r] = id;
-      if (a.logp) a.logp[(size_t)m * K + r] = v - lse;
-      if (r == 0 && a.argmax) a.argmax[m] = id;
-    }
+// Stage 1 of the per-row merge of the LM-head tiles: workgroup (row m,
+// part p) takes 256 consecutive tiles, one per thread; each wave extracts
+// its kappa best, wave 0 merges the 4 wave lists the same way and writes the
+// part's (max, sum exp) and kappa best keys.
+template <int KB>
+__global__ __launch_bounds__(256) void head_part_kernel(HeadMergeArgs a) {
+  __shared__ float2 sh_ms[4];
+  __shared__ uint64_t sh_top[4][KB];
+  const int m = blockIdx.x, p = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = a.kappa;
+  const int t = p * 256 + tid;
+  const bool live = t < a.n_tiles;
+  const int tc = live ? t : 0;
+  float2 acc = a.tile_ms[(size_t)tc * a.M + m];
+  uint64_t v[KB];
+  const uint64_t* top = a.tile_top + ((size_t)tc * a.M + m) * K;
+#pragma unroll
+  for (int r = 0; r < KB; ++r) v[r] = top[r < K ? r : 0];
+#pragma unroll
+  for (int r = 0; r < KB; ++r) v[r] = (live && r < K) ? v[r] : 0ull;
+  if (!live) acc = make_float2(-INFINITY, 0.0f);
+  acc = wave_ms(acc);
+  uint64_t w[KB];
+  wave_topk<KB>(v, K, w);
+  if (lane == 0) {
+    sh_ms[wave] = acc;
+#pragma unroll
+    for (int r = 0; r < KB; ++r) sh_top[wave][r] = w[r];
   }
-  if (tid == 0 && a.lse) a.lse[m] = lse;
+  __syncthreads();
+  if (wave != 0) return;
+  // lanes 0..3 hold the four wave lists
+#pragma unroll
+  for (int r = 0; r < KB; ++r) v[r] = lane < 4 ? sh_top[lane][r] : 0ull;
+  wave_topk<KB>(v, K, w);
+  if (lane == 0) {
+    float2 tot = sh_ms[0];
+    for (int x = 1; x < 4; ++x) tot = ms_merge(tot, sh_ms[x]);
+    const size_t q = (size_t)m * gridDim.y + p;
+    a.part_ms[q] = tot;
+#pragma unroll
+    for (int r = 0; r < KB; ++r)
+      if (r < K) a.part_top[q * K + r] = w[r];
+  }
+}
+
+// Stage 2: one wave per row merges the parts' lists (lane = part) and
+// (max, sum) pairs (in part order), and writes ids, log-probabilities,
+// argmax and logsumexp.
+template <int KB>
+__global__ __launch_bounds__(64) void head_final_kernel(HeadMergeArgs a, int parts) {
+  const int m = blockIdx.x, lane = threadIdx.x;
+  const int K = a.kappa;
+  const bool live = lane < parts;
+  const size_t q = (size_t)m * parts + (live ? lane : 0);
+  uint64_t v[KB];
+#pragma unroll
+  for (int r = 0; r < KB; ++r) v[r] = (live && r < K) ? a.part_top[q * K + (r < K ? r : 0)] : 0ull;
+  uint64_t w[KB];
+  wave_topk<KB>(v, K, w);
+  if (lane != 0) return;
+  float2 tot = a.part_ms[(size_t)m * parts];
+  for (int x = 1; x < parts; ++x) tot = ms_merge(tot, a.part_ms[(size_t)m * parts + x]);
+  const float lse = tot.x + logf(tot.y);
+#pragma unroll
+  for (int r = 0; r < KB; ++r) {
+    const uint64_t k = w[r];
+    const int id = k ? key_id(k) : -1;
+    const float val = k ? key_val(k) : -INFINITY;
+    if (r < K && a.ids) a.ids[(size_t)m * K + r] = id;
+    if (r < K && a.logp) a.logp[(size_t)m * K + r] = val - lse;
+    if (r == 0 && a.argmax) a.argmax[m] = id;
+  }
+  if (a.lse) a.lse[m] = lse;
 }
 
 __global__ void zero_kernel(int32_t* p, int64_t n) {
@@ -234,11 +261,23 @@ hipError_t launch_rows(const RowsArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+int head_parts(int n_tiles) { return (n_tiles + 255) / 256; }
+
 hipError_t launch_head_merge(const HeadMergeArgs& a, hipStream_t s) {
-  const size_t shmem = (size_t)256 * a.kappa * sizeof(uint64_t);
-  if (a.kappa <= 1) hipLaunchKernelGGL(head_merge_kernel<1>, dim3(a.M), dim3(256), shmem, s, a);
-  else if (a.kappa <= 8) hipLaunchKernelGGL(head_merge_kernel<8>, dim3(a.M), dim3(256), shmem, s, a);
-  else hipLaunchKernelGGL(head_merge_kernel<32>, dim3(a.M), dim3(256), shmem, s, a);
+  if (a.kappa < 1 || a.kappa > kMaxKappa) return hipErrorInvalidValue;
+  const int parts = head_parts(a.n_tiles);
+  if (parts > 64 || !a.part_ms || !a.part_top) return hipErrorInvalidValue;
+  const dim3 g1(a.M, parts);
+  if (a.kappa <= 1) {
+    hipLaunchKernelGGL(head_part_kernel<1>, g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(head_final_kernel<1>, dim3(a.M), dim3(64), 0, s, a, parts);
+  } else if (a.kappa <= 8) {
+    hipLaunchKernelGGL(head_part_kernel<8>, g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(head_final_kernel<8>, dim3(a.M), dim3(64), 0, s, a, parts);
+  } else {
+    hipLaunchKernelGGL(head_part_kernel<32>, g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(head_final_kernel<32>, dim3(a.M), dim3(64), 0, s, a, parts);
+  }
   return hipGetLastError();
 }
 

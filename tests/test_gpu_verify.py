@@ -136,6 +136,19 @@ def test_tiny_tree_rejection_and_match():
         _compare(case, gr, {0: o})
 
 
+@pytest.mark.parametrize("kappa", [16, 32])
+def test_tiny_wide_early_exit_message(kappa):
+    """The early-exit message at kappa above 8 (wider merge lists)."""
+    _torch()
+    w = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, ee_layer=1, kappa=kappa, seed=11)
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    _compare(case, gr, {0: o})
+    assert gr.ee_ids.shape[-1] == kappa
+
+
 def test_depth_reduced_14b_chain():
     """14B widths (d 5120, GQA 40/8, FFN 13824, vocab 152064) with 2 layers."""
     _torch()
