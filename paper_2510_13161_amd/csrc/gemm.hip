@@ -410,6 +410,20 @@ __device__ void epi_head(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4],
   }
 }
 
+template <int MT, int EPI>
+__device__ __forceinline__ void epilogue(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4], float* scr) {
+  if constexpr (EPI == EPI_RESID) {
+    epi_resid<MT>(a, t, acc, scr);
+  } else {
+    float mu[MT], rs[MT];
+    row_norm<MT>(a, mu, rs);
+    if constexpr (EPI == EPI_QKV) epi_qkv<MT>(a, t, acc, mu, rs);
+    else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<MT>(a, t, acc, scr, mu, rs);
+    else if constexpr (EPI == EPI_RELU) epi_relu<MT>(a, t, acc, scr, mu, rs);
+    else epi_head<MT>(a, t, acc, mu, rs);
+  }
+}
+
 template <int MT>
 struct KStep {
   bf16x8 w[4];
@@ -423,7 +437,9 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   __shared__ floatx4 red[NW][RCH * 4][kWave];
   __shared__ __attribute__((aligned(16))) float scr[16 * kScr];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  // wave-uniform (scalar) so that the k-loop branches and waits are scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int t = blockIdx.x / a.splits, s = blockIdx.x - t * a.splits;
   const int KS = a.K >> 5;
   const int kb0 = (int)((int64_t)KS * s / a.splits), ke0 = (int)((int64_t)KS * (s + 1) / a.splits);
@@ -453,24 +469,46 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
       x.al[mt] = load16(p + 512);
     }
   };
+  auto compute = [&](const KStep<MT>& x) {
 #pragma unroll
-  for (int d = 0; d < D; ++d)
-    if (d < n) issue(st[d], kb + d);
-  for (int i0 = 0; i0 < n; i0 += D) {
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int i = i0 + d;
-      if (i < n) {
+      for (int j = 0; j < 4; ++j) {
+        acc[mt][j] = mfma16x16x32(x.w[j], x.ah[mt], acc[mt][j]);
+        acc[mt][j] = mfma16x16x32(x.w[j], x.al[mt], acc[mt][j]);
+      }
+  };
+  // D k-steps in flight per wave (n is wave-uniform). The steady-state loop
+  // runs only over batches whose D refills are all real, so its body has no
+  // branch and each wait leaves the D-1 younger k-steps in flight; the last
+  // batch and a short run (n < D: every load issued up front) come after.
+  if (n >= D) {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+    for (int d = 0; d < D; ++d) issue(st[d], kb + d);
+    const int nfull = (n - D) / D;
+    for (int b = 0; b < nfull; ++b) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            acc[mt][j] = mfma16x16x32(st[d].w[j], st[d].ah[mt], acc[mt][j]);
-            acc[mt][j] = mfma16x16x32(st[d].w[j], st[d].al[mt], acc[mt][j]);
-          }
-        if (i + D < n) issue(st[d], kb + i + D);
+      for (int d = 0; d < D; ++d) {
+        compute(st[d]);
+        issue(st[d], kb + (b + 1) * D + d);
       }
     }
+    const int done = (nfull + 1) * D, r = n - done;  // 0 <= r < D steps left after this batch
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      compute(st[d]);
+      if (d < r) issue(st[d], kb + done + d);
+    }
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+      if (d < r) compute(st[d]);
+  } else {
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+      if (d < n) issue(st[d], kb + d);
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+      if (d < n) compute(st[d]);
   }
 
   // fixed-order sum of the waves' tiles
@@ -499,6 +537,16 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
     if (wave != 0) return;
   }
 
+  if (a.decoupled) {
+    // publish this split's tile for the separate epilogue kernel (plain
+    // stores; the kernel boundary orders them)
+    float* slot = a.partial + ((size_t)t * a.splits + s) * (MT * 1024) + lane * 4;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) *reinterpret_cast<floatx4*>(slot + (mt * 4 + j) * 256) = acc[mt][j];
+    return;
+  }
   if (a.splits > 1) {
     // publish this split's tile; the last split to arrive sums all of them
     float* slot = a.partial + ((size_t)t * a.splits + s) * (MT * 1024) + lane * 4;
@@ -547,21 +595,47 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
     if (lane == 0) counter_reset(&a.counters[t]);
   }
 
-  if constexpr (EPI == EPI_RESID) {
-    epi_resid<MT>(a, t, acc, scr);
-  } else {
-    float mu[MT], rs[MT];
-    row_norm<MT>(a, mu, rs);
-    if constexpr (EPI == EPI_QKV) epi_qkv<MT>(a, t, acc, mu, rs);
-    else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<MT>(a, t, acc, scr, mu, rs);
-    else if constexpr (EPI == EPI_RELU) epi_relu<MT>(a, t, acc, scr, mu, rs);
-    else epi_head<MT>(a, t, acc, mu, rs);
+  epilogue<MT, EPI>(a, t, acc, scr);
+}
+
+// Epilogue of a decoupled split-K GEMM: one wave per output tile sums the
+// tile's split partials in split order and runs the epilogue.
+template <int MT, int EPI>
+__global__ __launch_bounds__(64) void gemm_epi_kernel(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) float scr[16 * kScr];
+  const int lane = threadIdx.x, t = blockIdx.x;
+  floatx4 acc[MT][4];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const float* base = a.partial + (size_t)t * a.splits * (MT * 1024) + lane * 4;
+  for (int sp0 = 0; sp0 < a.splits; sp0 += 4) {
+    floatx4 part[4][MT][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int sp = sp0 + u < a.splits ? sp0 + u : sp0;
+      const float* src = base + (size_t)sp * (MT * 1024);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) part[u][mt][j] = *reinterpret_cast<const floatx4*>(src + (mt * 4 + j) * 256);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (sp0 + u < a.splits)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[mt][j] += part[u][mt][j];
   }
+  epilogue<MT, EPI>(a, t, acc, scr);
 }
 
 template <int MT, int NW, int EPI>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((gemm_kernel<MT, NW, EPI>), dim3(a.n_tiles * a.splits), dim3(64 * NW), 0, s, a);
+  if (a.decoupled) hipLaunchKernelGGL((gemm_epi_kernel<MT, EPI>), dim3(a.n_tiles), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -623,6 +697,7 @@ __global__ __launch_bounds__(256) void colsum_kernel(const uint16_t* w, int64_t 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
   if (a.n_tiles < 1 || a.splits < 1 || a.K % 32 || a.M < 1 || a.M > 16 * a.MT) return hipErrorInvalidValue;
   if (a.splits > 1 && (!a.partial || !a.counters)) return hipErrorInvalidValue;
+  if (a.decoupled && !a.partial) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_QKV: return launch_epi<EPI_QKV>(a, s);
     case EPI_RESID: return launch_epi<EPI_RESID>(a, s);
