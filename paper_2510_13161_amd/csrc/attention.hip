@@ -4,13 +4,15 @@
 // registers). GQA: query head h reads kv head h / (H / H_kv).
 //
 // Flash-decoding over 256-key chunks: a workgroup owns one (sequence, kv
-// head, chunk) and each of its 4 waves one 64-key block. A wave loads its
-// block's K as MFMA operands and V rows into its own LDS (16-byte writes, read
-// back transposed two bytes at a time with conflict-free strides) once, then
-// serves the kv head's GQA query tiles, up to three per pass:
+// head, 16-query tile of the head's GQA group, chunk) and each of its 4 waves
+// one 64-key block. A wave loads its block's K as MFMA operands and V rows
+// into its own LDS (16-byte writes, read back transposed two bytes at a time
+// with conflict-free strides), then
 //   S^T[key][query] = K Q^T        MFMA 16x16x32; Q (fp32) as bf16 hi + lo;
 //   block softmax statistics       one query per lane column: 2 shuffles;
 //   O[query][d] += P V             P stays in registers as the MFMA operand.
+// Scores are kept in base-2 units (the 1/sqrt(hd) scale times log2 e), so
+// every exponential is one hardware exp2.
 // The 4 waves' (max, sum, output) are merged in LDS in wave order. A chunk
 // that covers the whole sequence writes the normalised output straight into
 // the output-projection's activation image; otherwise chunks publish their
@@ -21,7 +23,9 @@
 namespace msd {
 namespace {
 
-constexpr int kQG = 3;  // query tiles per pass (one pass for G * n_slots <= 48)
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // image write of 8 consecutive output dims [8 c8, 8 c8 + 8) of query qg
 template <int HD>
@@ -44,7 +48,7 @@ struct AttnLds {
   static constexpr int kVS = HD + 4;  // bf16 per LDS row of V (one key), conflict-free strides
   static constexpr int kOS = HD + 4;  // floats per LDS row of a wave's output
   static constexpr int kVBytes = 64 * kVS * 2;
-  static constexpr int kOBytes = kQG * 16 * kOS * 4;
+  static constexpr int kOBytes = 16 * kOS * 4;
   static constexpr int kRegion = kVBytes > kOBytes ? kVBytes : kOBytes;
 };
 
@@ -57,26 +61,26 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   constexpr int VIT = HD / 8;    // 16-byte V chunks per lane per 64-key block
   constexpr int KPI = 512 / HD;  // keys per V chunk iteration
   __shared__ __attribute__((aligned(16))) unsigned char region_all[4][Lds::kRegion];
-  __shared__ float ml_sh[4][kQG * 16][2];
-  __shared__ __attribute__((aligned(16))) uint16_t qs[kQG * KSTEPS * 2 * 512];
+  __shared__ float ml_sh[4][16][2];
+  __shared__ __attribute__((aligned(16))) uint16_t qs[KSTEPS * 2 * 512];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int b = blockIdx.z, kvh = blockIdx.y, c = blockIdx.x;
-  const int L = a.len[b];
+  const int G = a.n_heads / a.n_kv_heads;
   const int ns = a.n_slots;
+  const int Qn = G * ns;
+  const int QT = (Qn + 15) >> 4;
+  const int b = blockIdx.z, kvh = blockIdx.y / QT, qt = blockIdx.y - kvh * QT, c = blockIdx.x;
+  const int L = a.len[b];
   const int T = L + ns;
   if (T > a.capacity) {
-    if (c == 0 && kvh == 0 && tid == 0) atomicOr(a.status, 1u);
+    if (c == 0 && blockIdx.y == 0 && tid == 0) atomicOr(a.status, 1u);
     return;
   }
   const int nch = (T + kAttnChunk - 1) / kAttnChunk;
   if (c >= nch) return;
   uint16_t* vs = reinterpret_cast<uint16_t*>(region_all[wave]);  // [64 keys][kVS]
-  float* os = reinterpret_cast<float*>(region_all[wave]);        // [48 queries][kOS]
-  const int G = a.n_heads / a.n_kv_heads;
-  const int Qn = G * ns;
-  const int QT = (Qn + 15) >> 4;
+  float* os = reinterpret_cast<float*>(region_all[wave]);        // [16 queries][kOS]
   const size_t row0 = ((size_t)b * a.n_kv_heads + kvh) * a.capacity;
   const uint16_t* kbase = a.k_cache + row0 * HD;
   const uint16_t* vbase = a.v_cache + row0 * HD;
@@ -100,195 +104,175 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk) kf[j][kk] = load16(kbase + (size_t)pos * HD + kk * 32 + g * 8);
   }
+
+  // the query tile as split-bf16 MFMA operands, shared by the 4 waves
+  // through LDS: qs[k-step][hi / lo][lane][8]
+  for (int x = tid; x < KSTEPS * 64; x += blockDim.x) {
+    const int kk = x >> 6, l = x & 63;
+    const int qv = qt * 16 + (l & 15);
+    const bool qok = qv < Qn;
+    const int gq = qok ? qv / ns : 0;
+    const int slot = qok ? qv - gq * ns : 0;
+    const float* qp = a.q + ((size_t)(b * ns + slot) * a.n_heads + kvh * G + gq) * HD + kk * 32 + (l >> 4) * 8;
+    const u32x4 r0 = *reinterpret_cast<const u32x4*>(qp);
+    const u32x4 r1 = *reinterpret_cast<const u32x4*>(qp + 4);
+    const float qm = qok ? 1.0f : 0.0f;
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[i] = __uint_as_float(r0[i]) * qm;
+      v[4 + i] = __uint_as_float(r1[i]) * qm;
+    }
+    u32x4 hw, lw;
+    split8_words(v, hw, lw);
+    uint16_t* dst = qs + (size_t)(kk * 2) * 512 + l * 8;
+    *reinterpret_cast<u32x4*>(dst) = hw;
+    *reinterpret_cast<u32x4*>(dst + 512) = lw;
+  }
+  // V rows into the wave's LDS as they are (16-byte writes), read back as
+  // P V operands: lane l takes dim 16 ds + l%16 of keys 32 kb + 4 g + e and
+  // 32 kb + 16 + 4 g + e (e < 4), the k order of P below
+#pragma unroll
+  for (int it = 0; it < VIT; ++it) {
+    const int key = it * KPI + lane / (HD / 8);
+    *reinterpret_cast<u32x4*>(vs + key * Lds::kVS + (lane % (HD / 8)) * 8) = vraw[it];
+  }
+  __syncthreads();
   bf16x8 vb[2][DSUB];
-
-  for (int qt0 = 0; qt0 < QT; qt0 += kQG) {
-    // the pass's query tiles as split-bf16 MFMA operands, shared by the
-    // 4 waves through LDS: qs[tile][k-step][hi / lo][lane][8]
-    for (int x = tid; x < kQG * KSTEPS * 64; x += blockDim.x) {
-      const int q = x / (KSTEPS * 64), kk = (x / 64) % KSTEPS, l = x & 63;
-      const int qv = (qt0 + q) * 16 + (l & 15);
-      const bool qok = qv < Qn;
-      const int gq = qok ? qv / ns : 0;
-      const int slot = qok ? qv - gq * ns : 0;
-      const float* qp = a.q + ((size_t)(b * ns + slot) * a.n_heads + kvh * G + gq) * HD + kk * 32 + (l >> 4) * 8;
-      const u32x4 r0 = *reinterpret_cast<const u32x4*>(qp);
-      const u32x4 r1 = *reinterpret_cast<const u32x4*>(qp + 4);
-      const float qm = qok ? 1.0f : 0.0f;
-      float v[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        v[i] = __uint_as_float(r0[i]) * qm;
-        v[4 + i] = __uint_as_float(r1[i]) * qm;
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int ds = 0; ds < DSUB; ++ds) {
+      const uint16_t* col = vs + 16 * ds + r16;
+      uint16_t e8[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        e8[e] = col[(32 * kb + 4 * g + e) * Lds::kVS];
+        e8[4 + e] = col[(32 * kb + 16 + 4 * g + e) * Lds::kVS];
       }
-      u32x4 hw, lw;
-      split8_words(v, hw, lw);
-      uint16_t* dst = qs + (size_t)((q * KSTEPS + kk) * 2) * 512 + l * 8;
-      *reinterpret_cast<u32x4*>(dst) = hw;
-      *reinterpret_cast<u32x4*>(dst + 512) = lw;
-    }
-    if (qt0 == 0) {
-      // V rows into the wave's LDS as they are (16-byte writes), read back as
-      // P V operands: lane l takes dim 16 ds + l%16 of keys 32 kb + 4 g + e
-      // and 32 kb + 16 + 4 g + e (e < 4), the k order of P below
+      u32x4 w;
 #pragma unroll
-      for (int it = 0; it < VIT; ++it) {
-        const int key = it * KPI + lane / (HD / 8);
-        *reinterpret_cast<u32x4*>(vs + key * Lds::kVS + (lane % (HD / 8)) * 8) = vraw[it];
-      }
-    }
-    __syncthreads();
-    if (qt0 == 0) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int ds = 0; ds < DSUB; ++ds) {
-          const uint16_t* col = vs + 16 * ds + r16;
-          uint16_t e8[8];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            e8[e] = col[(32 * kb + 4 * g + e) * Lds::kVS];
-            e8[4 + e] = col[(32 * kb + 16 + 4 * g + e) * Lds::kVS];
-          }
-          u32x4 w;
-#pragma unroll
-          for (int x = 0; x < 4; ++x) w[x] = (uint32_t)e8[2 * x] | ((uint32_t)e8[2 * x + 1] << 16);
-          vb[kb][ds] = __builtin_bit_cast(bf16x8, w);
-        }
+      for (int x = 0; x < 4; ++x) w[x] = (uint32_t)e8[2 * x] | ((uint32_t)e8[2 * x + 1] << 16);
+      vb[kb][ds] = __builtin_bit_cast(bf16x8, w);
     }
 
-    float run_m[kQG], run_l[kQG];
-    floatx4 o[kQG][DSUB];
+  const int qv = qt * 16 + r16;
+  const uint64_t anc = qv < Qn ? a.topo.anc[qv % ns] : 0ull;
+  floatx4 sc[4];
 #pragma unroll
-    for (int q = 0; q < kQG; ++q) {
-      run_m[q] = -INFINITY;
-      run_l[q] = 0.0f;
+  for (int j = 0; j < 4; ++j) {
+    sc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ds = 0; ds < DSUB; ++ds) o[q][ds] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < KSTEPS; ++kk) {
+      const uint16_t* qf = qs + (size_t)(kk * 2) * 512 + lane * 8;
+      sc[j] = mfma16x16x32(kf[j][kk], load16(qf), sc[j]);
+      sc[j] = mfma16x16x32(kf[j][kk], load16(qf + 512), sc[j]);
     }
+  }
+  // lane holds S^T[key 16j + 4g + r][query r16]: scale (base 2), mask, softmax
+  const float scale2 = a.scale * kLog2e;
+  float mx = -INFINITY;
 #pragma unroll
-    for (int q = 0; q < kQG; ++q) {
-      const int qv = (qt0 + q) * 16 + r16;
-      if ((qt0 + q) * 16 >= Qn) break;
-      const uint64_t anc = qv < Qn ? a.topo.anc[qv % ns] : 0ull;
-      floatx4 sc[4];
+  for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        sc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < KSTEPS; ++kk) {
-          const uint16_t* qf = qs + (size_t)((q * KSTEPS + kk) * 2) * 512 + lane * 8;
-          sc[j] = mfma16x16x32(kf[j][kk], load16(qf), sc[j]);
-          sc[j] = mfma16x16x32(kf[j][kk], load16(qf + 512), sc[j]);
-        }
-      }
-      // lane holds S^T[key 16j + 4g + r][query r16]: scale, mask, softmax
-      float mx = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int pos = k0 + 16 * j + 4 * g + r;
-          const bool vis = pos < key_hi && (pos < L || ((anc >> (pos - L)) & 1ull));
-          sc[j][r] = vis ? sc[j][r] * a.scale : -INFINITY;
-          mx = fmaxf(mx, sc[j][r]);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mref = mx == -INFINITY ? 0.0f : mx;
-      float ls = 0.0f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          sc[j][r] = expf(sc[j][r] - mref);
-          ls += sc[j][r];
-        }
-      ls += __shfl_xor(ls, 16);
-      ls += __shfl_xor(ls, 32);
-      run_l[q] = ls;
-      run_m[q] = mx;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        // P as bf16 hi + lo (k order: keys 4g+r of the two 16-key tiles)
-        u32x4 ph, pl;
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          const float p0 = sc[2 * kb + (x >> 1)][2 * (x & 1)];
-          const float p1 = sc[2 * kb + (x >> 1)][2 * (x & 1) + 1];
-          ph[x] = pack_bf16x2(p0, p1);
-          pl[x] = pack_bf16x2(p0 - bf_lo(ph[x]), p1 - bf_hi(ph[x]));
-        }
-        const bf16x8 pah = __builtin_bit_cast(bf16x8, ph);
-        const bf16x8 pal = __builtin_bit_cast(bf16x8, pl);
-#pragma unroll
-        for (int ds = 0; ds < DSUB; ++ds) {
-          o[q][ds] = mfma16x16x32(pah, vb[kb][ds], o[q][ds]);
-          o[q][ds] = mfma16x16x32(pal, vb[kb][ds], o[q][ds]);
-        }
-      }
+    for (int r = 0; r < 4; ++r) {
+      const int pos = k0 + 16 * j + 4 * g + r;
+      const bool vis = pos < key_hi && (pos < L || ((anc >> (pos - L)) & 1ull));
+      sc[j][r] = vis ? sc[j][r] * scale2 : -INFINITY;
+      mx = fmaxf(mx, sc[j][r]);
     }
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float mref = mx == -INFINITY ? 0.0f : mx;
+  float ls = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      sc[j][r] = exp2_hw(sc[j][r] - mref);
+      ls += sc[j][r];
+    }
+  ls += __shfl_xor(ls, 16);
+  ls += __shfl_xor(ls, 32);
+  floatx4 o[DSUB];
+#pragma unroll
+  for (int ds = 0; ds < DSUB; ++ds) o[ds] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    // P as bf16 hi + lo (k order: keys 4g+r of the two 16-key tiles)
+    u32x4 ph, pl;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const float p0 = sc[2 * kb + (x >> 1)][2 * (x & 1)];
+      const float p1 = sc[2 * kb + (x >> 1)][2 * (x & 1) + 1];
+      ph[x] = pack_bf16x2(p0, p1);
+      pl[x] = pack_bf16x2(p0 - bf_lo(ph[x]), p1 - bf_hi(ph[x]));
+    }
+    const bf16x8 pah = __builtin_bit_cast(bf16x8, ph);
+    const bf16x8 pal = __builtin_bit_cast(bf16x8, pl);
+#pragma unroll
+    for (int ds = 0; ds < DSUB; ++ds) {
+      o[ds] = mfma16x16x32(pah, vb[kb][ds], o[ds]);
+      o[ds] = mfma16x16x32(pal, vb[kb][ds], o[ds]);
+    }
+  }
 
-    // publish the wave's (max, sum, output) to its LDS region: every wave's
-    // V reads are done once all have passed this barrier
-    __syncthreads();
+  // publish the wave's (max, sum, output) to its LDS region: every wave's
+  // V reads are done once all have passed this barrier
+  __syncthreads();
 #pragma unroll
-    for (int q = 0; q < kQG; ++q) {
+  for (int ds = 0; ds < DSUB; ++ds)
 #pragma unroll
-      for (int ds = 0; ds < DSUB; ++ds)
+    for (int r = 0; r < 4; ++r) os[(4 * g + r) * Lds::kOS + ds * 16 + r16] = o[ds][r];
+  if (g == 0) {
+    ml_sh[wave][r16][0] = mx;
+    ml_sh[wave][r16][1] = ls;
+  }
+  __syncthreads();
+  // merge the 4 waves (wave order), then output or publish the chunk
+  for (int x = tid; x < 16 * C8; x += blockDim.x) {
+    const int qloc = x / C8, c8 = x - qloc * C8;
+    const int qg = qt * 16 + qloc;
+    if (qg >= Qn) continue;
+    float M = -INFINITY;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) os[(q * 16 + 4 * g + r) * Lds::kOS + ds * 16 + r16] = o[q][ds][r];
-      if (g == 0) {
-        ml_sh[wave][q * 16 + r16][0] = run_m[q];
-        ml_sh[wave][q * 16 + r16][1] = run_l[q];
-      }
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
+    float S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float mw = ml_sh[w][qloc][0];
+      const float f = mw == -INFINITY ? 0.0f : exp2_hw(mw - M);
+      S += ml_sh[w][qloc][1] * f;
+      const float* src = reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 8 * c8;
+      const float4 v0 = *reinterpret_cast<const float4*>(src);
+      const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
+      o8[0] += f * v0.x;
+      o8[1] += f * v0.y;
+      o8[2] += f * v0.z;
+      o8[3] += f * v0.w;
+      o8[4] += f * v1.x;
+      o8[5] += f * v1.y;
+      o8[6] += f * v1.z;
+      o8[7] += f * v1.w;
     }
-    __syncthreads();
-    // merge the 4 waves (wave order), then output or publish the chunk
-    for (int x = tid; x < kQG * 16 * C8; x += blockDim.x) {
-      const int qloc = x / C8, c8 = x - qloc * C8;
-      const int qg = qt0 * 16 + qloc;
-      if (qg >= Qn) continue;
-      float M = -INFINITY;
+    if (nch == 1) {
+      const float inv = S > 0.0f ? 1.0f / S : 0.0f;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
-      float S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float mw = ml_sh[w][qloc][0];
-        const float f = mw == -INFINITY ? 0.0f : expf(mw - M);
-        S += ml_sh[w][qloc][1] * f;
-        const float* src = reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 8 * c8;
-        const float4 v0 = *reinterpret_cast<const float4*>(src);
-        const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
-        o8[0] += f * v0.x;
-        o8[1] += f * v0.y;
-        o8[2] += f * v0.z;
-        o8[3] += f * v0.w;
-        o8[4] += f * v1.x;
-        o8[5] += f * v1.y;
-        o8[6] += f * v1.z;
-        o8[7] += f * v1.w;
-      }
-      if (nch == 1) {
-        const float inv = S > 0.0f ? 1.0f / S : 0.0f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o8[e] *= inv;
-        write_out<HD>(a, b, kvh, qg, c8, o8);
-      } else {
-        const size_t pidx = (((size_t)b * a.n_kv_heads + kvh) * a.max_chunks + c) * Qn + qg;
-        float* po = a.part_o + pidx * HD + 8 * c8;
-        *reinterpret_cast<float4*>(po) = make_float4(o8[0], o8[1], o8[2], o8[3]);
-        *reinterpret_cast<float4*>(po + 4) = make_float4(o8[4], o8[5], o8[6], o8[7]);
-        if (c8 == 0) reinterpret_cast<float2*>(a.part_ml)[pidx] = make_float2(M, S);
-      }
+      for (int e = 0; e < 8; ++e) o8[e] *= inv;
+      write_out<HD>(a, b, kvh, qg, c8, o8);
+    } else {
+      const size_t pidx = (((size_t)b * a.n_kv_heads + kvh) * a.max_chunks + c) * Qn + qg;
+      float* po = a.part_o + pidx * HD + 8 * c8;
+      *reinterpret_cast<float4*>(po) = make_float4(o8[0], o8[1], o8[2], o8[3]);
+      *reinterpret_cast<float4*>(po + 4) = make_float4(o8[4], o8[5], o8[6], o8[7]);
+      if (c8 == 0) reinterpret_cast<float2*>(a.part_ml)[pidx] = make_float2(M, S);
     }
-    __syncthreads();
   }
 }
 
 // Merge of the chunk partials of sequences that span more than one chunk:
-// one thread per (sequence, kv head, query, 8 output dims), chunks in order.
+// one thread per (sequence, kv head, query, 8 output dims), chunks in order;
+// the partial maxima are in base-2 units like the scores they came from.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   constexpr int C8 = HD / 8;
@@ -323,8 +307,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     for (int u = 0; u < 4; ++u) {
       if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
       const float Mn = fmaxf(M, ml[u].x);
-      const float fa = M == -INFINITY ? 0.0f : expf(M - Mn);
-      const float fb = expf(ml[u].x - Mn);
+      const float fa = M == -INFINITY ? 0.0f : exp2_hw(M - Mn);
+      const float fb = exp2_hw(ml[u].x - Mn);
       S = S * fa + ml[u].y * fb;
       const float pv[8] = {v0[u].x, v0[u].y, v0[u].z, v0[u].w, v1[u].x, v1[u].y, v1[u].z, v1[u].w};
 #pragma unroll
@@ -342,7 +326,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s) {
   if (a.max_chunks > kMaxAttnChunks || a.max_chunks < 1) return hipErrorInvalidValue;
-  const dim3 grid(a.max_chunks, a.n_kv_heads, a.batch);
+  const int qt = (a.n_heads / a.n_kv_heads * a.n_slots + 15) / 16;
+  const dim3 grid(a.max_chunks, a.n_kv_heads * qt, a.batch);
   const int64_t items = (int64_t)a.batch * a.n_kv_heads * (a.n_heads / a.n_kv_heads) * a.n_slots *
                         (head_dim / 8);
   const dim3 mgrid((unsigned)((items + 255) / 256));

@@ -138,7 +138,7 @@ struct AttnArgs {
   uint16_t* out_img;        // image of the output (K = H * hd)
   int32_t MT;
   float* part_o;            // [batch][Hkv][chunks][Qn][hd]
-  float* part_ml;           // [batch][Hkv][chunks][Qn][2] (max, sum exp)
+  float* part_ml;           // [batch][Hkv][chunks][Qn][2] (max of score * log2 e, sum exp2)
   int32_t batch, n_heads, n_kv_heads, capacity, n_slots;
   int32_t max_chunks;       // 256-key chunks of the longest sequence
   float scale;
