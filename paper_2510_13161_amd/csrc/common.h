@@ -211,18 +211,6 @@ __device__ __forceinline__ float2 load_coherent2(const float* p) {
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
-// Pairwise combination of (count, mean, M2) summaries (Chan, Golub & LeVeque):
-// n = na + nb, d = mb - ma, mean = ma + d nb / n, M2 = M2a + M2b + d^2 na nb / n.
-__device__ __forceinline__ void chan_combine(float& n, float& mean, float& m2, float nb, float mb,
-                                             float m2b) {
-  const float nt = n + nb;
-  if (nt <= 0.0f) return;
-  const float d = mb - mean;
-  mean += d * (nb / nt);
-  m2 += m2b + d * d * (n * nb / nt);
-  n = nt;
-}
-
 // Activation image: the split-bf16 MFMA operand form of an activation matrix
 // [M][K] (M padded to 16 MT rows). Element order [K/32][MT][2][64][8]: k-step
 // ks, row tile mt, part (0 = hi, 1 = lo), lane l = row 16 mt + l%16 and

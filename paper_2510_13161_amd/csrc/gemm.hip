@@ -79,10 +79,13 @@ __device__ __forceinline__ int out_col(const GemmArgs& a, int t, int j, int q, i
   return kTileN * t + 16 * j + 4 * q + r;
 }
 
-// Per-row (mu, r) of the pre-norm, for the lane's row 16 mt + l%16: the four
-// lanes of a row each combine a quarter of the producer's 64-column
-// summaries (loads issued together), then the quarters are combined in lane
-// order so that all four lanes hold identical bits.
+// Per-row (mu, r) of the pre-norm, for the lane's row 16 mt + l%16, from the
+// producer's per-64-column (mean, M2) summaries. All summaries count 64
+// columns, so the row's mean is the mean of the summary means and
+//   M2 = sum_i M2_i + 64 sum_i (mean_i - mean)^2
+// (the exact merge of equal-count groups). The four lanes of a row each take
+// every fourth summary (loads issued together) and their partial sums are
+// combined by a butterfly, which gives all four lanes identical bits.
 template <int MT>
 __device__ void row_norm(const GemmArgs& a, float (&mu)[MT], float (&rs)[MT]) {
   constexpr int kMaxPer = 40;  // summaries per lane: K <= 40 * 4 * 64 = 10240
@@ -103,23 +106,22 @@ __device__ void row_norm(const GemmArgs& a, float (&mu)[MT], float (&rs)[MT]) {
       const int tt = q + 4 * i;
       st[i] = nm.stats[(size_t)(tt < nm.tiles ? tt : 0) * a.M + mm];
     }
-    float n = 0.0f, mean = 0.0f, m2 = 0.0f;
+    float sm = 0.0f;
 #pragma unroll
     for (int i = 0; i < kMaxPer; ++i)
-      if (q + 4 * i < nm.tiles) chan_combine(n, mean, m2, (float)kTileN, st[i].x, st[i].y);
+      if (q + 4 * i < nm.tiles) sm += st[i].x;
+    sm += __shfl_xor(sm, 16);
+    sm += __shfl_xor(sm, 32);
+    const float mean = sm / (float)nm.tiles;
+    float m2 = 0.0f;
 #pragma unroll
-    for (int o = 16; o <= 32; o <<= 1) {
-      const float n2 = __shfl_xor(n, o), mean2 = __shfl_xor(mean, o), m22 = __shfl_xor(m2, o);
-      if (lane & o) {  // combine as (lower lane, higher lane) in both lanes
-        float nn = n2, me = mean2, mm2 = m22;
-        chan_combine(nn, me, mm2, n, mean, m2);
-        n = nn;
-        mean = me;
-        m2 = mm2;
-      } else {
-        chan_combine(n, mean, m2, n2, mean2, m22);
+    for (int i = 0; i < kMaxPer; ++i)
+      if (q + 4 * i < nm.tiles) {
+        const float dv = st[i].x - mean;
+        m2 += st[i].y + (float)kTileN * dv * dv;
       }
-    }
+    m2 += __shfl_xor(m2, 16);
+    m2 += __shfl_xor(m2, 32);
     const float var = m2 / (float)a.K;
     if (nm.kind == 1) {
       rs[mt] = 1.0f / sqrtf(var + mean * mean + nm.eps);
