@@ -79,56 +79,125 @@ __device__ __forceinline__ int out_col(const GemmArgs& a, int t, int j, int q, i
   return kTileN * t + 16 * j + 4 * q + r;
 }
 
-// Per-row (mu, r) of the pre-norm, for the lane's row 16 mt + l%16, from the
-// producer's per-64-column (mean, M2) summaries. All summaries count 64
-// columns, so the row's mean is the mean of the summary means and
-//   M2 = sum_i M2_i + 64 sum_i (mean_i - mean)^2
-// (the exact merge of equal-count groups). The four lanes of a row each take
-// every fourth summary (loads issued together) and their partial sums are
-// combined by a butterfly, which gives all four lanes identical bits.
-template <int MT>
-__device__ void row_norm(const GemmArgs& a, float (&mu)[MT], float (&rs)[MT]) {
-  constexpr int kMaxPer = 40;  // summaries per lane: K <= 40 * 4 * 64 = 10240
+// ---------------------------------------------------------------------------
+// epilogue inputs that do not depend on the product
+// ---------------------------------------------------------------------------
+constexpr int kMaxPer = 40;  // pre-norm summaries per lane: K <= 40 * 4 * 64 = 10240
+constexpr u32x4 kUnitGain = {0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};  // bf16 1.0 pairs
+
+// Per lane (row 16 mt + l%16, lane group q = l/16) of one row tile. With one
+// row tile the finishing wave loads them right after its k-loop, so that
+// their round trip overlaps the wave reduction and the split-K hand-off;
+// with more row tiles each row tile loads its own inside the epilogue.
+struct EpiIn {
+  float2 st[kMaxPer];  // pre-norm: the row's 64-column (mean, M2) summaries q, q+4, ...
+  float4 x[4];         // EPI_RESID: residual x[m][64 t + 16 j + 4 q ..]
+  u32x2 bias[4];       // EPI_RESID: its bias (bf16 pairs)
+  u32x4 gain[2][2];    // EPI_RESID: gains of the two images, halves h = 0, 1
+  int L;               // EPI_QKV: committed length of the row's sequence
+  float2 cs[2][4];     // EPI_QKV: rotary (cos, sin) of the row's position
+  u32x2 qb[2][2];      // EPI_QKV: bias (bf16 pairs), [j][lo / hi half]
+};
+
+template <int EPI>
+__device__ __forceinline__ constexpr bool has_norm() {
+  return EPI != EPI_RESID;
+}
+
+// committed length of the sequence of row m (EPI_QKV)
+__device__ __forceinline__ int row_len(const GemmArgs& a, int m) {
+  return a.len[(m < a.M ? m : 0) / a.n_slots];
+}
+
+template <int EPI>
+__device__ __forceinline__ void epi_load(const GemmArgs& a, int t, int mt, EpiIn& in) {
   const int lane = threadIdx.x & 63, q = lane >> 4, r16 = lane & 15;
-  const RowNorm& nm = a.norm;
+  const int m = 16 * mt + r16;
+  const int mm = m < a.M ? m : 0;
+  if constexpr (has_norm<EPI>()) {
+    if (a.norm.kind != 0) {
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    mu[mt] = 0.0f;
-    rs[mt] = 1.0f;
-  }
-  if (nm.kind == 0) return;
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = 16 * mt + r16;
-    const int mm = m < a.M ? m : 0;
-    float2 st[kMaxPer];
-#pragma unroll
-    for (int i = 0; i < kMaxPer; ++i) {
-      const int tt = q + 4 * i;
-      st[i] = nm.stats[(size_t)(tt < nm.tiles ? tt : 0) * a.M + mm];
-    }
-    float sm = 0.0f;
-#pragma unroll
-    for (int i = 0; i < kMaxPer; ++i)
-      if (q + 4 * i < nm.tiles) sm += st[i].x;
-    sm += __shfl_xor(sm, 16);
-    sm += __shfl_xor(sm, 32);
-    const float mean = sm / (float)nm.tiles;
-    float m2 = 0.0f;
-#pragma unroll
-    for (int i = 0; i < kMaxPer; ++i)
-      if (q + 4 * i < nm.tiles) {
-        const float dv = st[i].x - mean;
-        m2 += st[i].y + (float)kTileN * dv * dv;
+      for (int i = 0; i < kMaxPer; ++i) {
+        const int tt = q + 4 * i;
+        in.st[i] = a.norm.stats[(size_t)(tt < a.norm.tiles ? tt : 0) * a.M + mm];
       }
-    m2 += __shfl_xor(m2, 16);
-    m2 += __shfl_xor(m2, 32);
-    const float var = m2 / (float)a.K;
-    if (nm.kind == 1) {
-      rs[mt] = 1.0f / sqrtf(var + mean * mean + nm.eps);
-    } else {
-      rs[mt] = 1.0f / sqrtf(var + nm.eps);
-      mu[mt] = mean;
     }
+  }
+  if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n0 = kTileN * t + 16 * j + 4 * q;
+      in.x[j] = *reinterpret_cast<const float4*>(a.x + (size_t)mm * a.N + n0);
+      in.bias[j] = a.b0 ? *reinterpret_cast<const u32x2*>(a.b0 + n0) : u32x2{0u, 0u};
+    }
+#pragma unroll
+    for (int o = 0; o < 2; ++o)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        in.gain[o][h] = a.img_out[o].img && a.img_out[o].gain
+                            ? *reinterpret_cast<const u32x4*>(a.img_out[o].gain + kTileN * t + 32 * h + 8 * q)
+                            : kUnitGain;
+  }
+  if constexpr (EPI == EPI_QKV) {
+    const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
+    const int H = a.n_heads, Hk = a.n_kv_heads;
+    const int hh = t / tph, gi = t - hh * tph;
+    const int which = hh < H ? 0 : (hh < H + Hk ? 1 : 2);
+    const int hloc = hh - (which == 0 ? 0 : (which == 1 ? H : H + Hk));
+    const uint16_t* bias = which == 0 ? a.b0 : (which == 1 ? a.b1 : a.b2);
+    const int slot = mm - (mm / a.n_slots) * a.n_slots;
+    int pos = in.L + a.depth[slot];
+    pos = pos < 0 ? 0 : (pos < a.rope_rows ? pos : a.rope_rows - 1);  // out-of-range rows are flagged, not used
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int dlo = gi * 32 + 16 * j + 4 * q, dhi = half + dlo;
+      if (which < 2 && a.rope) {
+        const float2* cs = a.rope + (size_t)pos * half + dlo;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) in.cs[j][r] = cs[r];
+      }
+      in.qb[j][0] = bias ? *reinterpret_cast<const u32x2*>(bias + hloc * hd + dlo) : u32x2{0u, 0u};
+      in.qb[j][1] = bias ? *reinterpret_cast<const u32x2*>(bias + hloc * hd + dhi) : u32x2{0u, 0u};
+    }
+  }
+}
+
+// Per-row (mu, r) of the pre-norm from the producer's per-64-column
+// (mean, M2) summaries. All summaries count 64 columns, so the row's mean is
+// the mean of the summary means and
+//   M2 = sum_i M2_i + 64 sum_i (mean_i - mean)^2
+// (the exact merge of equal-count groups). The four lanes of a row each hold
+// every fourth summary and their partial sums are combined by a butterfly,
+// which gives all four lanes identical bits.
+__device__ __forceinline__ void norm_finish(const GemmArgs& a, const EpiIn& in, float& mu,
+                                            float& rs) {
+  const int q = (threadIdx.x & 63) >> 4;
+  const RowNorm& nm = a.norm;
+  mu = 0.0f;
+  rs = 1.0f;
+  if (nm.kind == 0) return;
+  float sm = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i)
+    if (q + 4 * i < nm.tiles) sm += in.st[i].x;
+  sm += __shfl_xor(sm, 16);
+  sm += __shfl_xor(sm, 32);
+  const float mean = sm / (float)nm.tiles;
+  float m2 = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i)
+    if (q + 4 * i < nm.tiles) {
+      const float dv = in.st[i].x - mean;
+      m2 += in.st[i].y + (float)kTileN * dv * dv;
+    }
+  m2 += __shfl_xor(m2, 16);
+  m2 += __shfl_xor(m2, 32);
+  const float var = m2 / (float)a.K;
+  if (nm.kind == 1) {
+    rs = 1.0f / sqrtf(var + mean * mean + nm.eps);
+  } else {
+    rs = 1.0f / sqrtf(var + nm.eps);
+    mu = mean;
   }
 }
 
@@ -149,22 +218,19 @@ __device__ __forceinline__ void wave_lds_sync() {
 constexpr int kScr = kTileN + 4;  // scratch row stride (floats)
 
 // Image of 32 consecutive columns [c0, c0 + 32) of a 16-row tile held in
-// scratch[16][kScr], times an optional gain, written as image k-step ks.
-__device__ __forceinline__ void scratch_to_image(const float* scr, int c0, const uint16_t* gain,
-                                                 int gcol0, int M, int mt, int MT, int ks,
-                                                 uint16_t* img) {
+// scratch[16][kScr], times the lane's 8 gains (bf16 pairs), written as image
+// k-step ks.
+__device__ __forceinline__ void scratch_to_image(const float* scr, int c0, const u32x4& gw, int M,
+                                                 int mt, int MT, int ks, uint16_t* img) {
   const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
   const float* src = scr + r16 * kScr + c0 + 8 * q;
   const float4 v0 = *reinterpret_cast<const float4*>(src);
   const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
   float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-  if (gain) {
-    const u32x4 gw = *reinterpret_cast<const u32x4*>(gain + gcol0 + 8 * q);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[2 * i] *= bf_lo(gw[i]);
-      v[2 * i + 1] *= bf_hi(gw[i]);
-    }
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] *= bf_lo(gw[i]);
+    v[2 * i + 1] *= bf_hi(gw[i]);
   }
   const bool valid = 16 * mt + r16 < M;
 #pragma unroll
@@ -177,252 +243,234 @@ __device__ __forceinline__ void scratch_to_image(const float* scr, int c0, const
 }
 
 // ---------------------------------------------------------------------------
-// epilogues (wave 0 of the finishing workgroup; acc = the whole tile)
-// lane l, value [mt][j][r]: row 16 mt + l%16, column 64 t + 16 j + 4 (l/16) + r
+// epilogues (wave 0 of the finishing workgroup), one row tile mt at a time;
+// lane l, value [j][r]: row 16 mt + l%16, column 64 t + 16 j + 4 (l/16) + r
 // ---------------------------------------------------------------------------
-template <int MT>
-__device__ void epi_resid(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4], float* scr) {
+__device__ void epi_resid(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4], float* scr,
+                          const EpiIn& in) {
   const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = 16 * mt + r16;
-    const bool valid = m < a.M;
-    const int mm = valid ? m : 0;
-    float v[4][4];
-    float sum = 0.0f;
+  const int m = 16 * mt + r16;
+  const bool valid = m < a.M;
+  const int mm = valid ? m : 0;
+  float v[4][4];
+  float sum = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n0 = kTileN * t + 16 * j + 4 * q;
-      float4* xp = reinterpret_cast<float4*>(a.x + (size_t)mm * a.N + n0);
-      const float4 xv = *xp;
-      float bb[4] = {0.f, 0.f, 0.f, 0.f};
-      if (a.b0) {
-        const u32x2 bw = *reinterpret_cast<const u32x2*>(a.b0 + n0);
-        bb[0] = bf_lo(bw[0]);
-        bb[1] = bf_hi(bw[0]);
-        bb[2] = bf_lo(bw[1]);
-        bb[3] = bf_hi(bw[1]);
-      }
-      const float xs[4] = {xv.x, xv.y, xv.z, xv.w};
+  for (int j = 0; j < 4; ++j) {
+    const int n0 = kTileN * t + 16 * j + 4 * q;
+    const float bb[4] = {bf_lo(in.bias[j][0]), bf_hi(in.bias[j][0]), bf_lo(in.bias[j][1]),
+                         bf_hi(in.bias[j][1])};
+    const float xs[4] = {in.x[j].x, in.x[j].y, in.x[j].z, in.x[j].w};
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        v[j][r] = valid ? xs[r] + (acc[mt][j][r] + bb[r]) : 0.0f;
-        sum += v[j][r];
-      }
-      if (valid) *xp = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+    for (int r = 0; r < 4; ++r) {
+      v[j][r] = valid ? xs[r] + (acc[j][r] + bb[r]) : 0.0f;
+      sum += v[j][r];
     }
-    if (a.stats_out) {
-      sum += __shfl_xor(sum, 16);
-      sum += __shfl_xor(sum, 32);
-      const float mean = sum * (1.0f / kTileN);
-      float m2 = 0.0f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float dv = v[j][r] - mean;
-          m2 += dv * dv;
-        }
-      m2 += __shfl_xor(m2, 16);
-      m2 += __shfl_xor(m2, 32);
-      if (q == 0 && valid) a.stats_out[(size_t)t * a.M + m] = make_float2(mean, m2);
-    }
-    if (a.img_out[0].img || a.img_out[1].img) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        *reinterpret_cast<float4*>(scr + r16 * kScr + 16 * j + 4 * q) =
-            make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
-      wave_lds_sync();
-#pragma unroll
-      for (int o = 0; o < 2; ++o) {
-        if (!a.img_out[o].img) continue;
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-          scratch_to_image(scr, 32 * h, a.img_out[o].gain, kTileN * t + 32 * h, a.M, mt, a.MT,
-                           2 * t + h, a.img_out[o].img);
-      }
-      wave_lds_sync();
-    }
+    if (valid)
+      *reinterpret_cast<float4*>(a.x + (size_t)mm * a.N + n0) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
   }
-}
-
-template <int MT>
-__device__ void epi_swiglu(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4], float* scr,
-                           const float (&mu)[MT], const float (&rs)[MT]) {
-  const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
-  for (int mt = 0; mt < MT; ++mt) {
+  if (a.stats_out) {
+    sum += __shfl_xor(sum, 16);
+    sum += __shfl_xor(sum, 32);
+    const float mean = sum * (1.0f / kTileN);
+    float m2 = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      float act[4];
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float g = normed(a, acc[mt][j][r], mu[mt], rs[mt], out_col(a, t, j, q, r));
-        const float u = normed(a, acc[mt][j + 2][r], mu[mt], rs[mt], out_col(a, t, j + 2, q, r));
-        act[r] = silu(g) * u;
+        const float dv = v[j][r] - mean;
+        m2 += dv * dv;
       }
+    m2 += __shfl_xor(m2, 16);
+    m2 += __shfl_xor(m2, 32);
+    if (q == 0 && valid) a.stats_out[(size_t)t * a.M + m] = make_float2(mean, m2);
+  }
+  if (a.img_out[0].img || a.img_out[1].img) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
       *reinterpret_cast<float4*>(scr + r16 * kScr + 16 * j + 4 * q) =
-          make_float4(act[0], act[1], act[2], act[3]);
-    }
+          make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
     wave_lds_sync();
-    scratch_to_image(scr, 0, nullptr, 0, a.M, mt, a.MT, t, a.act_img);
+#pragma unroll
+    for (int o = 0; o < 2; ++o) {
+      if (!a.img_out[o].img) continue;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        scratch_to_image(scr, 32 * h, in.gain[o][h], a.M, mt, a.MT, 2 * t + h, a.img_out[o].img);
+    }
     wave_lds_sync();
   }
 }
 
-template <int MT>
-__device__ void epi_relu(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4], float* scr,
-                         const float (&mu)[MT], const float (&rs)[MT]) {
+__device__ void epi_swiglu(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4], float* scr,
+                           float mu, float rs) {
   const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
-  for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float v[4];
+  for (int j = 0; j < 2; ++j) {
+    float act[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int col = out_col(a, t, j, q, r);
-        float y = normed(a, acc[mt][j][r], mu[mt], rs[mt], col);
-        if (a.b0) y += bf2f(a.b0[col]);
-        v[r] = fmaxf(y, 0.0f);
-      }
-      *reinterpret_cast<float4*>(scr + r16 * kScr + 16 * j + 4 * q) = make_float4(v[0], v[1], v[2], v[3]);
+    for (int r = 0; r < 4; ++r) {
+      const float g = normed(a, acc[j][r], mu, rs, out_col(a, t, j, q, r));
+      const float u = normed(a, acc[j + 2][r], mu, rs, out_col(a, t, j + 2, q, r));
+      act[r] = silu(g) * u;
     }
-    wave_lds_sync();
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-      scratch_to_image(scr, 32 * h, nullptr, 0, a.M, mt, a.MT, 2 * t + h, a.act_img);
-    wave_lds_sync();
+    *reinterpret_cast<float4*>(scr + r16 * kScr + 16 * j + 4 * q) =
+        make_float4(act[0], act[1], act[2], act[3]);
   }
+  wave_lds_sync();
+  scratch_to_image(scr, 0, kUnitGain, a.M, mt, a.MT, t, a.act_img);
+  wave_lds_sync();
 }
 
-template <int MT>
-__device__ void epi_qkv(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4],
-                        const float (&mu)[MT], const float (&rs)[MT]) {
+__device__ void epi_relu(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4], float* scr,
+                         float mu, float rs) {
+  const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float v[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int col = out_col(a, t, j, q, r);
+      float y = normed(a, acc[j][r], mu, rs, col);
+      if (a.b0) y += bf2f(a.b0[col]);
+      v[r] = fmaxf(y, 0.0f);
+    }
+    *reinterpret_cast<float4*>(scr + r16 * kScr + 16 * j + 4 * q) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  wave_lds_sync();
+#pragma unroll
+  for (int h = 0; h < 2; ++h) scratch_to_image(scr, 32 * h, kUnitGain, a.M, mt, a.MT, 2 * t + h, a.act_img);
+  wave_lds_sync();
+}
+
+__device__ void epi_qkv(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4], float mu,
+                        float rs, const EpiIn& in) {
   const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
   const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
   const int H = a.n_heads, Hk = a.n_kv_heads;
   const int hh = t / tph, gi = t - hh * tph;
   const int which = hh < H ? 0 : (hh < H + Hk ? 1 : 2);
   const int hloc = hh - (which == 0 ? 0 : (which == 1 ? H : H + Hk));
-  const uint16_t* bias = which == 0 ? a.b0 : (which == 1 ? a.b1 : a.b2);
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = 16 * mt + r16;
-    if (m >= a.M) continue;
-    const int b = m / a.n_slots, slot = m - b * a.n_slots;
-    const int L = a.len[b];
-    if (L + a.n_slots > a.capacity) {
-      if (q == 0 && slot == 0) atomicOr(a.status, 1u);
-      continue;
-    }
-    const int pos = L + a.depth[slot];
+  const int m = 16 * mt + r16;
+  if (m >= a.M) return;
+  const int b = m / a.n_slots, slot = m - b * a.n_slots;
+  const int L = in.L;
+  if (L < 0 || L + a.n_slots > a.capacity) {
+    if (q == 0 && slot == 0) atomicOr(a.status, 1u);
+    return;
+  }
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int dlo = gi * 32 + 16 * j + 4 * q, dhi = half + dlo;
-      float lo[4], hi[4];
+  for (int j = 0; j < 2; ++j) {
+    const int dlo = gi * 32 + 16 * j + 4 * q, dhi = half + dlo;
+    const float blo[4] = {bf_lo(in.qb[j][0][0]), bf_hi(in.qb[j][0][0]), bf_lo(in.qb[j][0][1]),
+                          bf_hi(in.qb[j][0][1])};
+    const float bhi[4] = {bf_lo(in.qb[j][1][0]), bf_hi(in.qb[j][1][0]), bf_lo(in.qb[j][1][1]),
+                          bf_hi(in.qb[j][1][1])};
+    float lo[4], hi[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      lo[r] = normed(a, acc[j][r], mu, rs, hh * hd + dlo + r) + blo[r];
+      hi[r] = normed(a, acc[j + 2][r], mu, rs, hh * hd + dhi + r) + bhi[r];
+    }
+    if (which < 2 && a.rope) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        lo[r] = normed(a, acc[mt][j][r], mu[mt], rs[mt], hh * hd + dlo + r);
-        hi[r] = normed(a, acc[mt][j + 2][r], mu[mt], rs[mt], hh * hd + dhi + r);
-        if (bias) {
-          lo[r] += bf2f(bias[hloc * hd + dlo + r]);
-          hi[r] += bf2f(bias[hloc * hd + dhi + r]);
-        }
+        const float2 c = in.cs[j][r];
+        const float rl = lo[r] * c.x - hi[r] * c.y;
+        const float rh = hi[r] * c.x + lo[r] * c.y;
+        lo[r] = rl;
+        hi[r] = rh;
       }
-      if (which < 2 && a.rope) {
-        const float2* cs = a.rope + (size_t)pos * half + dlo;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float2 c = cs[r];
-          const float rl = lo[r] * c.x - hi[r] * c.y;
-          const float rh = hi[r] * c.x + lo[r] * c.y;
-          lo[r] = rl;
-          hi[r] = rh;
-        }
-      }
-      if (which == 0) {
-        float* qp = a.q_out + ((size_t)m * H + hloc) * hd;
-        *reinterpret_cast<float4*>(qp + dlo) = make_float4(lo[0], lo[1], lo[2], lo[3]);
-        *reinterpret_cast<float4*>(qp + dhi) = make_float4(hi[0], hi[1], hi[2], hi[3]);
-      } else {
-        uint16_t* cache = which == 1 ? a.k_cache : a.v_cache;
-        uint16_t* row = cache + (((size_t)b * Hk + hloc) * a.capacity + L + slot) * hd;
-        const u32x2 wl = {pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
-        const u32x2 wh = {pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
-        *reinterpret_cast<u32x2*>(row + dlo) = wl;
-        *reinterpret_cast<u32x2*>(row + dhi) = wh;
-      }
+    }
+    if (which == 0) {
+      float* qp = a.q_out + ((size_t)m * H + hloc) * hd;
+      *reinterpret_cast<float4*>(qp + dlo) = make_float4(lo[0], lo[1], lo[2], lo[3]);
+      *reinterpret_cast<float4*>(qp + dhi) = make_float4(hi[0], hi[1], hi[2], hi[3]);
+    } else {
+      uint16_t* cache = which == 1 ? a.k_cache : a.v_cache;
+      uint16_t* row = cache + (((size_t)b * Hk + hloc) * a.capacity + L + slot) * hd;
+      const u32x2 wl = {pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
+      const u32x2 wh = {pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
+      *reinterpret_cast<u32x2*>(row + dlo) = wl;
+      *reinterpret_cast<u32x2*>(row + dhi) = wh;
     }
   }
 }
 
 // Per row of the tile: logits out, (max, sum exp), top-kappa rank keys.
-template <int MT>
-__device__ void epi_head(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4],
-                         const float (&mu)[MT], const float (&rs)[MT]) {
+__device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4], float mu,
+                         float rs) {
   const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = 16 * mt + r16;
-    const bool valid = m < a.M;
-    float v[4][4];
-    float mx = -INFINITY;
+  const int m = 16 * mt + r16;
+  const bool valid = m < a.M;
+  float v[4][4];
+  float mx = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n0 = kTileN * t + 16 * j + 4 * q;
-      const bool cv = kTileN * t + 16 * j < a.N;  // N % 16 == 0: whole groups
+  for (int j = 0; j < 4; ++j) {
+    const int n0 = kTileN * t + 16 * j + 4 * q;
+    const bool cv = kTileN * t + 16 * j < a.N;  // N % 16 == 0: whole groups
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        v[j][r] = cv ? normed(a, acc[mt][j][r], mu[mt], rs[mt], cv ? n0 + r : 0) : -INFINITY;
-        mx = fmaxf(mx, v[j][r]);
-      }
-      if (a.logits && valid && cv)
-        *reinterpret_cast<float4*>(a.logits + (size_t)m * a.N + n0) =
-            make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+    for (int r = 0; r < 4; ++r) {
+      v[j][r] = cv ? normed(a, acc[j][r], mu, rs, cv ? n0 + r : 0) : -INFINITY;
+      mx = fmaxf(mx, v[j][r]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    float se = 0.0f;
+    if (a.logits && valid && cv)
+      *reinterpret_cast<float4*>(a.logits + (size_t)m * a.N + n0) =
+          make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  float se = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) se += v[j][r] == -INFINITY ? 0.0f : expf(v[j][r] - mx);
+  se += __shfl_xor(se, 16);
+  se += __shfl_xor(se, 32);
+  if (q == 0 && valid) a.tile_ms[(size_t)t * a.M + m] = make_float2(mx, se);
+  uint64_t key[4][4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      key[j][r] = v[j][r] == -INFINITY ? 0ull : rank_key(v[j][r], kTileN * t + 16 * j + 4 * q + r);
+  uint64_t* top = a.tile_top + ((size_t)t * a.M + (valid ? m : 0)) * a.kappa;
+  for (int rr = 0; rr < a.kappa; ++rr) {
+    uint64_t best = 0ull;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) se += v[j][r] == -INFINITY ? 0.0f : expf(v[j][r] - mx);
-    se += __shfl_xor(se, 16);
-    se += __shfl_xor(se, 32);
-    if (q == 0 && valid) a.tile_ms[(size_t)t * a.M + m] = make_float2(mx, se);
-    uint64_t key[4][4];
+      for (int r = 0; r < 4; ++r) best = key[j][r] > best ? key[j][r] : best;
+    uint64_t o = __shfl_xor(best, 16);
+    best = o > best ? o : best;
+    o = __shfl_xor(best, 32);
+    best = o > best ? o : best;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        key[j][r] = v[j][r] == -INFINITY ? 0ull : rank_key(v[j][r], kTileN * t + 16 * j + 4 * q + r);
-    uint64_t* top = a.tile_top + ((size_t)t * a.M + (valid ? m : 0)) * a.kappa;
-    for (int rr = 0; rr < a.kappa; ++rr) {
-      uint64_t best = 0ull;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) best = key[j][r] > best ? key[j][r] : best;
-      uint64_t o = __shfl_xor(best, 16);
-      best = o > best ? o : best;
-      o = __shfl_xor(best, 32);
-      best = o > best ? o : best;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) key[j][r] = key[j][r] == best ? 0ull : key[j][r];
-      if (q == 0 && valid) top[rr] = best;
-    }
+      for (int r = 0; r < 4; ++r) key[j][r] = key[j][r] == best ? 0ull : key[j][r];
+    if (q == 0 && valid) top[rr] = best;
   }
 }
 
+// The epilogue of the finished tile. in1 holds the inputs of a single row
+// tile loaded ahead (MT == 1); otherwise each row tile loads its own here.
 template <int MT, int EPI>
-__device__ __forceinline__ void epilogue(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4], float* scr) {
-  if constexpr (EPI == EPI_RESID) {
-    epi_resid<MT>(a, t, acc, scr);
-  } else {
-    float mu[MT], rs[MT];
-    row_norm<MT>(a, mu, rs);
-    if constexpr (EPI == EPI_QKV) epi_qkv<MT>(a, t, acc, mu, rs);
-    else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<MT>(a, t, acc, scr, mu, rs);
-    else if constexpr (EPI == EPI_RELU) epi_relu<MT>(a, t, acc, scr, mu, rs);
-    else epi_head<MT>(a, t, acc, mu, rs);
+__device__ __forceinline__ void epilogue(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4],
+                                         float* scr, const EpiIn& in1) {
+  for (int mt = 0; mt < MT; ++mt) {
+    EpiIn inl;
+    if constexpr (MT > 1) {
+      if constexpr (EPI == EPI_QKV) inl.L = row_len(a, 16 * mt + (threadIdx.x & 15));
+      epi_load<EPI>(a, t, mt, inl);
+    }
+    const EpiIn& in = MT == 1 ? in1 : inl;
+    float mu = 0.0f, rs = 1.0f;
+    if constexpr (has_norm<EPI>()) norm_finish(a, in, mu, rs);
+    if constexpr (EPI == EPI_RESID) epi_resid(a, t, mt, acc[mt], scr, in);
+    else if constexpr (EPI == EPI_QKV) epi_qkv(a, t, mt, acc[mt], mu, rs, in);
+    else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, t, mt, acc[mt], scr, mu, rs);
+    else if constexpr (EPI == EPI_RELU) epi_relu(a, t, mt, acc[mt], scr, mu, rs);
+    else epi_head(a, t, mt, acc[mt], mu, rs);
   }
 }
 
@@ -453,6 +501,11 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) wp[j] = weight_frag(a, t, j, lane);
   const uint16_t* ap = a.a_img + lane * 8;
+
+  // one row tile: the epilogue's inputs are loaded ahead (the sequence
+  // length that addresses the rotary table before the k-loop)
+  EpiIn in1;
+  if constexpr (MT == 1 && EPI == EPI_QKV) in1.L = row_len(a, lane & 15);
 
   floatx4 acc[MT][4];
 #pragma unroll
@@ -511,6 +564,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int d = 0; d < D; ++d)
       if (d < n) compute(st[d]);
+  }
+
+  if constexpr (MT == 1) {
+    if (wave == 0 && !a.decoupled) epi_load<EPI>(a, t, 0, in1);
   }
 
   // fixed-order sum of the waves' tiles
@@ -597,7 +654,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
     if (lane == 0) counter_reset(&a.counters[t]);
   }
 
-  epilogue<MT, EPI>(a, t, acc, scr);
+  epilogue<MT, EPI>(a, t, acc, scr, in1);
 }
 
 // Epilogue of a decoupled split-K GEMM: one wave per output tile sums the
@@ -631,7 +688,12 @@ __global__ __launch_bounds__(64) void gemm_epi_kernel(GemmArgs a) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) acc[mt][j] += part[u][mt][j];
   }
-  epilogue<MT, EPI>(a, t, acc, scr);
+  EpiIn in1;
+  if constexpr (MT == 1) {
+    if constexpr (EPI == EPI_QKV) in1.L = row_len(a, lane & 15);
+    epi_load<EPI>(a, t, 0, in1);
+  }
+  epilogue<MT, EPI>(a, t, acc, scr, in1);
 }
 
 template <int MT, int NW, int EPI>
