@@ -250,8 +250,9 @@ msd_status msd_kv_commit(const msd_model* model, msd_kv_cache* kv, const msd_blo
  * begin[i] / end[i] on its stream around the launch of kernel class `kclass`
  * in layer i (i < n; classes: 0 QKV projection, 1 attention, 2 output
  * projection, 3 FFN up projection, 4 FFN down projection). The events are
- * caller-owned HIP events; pass n = 0 to switch it off. Not thread-safe
- * with concurrent verify calls on the same model.
+ * caller-owned HIP events; a NULL pair skips that layer (sampling a few
+ * layers keeps the events' own cost low); pass n = 0 to switch it off. Not
+ * thread-safe with concurrent verify calls on the same model.
  */
 enum { MSD_K_QKV = 0, MSD_K_ATTN = 1, MSD_K_OPROJ = 2, MSD_K_FFN_UP = 3, MSD_K_FFN_DOWN = 4 };
 msd_status msd_set_profile(msd_model* model, int32_t kclass, hipEvent_t* begin, hipEvent_t* end,

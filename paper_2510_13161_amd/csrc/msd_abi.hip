@@ -251,7 +251,8 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 hipError_t prof_mark(const msd_model* m, int kclass, int layer, bool begin, hipStream_t s) {
   if (m->prof_class != kclass || layer >= (int)m->prof_begin.size()) return hipSuccess;
-  return hipEventRecord(begin ? m->prof_begin[layer] : m->prof_end[layer], s);
+  hipEvent_t ev = begin ? m->prof_begin[layer] : m->prof_end[layer];
+  return ev ? hipEventRecord(ev, s) : hipSuccess;
 }
 
 }  // namespace

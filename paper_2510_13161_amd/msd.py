@@ -169,7 +169,8 @@ def kv_commit(handle, kv: KVCache, block: Block, acc_len, path, stream=None) -> 
 
 
 def set_profile(handle, kclass: int, begin_events, end_events) -> None:
-    """begin/end: sequences of raw hipEvent_t handles (ints), one per layer; [] turns it off."""
+    """begin/end: sequences of raw hipEvent_t handles (ints), one per layer,
+    None to skip a layer; [] turns it off."""
     n = len(begin_events)
     B = (ctypes.c_void_p * max(n, 1))(*begin_events)
     E = (ctypes.c_void_p * max(n, 1))(*end_events)
