@@ -15,9 +15,10 @@
 // every exponential is one hardware exp2.
 // The 4 waves' (max, sum, output) are merged in LDS in wave order. A chunk
 // that covers the whole sequence writes the normalised output straight into
-// the output-projection's activation image; otherwise chunks publish their
-// partials and a second kernel merges them in chunk order. All statistics
-// in fp32; no floating-point atomics.
+// the output-projection's activation image; otherwise the chunks publish
+// their partials with coherent stores and the last chunk of the (sequence,
+// kv head, query tile) to arrive merges all of them in chunk order. All
+// statistics in fp32; no floating-point atomics: bit-reproducible.
 #include "kernels.h"
 
 namespace msd {
@@ -230,6 +231,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
   __syncthreads();
   // merge the 4 waves (wave order), then output or publish the chunk
+  const size_t pbase = ((size_t)b * a.n_kv_heads + kvh) * a.max_chunks;
   for (int x = tid; x < 16 * C8; x += blockDim.x) {
     const int qloc = x / C8, c8 = x - qloc * C8;
     const int qg = qt * 16 + qloc;
@@ -261,82 +263,75 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       for (int e = 0; e < 8; ++e) o8[e] *= inv;
       write_out<HD>(a, b, kvh, qg, c8, o8);
     } else {
-      const size_t pidx = (((size_t)b * a.n_kv_heads + kvh) * a.max_chunks + c) * Qn + qg;
+      const size_t pidx = (pbase + c) * Qn + qg;
       float* po = a.part_o + pidx * HD + 8 * c8;
-      *reinterpret_cast<float4*>(po) = make_float4(o8[0], o8[1], o8[2], o8[3]);
-      *reinterpret_cast<float4*>(po + 4) = make_float4(o8[4], o8[5], o8[6], o8[7]);
-      if (c8 == 0) reinterpret_cast<float2*>(a.part_ml)[pidx] = make_float2(M, S);
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) store_coherent2(po + e, o8[e], o8[e + 1]);
+      if (c8 == 0) store_coherent2(a.part_ml + 2 * pidx, M, S);
     }
   }
-}
+  if (nch == 1) return;
 
-// Merge of the chunk partials of sequences that span more than one chunk:
-// one thread per (sequence, kv head, query, 8 output dims), chunks in order;
-// the partial maxima are in base-2 units like the scores they came from.
-template <int HD>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-  constexpr int C8 = HD / 8;
-  const int G = a.n_heads / a.n_kv_heads, ns = a.n_slots, Qn = G * ns;
-  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t per_seq = (int64_t)a.n_kv_heads * Qn * C8;
-  if (x >= (int64_t)a.batch * per_seq) return;
-  const int b = (int)(x / per_seq);
-  int64_t rem = x - b * per_seq;
-  const int kvh = (int)(rem / ((int64_t)Qn * C8));
-  rem -= (int64_t)kvh * Qn * C8;
-  const int qg = (int)(rem / C8), c8 = (int)(rem - (int64_t)qg * C8);
-  const int T = a.len[b] + ns;
-  if (T > a.capacity) return;
-  const int nch = (T + kAttnChunk - 1) / kAttnChunk;
-  if (nch == 1) return;  // the chunk kernel wrote the output directly
-  const size_t base = ((size_t)b * a.n_kv_heads + kvh) * a.max_chunks;
-  float M = -INFINITY, S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int c0 = 0; c0 < nch; c0 += 4) {
-    float2 ml[4];
-    float4 v0[4], v1[4];
+  // hand-off: the last chunk to arrive merges the chunks in chunk order
+  __shared__ int last;
+  drain_stores();
+  __syncthreads();
+  int32_t* ctr = a.counters + ((size_t)b * a.n_kv_heads + kvh) * QT + qt;
+  if (tid == 0) last = counter_add(ctr, 1) == nch - 1;
+  __syncthreads();
+  if (!last) return;
+  for (int x = tid; x < 16 * C8; x += blockDim.x) {
+    const int qloc = x / C8, c8 = x - qloc * C8;
+    const int qg = qt * 16 + qloc;
+    if (qg >= Qn) continue;
+    float M = -INFINITY, S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int c0 = 0; c0 < nch; c0 += 4) {
+      float2 ml[4];
+      float v[4][8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int cc = c0 + u < nch ? c0 + u : c0;
-      const size_t pidx = (base + cc) * Qn + qg;
-      ml[u] = reinterpret_cast<const float2*>(a.part_ml)[pidx];
-      const float* po = a.part_o + pidx * HD + 8 * c8;
-      v0[u] = *reinterpret_cast<const float4*>(po);
-      v1[u] = *reinterpret_cast<const float4*>(po + 4);
+      for (int u = 0; u < 4; ++u) {
+        const int cc = c0 + u < nch ? c0 + u : c0;
+        const size_t pidx = (pbase + cc) * Qn + qg;
+        ml[u] = load_coherent2(a.part_ml + 2 * pidx);
+        const float* po = a.part_o + pidx * HD + 8 * c8;
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const float2 t2 = load_coherent2(po + e);
+          v[u][e] = t2.x;
+          v[u][e + 1] = t2.y;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
+        const float Mn = fmaxf(M, ml[u].x);
+        const float fa = M == -INFINITY ? 0.0f : exp2_hw(M - Mn);
+        const float fb = exp2_hw(ml[u].x - Mn);
+        S = S * fa + ml[u].y * fb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o8[e] = o8[e] * fa + v[u][e] * fb;
+        M = Mn;
+      }
     }
+    const float inv = S > 0.0f ? 1.0f / S : 0.0f;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
-      const float Mn = fmaxf(M, ml[u].x);
-      const float fa = M == -INFINITY ? 0.0f : exp2_hw(M - Mn);
-      const float fb = exp2_hw(ml[u].x - Mn);
-      S = S * fa + ml[u].y * fb;
-      const float pv[8] = {v0[u].x, v0[u].y, v0[u].z, v0[u].w, v1[u].x, v1[u].y, v1[u].z, v1[u].w};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o8[e] = o8[e] * fa + pv[e] * fb;
-      M = Mn;
-    }
+    for (int e = 0; e < 8; ++e) o8[e] *= inv;
+    write_out<HD>(a, b, kvh, qg, c8, o8);
   }
-  const float inv = S > 0.0f ? 1.0f / S : 0.0f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) o8[e] *= inv;
-  write_out<HD>(a, b, kvh, qg, c8, o8);
+  if (tid == 0) counter_reset(ctr);
 }
 
 }  // namespace
 
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s) {
   if (a.max_chunks > kMaxAttnChunks || a.max_chunks < 1) return hipErrorInvalidValue;
+  if (a.max_chunks > 1 && !a.counters) return hipErrorInvalidValue;
   const int qt = (a.n_heads / a.n_kv_heads * a.n_slots + 15) / 16;
   const dim3 grid(a.max_chunks, a.n_kv_heads * qt, a.batch);
-  const int64_t items = (int64_t)a.batch * a.n_kv_heads * (a.n_heads / a.n_kv_heads) * a.n_slots *
-                        (head_dim / 8);
-  const dim3 mgrid((unsigned)((items + 255) / 256));
   if (head_dim == 128) {
     hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, s, a);
-    if (a.max_chunks > 1) hipLaunchKernelGGL(attn_merge_kernel<128>, mgrid, dim3(256), 0, s, a);
   } else if (head_dim == 64) {
     hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, s, a);
-    if (a.max_chunks > 1) hipLaunchKernelGGL(attn_merge_kernel<64>, mgrid, dim3(256), 0, s, a);
   } else {
     return hipErrorInvalidValue;
   }

@@ -101,7 +101,7 @@ Shapes shapes(const msd_model* m, int M) {
 struct Layout {
   size_t x, stats, q, img_x, img_h, img_f, img_attn, img_act, partial, counters, part_o, part_ml,
       tile_ms, tile_top, head_ms, head_top, total;
-  int64_t n_counters;
+  int64_t n_counters, n_gemm_counters;
   int32_t MT, max_chunks;
 };
 
@@ -140,7 +140,11 @@ Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacit
     }
   }
   L.partial = take(part);
-  L.n_counters = max_tiles;
+  // the GEMMs' split-K counters, then the attention's chunk counters (one per
+  // sequence, kv head and query tile); all cleared by the rows kernel
+  const int attn_qt = ((c.n_heads / c.n_kv_heads) * n_slots + 15) / 16;
+  L.n_gemm_counters = max_tiles;
+  L.n_counters = max_tiles + (int64_t)batch * c.n_kv_heads * attn_qt;
   L.counters = take((size_t)L.n_counters * sizeof(int32_t));
   L.max_chunks = (capacity + kAttnChunk - 1) / kAttnChunk;
   const size_t qn = (size_t)(c.n_heads / c.n_kv_heads) * n_slots;
@@ -571,6 +575,7 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
     aa.status = kv->status;
     aa.out_img = img_attn;
     aa.MT = L.MT;
+    aa.counters = counters + L.n_gemm_counters;
     aa.part_o = reinterpret_cast<float*>(w + L.part_o);
     aa.part_ml = reinterpret_cast<float*>(w + L.part_ml);
     aa.batch = blk->batch;
