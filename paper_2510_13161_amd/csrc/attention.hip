@@ -6,8 +6,8 @@
 // Flash-decoding over 256-key chunks: a workgroup owns one (sequence, kv
 // head, 16-query tile of the head's GQA group, chunk) and each of its 4 waves
 // one 64-key block. A wave loads its block's K as MFMA operands and V rows
-// into its own LDS (16-byte writes, read back transposed two bytes at a time
-// with conflict-free strides), then
+// into its own LDS (16-byte writes, read back as P V operands with the
+// gfx950 transposing LDS read), then
 //   S^T[key][query] = K Q^T        MFMA 16x16x32; Q (fp32) as bf16 hi + lo;
 //   block softmax statistics       one query per lane column: 2 shuffles;
 //   O[query][d] += P V             P stays in registers as the MFMA operand.
@@ -25,6 +25,9 @@ namespace msd {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -139,22 +142,19 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     *reinterpret_cast<u32x4*>(vs + key * Lds::kVS + (lane % (HD / 8)) * 8) = vraw[it];
   }
   __syncthreads();
+  // transposing LDS reads: in each 16-lane group, lane i receives element
+  // i % 4 of the 8-byte chunks addressed by lanes i / 4 + 4 k (k < 4), so
+  // lane s of group g points at key 32 kb + 4 g + s / 4 (+ 16), dims
+  // 16 ds + 4 (s % 4) .. +4, and gets dim 16 ds + s of keys 4 g + k
   bf16x8 vb[2][DSUB];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int ds = 0; ds < DSUB; ++ds) {
-      const uint16_t* col = vs + 16 * ds + r16;
-      uint16_t e8[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        e8[e] = col[(32 * kb + 4 * g + e) * Lds::kVS];
-        e8[4 + e] = col[(32 * kb + 16 + 4 * g + e) * Lds::kVS];
-      }
-      u32x4 w;
-#pragma unroll
-      for (int x = 0; x < 4; ++x) w[x] = (uint32_t)e8[2 * x] | ((uint32_t)e8[2 * x + 1] << 16);
-      vb[kb][ds] = __builtin_bit_cast(bf16x8, w);
+      const uint16_t* p0 = vs + (32 * kb + 4 * g + (r16 >> 2)) * Lds::kVS + 16 * ds + 4 * (r16 & 3);
+      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p0);
+      const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0 + 16 * Lds::kVS));
+      vb[kb][ds] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
     }
 
   const int qv = qt * 16 + r16;
