@@ -567,7 +567,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   }
 
   if constexpr (MT == 1) {
-    if (wave == 0 && !a.decoupled) epi_load<EPI>(a, t, 0, in1);
+    if (wave == 0) epi_load<EPI>(a, t, 0, in1);
   }
 
   // fixed-order sum of the waves' tiles
@@ -596,16 +596,6 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
     if (wave != 0) return;
   }
 
-  if (a.decoupled) {
-    // publish this split's tile for the separate epilogue kernel (plain
-    // stores; the kernel boundary orders them)
-    float* slot = a.partial + ((size_t)t * a.splits + s) * (MT * 1024) + lane * 4;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) *reinterpret_cast<floatx4*>(slot + (mt * 4 + j) * 256) = acc[mt][j];
-    return;
-  }
   if (a.splits > 1) {
     // publish this split's tile; the last split to arrive sums all of them
     float* slot = a.partial + ((size_t)t * a.splits + s) * (MT * 1024) + lane * 4;
@@ -657,49 +647,9 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   epilogue<MT, EPI>(a, t, acc, scr, in1);
 }
 
-// Epilogue of a decoupled split-K GEMM: one wave per output tile sums the
-// tile's split partials in split order and runs the epilogue.
-template <int MT, int EPI>
-__global__ __launch_bounds__(64) void gemm_epi_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) float scr[16 * kScr];
-  const int lane = threadIdx.x, t = blockIdx.x;
-  floatx4 acc[MT][4];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const float* base = a.partial + (size_t)t * a.splits * (MT * 1024) + lane * 4;
-  for (int sp0 = 0; sp0 < a.splits; sp0 += 4) {
-    floatx4 part[4][MT][4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int sp = sp0 + u < a.splits ? sp0 + u : sp0;
-      const float* src = base + (size_t)sp * (MT * 1024);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) part[u][mt][j] = *reinterpret_cast<const floatx4*>(src + (mt * 4 + j) * 256);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (sp0 + u < a.splits)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[mt][j] += part[u][mt][j];
-  }
-  EpiIn in1;
-  if constexpr (MT == 1) {
-    if constexpr (EPI == EPI_QKV) in1.L = row_len(a, lane & 15);
-    epi_load<EPI>(a, t, 0, in1);
-  }
-  epilogue<MT, EPI>(a, t, acc, scr, in1);
-}
-
 template <int MT, int NW, int EPI>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((gemm_kernel<MT, NW, EPI>), dim3(a.n_tiles * a.splits), dim3(64 * NW), 0, s, a);
-  if (a.decoupled) hipLaunchKernelGGL((gemm_epi_kernel<MT, EPI>), dim3(a.n_tiles), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -761,7 +711,6 @@ __global__ __launch_bounds__(256) void colsum_kernel(const uint16_t* w, int64_t 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
   if (a.n_tiles < 1 || a.splits < 1 || a.K % 32 || a.M < 1 || a.M > 16 * a.MT) return hipErrorInvalidValue;
   if (a.splits > 1 && (!a.partial || !a.counters)) return hipErrorInvalidValue;
-  if (a.decoupled && !a.partial) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_QKV: return launch_epi<EPI_QKV>(a, s);
     case EPI_RESID: return launch_epi<EPI_RESID>(a, s);

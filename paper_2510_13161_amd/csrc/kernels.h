@@ -52,8 +52,6 @@ struct GemmArgs {
   const uint16_t* a_img;   // input image [K/32][MT][2][64][8]
   int32_t M, MT, K, N;     // N = logical output columns (padding masked)
   int32_t n_tiles, splits, waves;
-  int32_t decoupled;       // 1: splits publish plain partials, a second kernel
-                           // (one wave per tile) sums them and runs the epilogue
   int32_t map;
   const uint16_t* w0;
   const uint16_t* w1;

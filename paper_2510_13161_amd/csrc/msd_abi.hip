@@ -22,7 +22,7 @@ struct msd_model {
   const float* head_c = nullptr;
   const float* head_e = nullptr;
   int32_t target_wgs = 240;        // split-K sizing target (workgroups per GEMM)
-  int32_t waves = 8;               // GEMM waves per workgroup for one row tile
+  int32_t waves = 8;               // waves of a split-K workgroup for one row tile
   int32_t prof_class = -1;         // instrumentation (msd_set_profile)
   std::vector<hipEvent_t> prof_begin, prof_end;
 };
@@ -77,9 +77,12 @@ struct Shapes {
   GemmShape qkv, o, up, down, head;
 };
 
+// Waves per workgroup: with one row tile, a GEMM with fewer tiles than the
+// workgroup target runs split-K workgroups of m->waves (8) waves; one with
+// at least that many tiles (FFN up, LM head) runs whole-K workgroups of 4
+// waves, two of which fit a CU. Several row tiles: 4 waves.
 Shapes shapes(const msd_model* m, int M) {
   const msd_model_config& c = m->cfg;
-  const int waves = row_tiles(M) == 1 ? m->waves : 4;
   Shapes s;
   s.qkv.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim / kTileN;
   s.qkv.K = c.d_model;
@@ -92,8 +95,8 @@ Shapes shapes(const msd_model* m, int M) {
   s.head.n_tiles = (c.vocab + kTileN - 1) / kTileN;
   s.head.K = c.d_model;
   for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
-    g->waves = waves;
-    g->splits = splits_for(m, g->n_tiles, g->K, waves);
+    g->waves = row_tiles(M) == 1 && g->n_tiles < m->target_wgs ? m->waves : 4;
+    g->splits = splits_for(m, g->n_tiles, g->K, g->waves);
   }
   return s;
 }
