@@ -18,6 +18,8 @@
  *                        (Sec. 2 greedy rule; stochastic rules, see below).
  *   msd_kv_commit        Sec. 2: commit the accepted tokens (and the root) to
  *                        the KV cache; everything else rolls back.
+ *   msd_reuse_select     Sec. 3.1 reuse criterion and next-window selection,
+ *                        App. C fallback statistics.
  *
  * Conventions
  *  - Every pointer marked "device" is HIP device memory owned by the caller;
@@ -244,6 +246,60 @@ msd_status msd_accept(const msd_model* model, const msd_block* block, const floa
  */
 msd_status msd_kv_commit(const msd_model* model, msd_kv_cache* kv, const msd_block* block,
                          const int32_t* acc_len, const int32_t* path, hipStream_t stream);
+
+/*
+ * Reuse criterion and next-window selection (Sec. 3.1, "Verification vs.
+ * reuse criterion" and "Operational selection of the next window") with the
+ * fallback statistics of App. C.
+ *
+ * The hypothesis tree T_t is what the draft built from the early-exit top-k
+ * roots: node i at depth d_i (roots d = 1) holds the token for position
+ * t + d_i, where position t + 1 is the one the current block's root row
+ * predicts. Topology is shared by the batch, tokens are per sequence.
+ */
+#define MSD_MAX_TREE_NODES 256
+typedef struct {
+  int32_t n_nodes;          /* 1 <= n_nodes <= MSD_MAX_TREE_NODES            */
+  const int32_t* parent;    /* host [n_nodes]; -1 = root, else 0 <= p < i   */
+  const int32_t* tokens;    /* device [batch][n_nodes]                       */
+} msd_hyp_tree;
+
+enum { MSD_NEXT_BRANCH = 0, MSD_NEXT_CONTINUE = 1, MSD_NEXT_FRESH = 2 };
+
+/* Running fallback statistics (device memory, zeroed once by the caller and
+ * accumulated by every call; calls sharing one must be stream-ordered).
+ * One trial = one sequence of one step. FF = fallbacks / trials; the mean
+ * overlap mass is omega_sum / omega_trials (App. C: FF <= 1 - Omega). */
+typedef struct {
+  uint64_t trials;
+  uint64_t fallbacks;        /* F_t = 1: fresh rollout                        */
+  uint64_t fallbacks_tau1;   /* of which A_t = 0                              */
+  uint64_t omega_trials;     /* trials with Omega computed                    */
+  double omega_sum;
+} msd_reuse_stats;
+
+/*
+ * Per sequence b, with A = acc_len[b], tau = A + 1 and the corrected prefix
+ * Pi+ = (tokens of the accepted slots path[b][1..A], next_tok[b]):
+ * reuse iff Pi+ is the token sequence of a root-to-node path of T_t ending at
+ * depth tau. Writes
+ *  next_case device int32 [batch]: MSD_NEXT_BRANCH (A = 0 and a root carries
+ *            the correction: the branch under that root is the next window),
+ *            MSD_NEXT_CONTINUE (A >= 1 and Pi+ is a path: the continuation
+ *            below its node), MSD_NEXT_FRESH (fallback: a fresh rollout)
+ *  next_node device int32 [batch]: the matched node (smallest index when
+ *            several match), -1 on fallback.
+ * Omega (optional, all of logits, lse, ee_ids non-NULL): the overlap mass at
+ * the root row, Omega_k = sum over the early-exit top-k ids of
+ * softmax(logits)[id] (App. C), fp64 accumulation, written to omega[b] if
+ * omega is non-NULL; logits/lse/ee_ids are the verify call's outputs
+ * ([M][vocab], [M], [M][kappa]). stats may be NULL.
+ */
+msd_status msd_reuse_select(const msd_model* model, const msd_block* block, const int32_t* acc_len,
+                            const int32_t* next_tok, const int32_t* path, const msd_hyp_tree* tree,
+                            const float* logits, const float* lse, const int32_t* ee_ids,
+                            int32_t kappa, int32_t* next_case, int32_t* next_node, float* omega,
+                            msd_reuse_stats* stats, hipStream_t stream);
 
 /*
  * Instrumentation (benchmarking only): when set, msd_verify_block records

@@ -4,9 +4,12 @@ TEST INFRASTRUCTURE ONLY: the test suite, ``__graft_entry__.smoke()`` and the
 benchmark's ``cpu_baseline`` leg use it; the product path never does.
 
 The functions here only marshal arrays into the C oracle and sequence its
-per-layer calls; every number comes from ``msdo.c``. The model description
-and weights come from the shared input generator (``synth``), which holds
-none of the method's arithmetic.
+per-layer calls; every number of the verification pass comes from
+``msdo.c``. The step after acceptance (the Sec. 3.1 reuse criterion over the
+draft's hypothesis tree, the App. C overlap mass) is written at the end of
+this file in plain Python and NumPy fp64. The model description and weights
+come from the shared input generator (``synth``), which holds none of the
+method's arithmetic.
 """
 from __future__ import annotations
 
@@ -318,3 +321,47 @@ def depths(parent: np.ndarray) -> np.ndarray:
     for i in range(1, len(parent)):
         d[i] = d[parent[i]] + 1
     return d
+
+
+# ---------------------------------------------------------------------------
+# After acceptance: reuse criterion and next-window selection (Sec. 3.1),
+# fallback statistics (App. C). Plain Python over the hypothesis tree (a few
+# hundred nodes at most), NumPy fp64 for the overlap mass.
+# ---------------------------------------------------------------------------
+NEXT_BRANCH, NEXT_CONTINUE, NEXT_FRESH = 0, 1, 2
+
+
+def tree_path(parent: Sequence[int], tokens: Sequence[int], v: int) -> List[int]:
+    """Tokens on the root-to-node path of node v of a hypothesis tree, root
+    first (the root at depth 1 holds the token for position t + 1)."""
+    seq = []
+    while v != -1:
+        seq.append(int(tokens[v]))
+        v = int(parent[v])
+    return seq[::-1]
+
+
+def reuse_select(parent: Sequence[int], tokens: Sequence[int], accepted: Sequence[int],
+                 correction: int) -> Tuple[int, int]:
+    """Sec. 3.1: with the accepted prefix Pi_t (A tokens) and the correction
+    c at tau = A + 1, reuse happens iff Pi_t^+ = (Pi_t, c) is a root-to-depth-
+    tau path of the hypothesis tree T_t. The next window is then the branch
+    rooted at c (A = 0) or the precomputed continuation at depth tau along
+    Pi_t (A >= 1); otherwise a fresh rollout. Returns (case, node): the case
+    (NEXT_BRANCH / NEXT_CONTINUE / NEXT_FRESH) and the smallest node whose
+    path is Pi_t^+, or -1."""
+    target = [int(x) for x in accepted] + [int(correction)]
+    for v in range(len(parent)):
+        if tree_path(parent, tokens, v) == target:
+            return (NEXT_BRANCH if len(accepted) == 0 else NEXT_CONTINUE), v
+    return NEXT_FRESH, -1
+
+
+def overlap_mass(logits_row: np.ndarray, ids: Sequence[int]) -> float:
+    """App. C: Omega_kappa = sum over the early-exit Top-kappa ids of
+    q(y) = Softmax(logits)(y), the final head's next-token law, in fp64."""
+    z = np.asarray(logits_row, dtype=np.float64)
+    mx = z.max()
+    lse = mx + np.log(np.exp(z - mx).sum())
+    return float(sum(np.exp(z[int(y)] - lse) for y in ids))
+

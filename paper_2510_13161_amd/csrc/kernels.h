@@ -195,4 +195,39 @@ struct CommitArgs {
 };
 hipError_t launch_commit(const CommitArgs& a, hipStream_t s);
 
+// ---------------------------------------------------------------------------
+// reuse criterion, next-window selection, fallback statistics
+// ---------------------------------------------------------------------------
+constexpr int kMaxTreeNodes = 256;
+
+struct TreeTopo {
+  int16_t parent[kMaxTreeNodes];  // -1 = root
+  uint8_t depth[kMaxTreeNodes];   // roots 1
+  int32_t n_nodes;
+};
+
+struct ReuseStats {  // layout of msd_reuse_stats
+  uint64_t trials, fallbacks, fallbacks_tau1, omega_trials;
+  double omega_sum;
+};
+
+struct ReuseArgs {
+  int32_t batch, n_slots;
+  const int32_t* tokens;       // the verified block [batch][n_slots]
+  const int32_t* acc_len;      // [batch]
+  const int32_t* next_tok;     // [batch]
+  const int32_t* path;         // [batch][n_slots]
+  const int32_t* tree_tokens;  // [batch][n_nodes]
+  const float* logits;         // [M][vocab] or null (no Omega)
+  const float* lse;            // [M]
+  const int32_t* ee_ids;       // [M][kappa]
+  int32_t kappa, vocab;
+  int32_t* next_case;          // [batch]
+  int32_t* next_node;          // [batch]
+  float* omega;                // [batch] or null
+  ReuseStats* stats;           // or null
+  TreeTopo tree;
+};
+hipError_t launch_reuse(const ReuseArgs& a, hipStream_t s);
+
 }  // namespace msd

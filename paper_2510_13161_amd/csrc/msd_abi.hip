@@ -13,6 +13,9 @@
 
 using namespace msd;
 
+static_assert(sizeof(msd_reuse_stats) == sizeof(ReuseStats), "reuse statistics layout");
+static_assert(MSD_MAX_TREE_NODES == kMaxTreeNodes, "hypothesis tree bound");
+
 struct msd_model {
   msd_model_config cfg;
   std::vector<const uint16_t*> t;  // MSD_N_TENSORS(n_layers) entries
@@ -755,6 +758,50 @@ msd_status msd_kv_commit(const msd_model* m, msd_kv_cache* kv, const msd_block* 
   a.copy_rows = chain ? 0 : 1;
   if (blk->n_slots < 2) a.copy_rows = 0;
   MSD_HIP(launch_commit(a, stream));
+  return MSD_OK;
+}
+
+msd_status msd_reuse_select(const msd_model* m, const msd_block* blk, const int32_t* acc_len,
+                            const int32_t* next_tok, const int32_t* path, const msd_hyp_tree* tree,
+                            const float* logits, const float* lse, const int32_t* ee_ids,
+                            int32_t kappa, int32_t* next_case, int32_t* next_node, float* omega,
+                            msd_reuse_stats* stats, hipStream_t stream) {
+  msd_status st = check_block(m, blk);
+  if (st != MSD_OK) return st;
+  if (!acc_len || !next_tok || !path || !next_case || !next_node)
+    return fail(MSD_ERR_INVALID_ARG, "null accept outputs or selection outputs");
+  if (!tree || !tree->parent || !tree->tokens) return fail(MSD_ERR_INVALID_ARG, "null hypothesis tree");
+  if (tree->n_nodes < 1 || tree->n_nodes > kMaxTreeNodes)
+    return fail(MSD_ERR_SHAPE, "hypothesis tree n_nodes must lie in [1, 256]");
+  const bool om = logits || lse || ee_ids;
+  if (om && !(logits && lse && ee_ids)) return fail(MSD_ERR_INVALID_ARG, "Omega needs logits, lse and ee_ids");
+  if (om && (kappa < 1 || kappa > kMaxKappa)) return fail(MSD_ERR_INVALID_ARG, "kappa out of [1, 32]");
+  ReuseArgs a{};
+  a.tree.n_nodes = tree->n_nodes;
+  for (int i = 0; i < tree->n_nodes; ++i) {
+    const int p = tree->parent[i];
+    if (p != -1 && (p < 0 || p >= i)) return fail(MSD_ERR_SHAPE, "tree parent[i] must be -1 or lie in [0, i)");
+    const int d = p < 0 ? 1 : a.tree.depth[p] + 1;
+    a.tree.parent[i] = (int16_t)p;
+    a.tree.depth[i] = (uint8_t)(d < 255 ? d : 255);  // deeper than any block never matches
+  }
+  a.batch = blk->batch;
+  a.n_slots = blk->n_slots;
+  a.tokens = blk->tokens;
+  a.acc_len = acc_len;
+  a.next_tok = next_tok;
+  a.path = path;
+  a.tree_tokens = tree->tokens;
+  a.logits = om ? logits : nullptr;
+  a.lse = lse;
+  a.ee_ids = ee_ids;
+  a.kappa = kappa;
+  a.vocab = m->cfg.vocab;
+  a.next_case = next_case;
+  a.next_node = next_node;
+  a.omega = omega;
+  a.stats = reinterpret_cast<ReuseStats*>(stats);
+  MSD_HIP(launch_reuse(a, stream));
   return MSD_OK;
 }
 

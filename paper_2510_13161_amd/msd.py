@@ -32,8 +32,10 @@ LAYER_SLOTS = ["attn_norm.g", "attn_norm.b", "wq", "wk", "wv", "bq", "bk", "bv",
 
 EXPORTED = ["msd_last_error", "msd_model_create", "msd_model_destroy", "msd_workspace_bytes",
             "msd_verify_block", "msd_early_exit_topk", "msd_accept", "msd_kv_commit",
-            "msd_set_profile"]
+            "msd_reuse_select", "msd_set_profile"]
 MSD_K_QKV, MSD_K_ATTN, MSD_K_OPROJ, MSD_K_FFN_UP, MSD_K_FFN_DOWN = 0, 1, 2, 3, 4
+MSD_NEXT_BRANCH, MSD_NEXT_CONTINUE, MSD_NEXT_FRESH = 0, 1, 2
+MSD_MAX_TREE_NODES = 256
 
 
 class MsdError(RuntimeError):
@@ -72,6 +74,18 @@ class Sampling(ctypes.Structure):
                 ("u_sample", ctypes.c_void_p)]
 
 
+class HypTree(ctypes.Structure):
+    _fields_ = [("n_nodes", ctypes.c_int32), ("parent", ctypes.POINTER(ctypes.c_int32)),
+                ("tokens", ctypes.c_void_p)]
+
+
+class ReuseStats(ctypes.Structure):
+    """Layout of msd_reuse_stats (40 bytes); keep it in a device tensor."""
+    _fields_ = [("trials", ctypes.c_uint64), ("fallbacks", ctypes.c_uint64),
+                ("fallbacks_tau1", ctypes.c_uint64), ("omega_trials", ctypes.c_uint64),
+                ("omega_sum", ctypes.c_double)]
+
+
 _lib = None
 
 
@@ -95,8 +109,9 @@ def lib() -> ctypes.CDLL:
         L.msd_accept.argtypes = [P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.msd_kv_commit.argtypes = [P, P, P, P, P, P]
         L.msd_set_profile.argtypes = [P, i32, P, P, i32]
+        L.msd_reuse_select.argtypes = [P, P, P, P, P, P, P, P, P, i32, P, P, P, P, P]
         for f in ("msd_model_create", "msd_verify_block", "msd_early_exit_topk", "msd_accept",
-                  "msd_kv_commit", "msd_set_profile"):
+                  "msd_kv_commit", "msd_reuse_select", "msd_set_profile"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -166,6 +181,33 @@ def accept(handle, block: Block, logits, argmax, sampling: Optional[Sampling], a
 def kv_commit(handle, kv: KVCache, block: Block, acc_len, path, stream=None) -> None:
     _check(lib().msd_kv_commit(handle, ctypes.byref(kv), ctypes.byref(block), _ptr(acc_len),
                                _ptr(path), _stream(stream)))
+
+
+def hyp_tree(parent, tokens) -> "HypTree":
+    """msd_hyp_tree over a host parent list (-1 = root) and a device int32
+    tensor of tokens [batch][n_nodes]; keeps the host array alive."""
+    n = len(parent)
+    P = (ctypes.c_int32 * n)(*parent)
+    t = HypTree(n, ctypes.cast(P, ctypes.POINTER(ctypes.c_int32)), _ptr(tokens))
+    t._keep = (P, tokens)
+    return t
+
+
+def reuse_select(handle, block: Block, acc_len, next_tok, path, tree: HypTree, next_case, next_node,
+                 logits=None, lse=None, ee_ids=None, kappa: int = 0, omega=None, stats=None,
+                 stream=None) -> None:
+    """stats: a device tensor of at least 40 bytes holding msd_reuse_stats."""
+    _check(lib().msd_reuse_select(handle, ctypes.byref(block), _ptr(acc_len), _ptr(next_tok),
+                                  _ptr(path), ctypes.byref(tree), _ptr(logits), _ptr(lse),
+                                  _ptr(ee_ids), int(kappa), _ptr(next_case), _ptr(next_node),
+                                  _ptr(omega), _ptr(stats), _stream(stream)))
+
+
+def read_reuse_stats(stats) -> dict:
+    """Copies a device msd_reuse_stats to the host."""
+    raw = bytes(stats.detach().cpu().contiguous().view(-1).numpy().tobytes()[:ctypes.sizeof(ReuseStats)])
+    r = ReuseStats.from_buffer_copy(raw)
+    return {f: getattr(r, f) for f, _ in ReuseStats._fields_}
 
 
 def set_profile(handle, kclass: int, begin_events, end_events) -> None:

@@ -149,6 +149,82 @@ def test_tiny_wide_early_exit_message(kappa):
     assert gr.ee_ids.shape[-1] == kappa
 
 
+def test_tiny_reuse_selection_and_fallback_statistics():
+    """Sec. 3.1 reuse criterion and next-window selection with the App. C
+    fallback statistics, through the C ABI, against the oracle. Accept
+    outcomes are planted (A cycles through 0..gamma along the chain block,
+    corrections drawn), the hypothesis tree (4 chains of gamma + 1 nodes,
+    shared topology, per-sequence tokens) holds the corrected prefix on two
+    sequences in three; Omega is taken at the root row over the oracle's
+    early-exit ids. Two calls accumulate the statistics."""
+    torch = _torch()
+    import oracle as orc
+    from paper_2510_13161_amd import msd
+    w = synth.WORKLOADS["14b_batch16"].with_model(synth.TINY, ee_layer=1, kappa=4, seed=5, ctx=(64, 96))
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run(commit=False)
+    B, n, V, kap = w.batch, w.n_slots, case.shape.vocab, w.kappa
+    rng = np.random.default_rng(9)
+    acc = np.array([b % n for b in range(B)], np.int32)
+    nxt = rng.integers(0, V, size=B).astype(np.int32)
+    path = np.full((B, n), -1, np.int32)
+    for b in range(B):
+        path[b, :acc[b] + 1] = np.arange(acc[b] + 1)
+    parent = []
+    for r in range(4):
+        for d in range(n):
+            parent.append(-1 if d == 0 else len(parent) - 1)
+    ttok = rng.integers(0, V, size=(B, len(parent))).astype(np.int32)
+    for b in range(B):
+        if b % 3 != 2:
+            pi = [int(t) for t in case.si.tokens[b, 1:acc[b] + 1]] + [int(nxt[b])]
+            ttok[b, (b % 4) * n:(b % 4) * n + len(pi)] = pi
+    ee_ids = np.zeros((B * n, kap), np.int32)
+    want_case, want_node, want_omega = [], [], []
+    weights = synth.host_weights(case.shape, w.seed)
+    for b in range(B):
+        o = H.oracle_sequence(case.shape, w, case.si, b, weights=weights)
+        c_, v_ = orc.reuse_select(parent, ttok[b], case.si.tokens[b, 1:acc[b] + 1], int(nxt[b]))
+        want_case.append(c_)
+        want_node.append(v_)
+        want_omega.append(orc.overlap_mass(o.logits[0], o.ee_ids[0]))
+        ee_ids[b * n] = o.ee_ids[0]
+    assert {orc.NEXT_BRANCH, orc.NEXT_CONTINUE, orc.NEXT_FRESH} <= set(want_case)
+
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    tok_dev = dev(case.si.tokens)
+    blk = msd.make_block(tok_dev, None)
+    tree = msd.hyp_tree(parent, dev(ttok))
+    out_case = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    out_node = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    omega = torch.zeros(B, dtype=torch.float32, device="cuda")
+    stats = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    logits, lse = dev(gr.logits), dev(gr.lse)
+    a_acc, a_nxt, a_path, a_ids = dev(acc), dev(nxt), dev(path), dev(ee_ids)
+    for _ in range(2):
+        msd.reuse_select(case.model.handle, blk, a_acc, a_nxt, a_path, tree, out_case, out_node,
+                         logits, lse, a_ids, kap, omega, stats)
+    torch.cuda.synchronize()
+    assert out_case.cpu().numpy().tolist() == want_case
+    assert out_node.cpu().numpy().tolist() == want_node
+    om = omega.cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(om - np.array(want_omega))) <= 1e-3
+    st = msd.read_reuse_stats(stats)
+    fresh = [c == orc.NEXT_FRESH for c in want_case]
+    assert st["trials"] == 2 * B and st["omega_trials"] == 2 * B
+    assert st["fallbacks"] == 2 * sum(fresh)
+    assert st["fallbacks_tau1"] == 2 * sum(f and a == 0 for f, a in zip(fresh, acc))
+    assert abs(st["omega_sum"] - 2 * sum(want_omega)) <= 2e-3 * B
+    # without Omega inputs: the same selection, statistics without Omega
+    stats.zero_()
+    msd.reuse_select(case.model.handle, blk, a_acc, a_nxt, a_path, tree, out_case, out_node, stats=stats)
+    torch.cuda.synchronize()
+    assert out_case.cpu().numpy().tolist() == want_case
+    st = msd.read_reuse_stats(stats)
+    assert st["trials"] == B and st["omega_trials"] == 0 and st["omega_sum"] == 0.0
+
+
 def test_depth_reduced_14b_chain():
     """14B widths (d 5120, GQA 40/8, FFN 13824, vocab 152064) with 2 layers."""
     _torch()
