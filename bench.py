@@ -159,6 +159,45 @@ def copy_calibration(nbytes: int) -> None:
                       "read_plus_write_gbs": round(8 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
+def after_accept(msd, torch, np, model, blk, acc, nxt, path, logits, lse, ids, w, vocab, reps=50):
+    """The step after acceptance (Sec. 3.1 reuse criterion and next-window
+    selection, App. C statistics) on the last timed step's outputs, timed on
+    its own: the hypothesis tree has kappa chains of n_slots nodes rooted at
+    each sequence's early-exit top-kappa (root row), continuation tokens
+    drawn. Returns its mean launch time, the fallback frequency and the mean
+    overlap mass of the tree it decided on."""
+    B, n, kap = w.batch, w.n_slots, w.kappa
+    parent = [(-1 if d == 0 else r * n + d - 1) for r in range(kap) for d in range(n)]
+    roots = ids.view(B, n, kap)[:, 0, :].cpu().numpy()
+    rng = np.random.default_rng(w.seed + 100)
+    ttok = rng.integers(0, vocab, size=(B, kap * n)).astype(np.int32)
+    for r in range(kap):
+        ttok[:, r * n] = roots[:, r]
+    tree = msd.hyp_tree(parent, torch.from_numpy(ttok).cuda())
+    nc = torch.empty(B, dtype=torch.int32, device="cuda")
+    nn_ = torch.empty(B, dtype=torch.int32, device="cuda")
+    om = torch.empty(B, dtype=torch.float32, device="cuda")
+    stats = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    call = lambda st: msd.reuse_select(model.handle, blk, acc, nxt, path, tree, nc, nn_, logits, lse,
+                                       ids, kap, om, st)
+    call(stats)
+    torch.cuda.synchronize()
+    r = msd.read_reuse_stats(stats)
+    for _ in range(3):
+        call(None)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        call(None)
+    e1.record()
+    torch.cuda.synchronize()
+    return {"reuse_select_us": round(e0.elapsed_time(e1) * 1e3 / reps, 2),
+            "fallback_frequency": r["fallbacks"] / max(r["trials"], 1),
+            "mean_omega": round(r["omega_sum"] / max(r["omega_trials"], 1), 6),
+            "tree": f"{kap} chains x {n} nodes on the early-exit top-{kap}"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -263,6 +302,8 @@ def main():
         print(f"bench.py: device status {status}", file=sys.stderr)
         sys.exit(1)
 
+    post = after_accept(msd, torch, np, model, blk, acc, nxt, path, logits, lse, ids, w, shape.vocab)
+
     roof, t_ee = None, None
     if events:
         dur = [b.elapsed_time(e) for rb, re_ in zip(evb, eve) for b, e in zip(rb, re_)]
@@ -295,6 +336,7 @@ def main():
         "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
         "roofline": roof,
         "ms_to_early_exit": None if t_ee is None else round(t_ee, 4),
+        "after_accept": post,
         "setup_s": round(t_setup, 2),
     }
     if not args.no_cpu_baseline:
