@@ -118,7 +118,6 @@ struct RowsArgs {
   int32_t depth[kMaxSlots];
 };
 hipError_t launch_rows(const RowsArgs& a, hipStream_t s);
-hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // verify attention

@@ -239,21 +239,7 @@ __global__ __launch_bounds__(64) void head_final_kernel(HeadMergeArgs a, int par
   if (a.lse) a.lse[m] = lse;
 }
 
-__global__ void zero_kernel(int32_t* p, int64_t n) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = 0;
-}
-
 }  // namespace
-
-hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  int64_t g = (n + 255) / 256;
-  if (g > 1024) g = 1024;
-  hipLaunchKernelGGL(zero_kernel, dim3((int)g), dim3(256), 0, s, p, n);
-  return hipGetLastError();
-}
 
 hipError_t launch_rows(const RowsArgs& a, hipStream_t s) {
   if (a.d % 64 || a.d > 64 * 256 || a.M < 1 || a.M > 16 * a.MT) return hipErrorInvalidValue;
