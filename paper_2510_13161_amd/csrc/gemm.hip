@@ -32,12 +32,15 @@ namespace {
 // group G of a matrix is a contiguous run of K/32 fragments of 1 KB, fragment
 // ks holding rows 16G..16G+15 x columns 32ks..32ks+31 in MFMA operand order
 // (lane l: row 16G + l%16, columns 32ks + 8(l/16) .. +8).
+// A tile is JT sub-tiles of 16 output columns (JT = 4: 64 columns; JT = 8:
+// 128 columns, for the SwiGLU FFN up projection with one row tile).
 // Returns the lane's pointer into fragment 0 of the group feeding sub-tile j.
+template <int JT>
 __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t, int j, int lane) {
   const size_t run = (size_t)(a.K >> 5) * 512;  // elements per 16-row group
   const uint16_t* base;
   int grp;
-  if (a.map == MAP_QKV) {
+  if (a.map == MAP_QKV) {  // JT = 4: a tile is 32 rotary pairs of one head
     const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
     const int hh = t / tph, gi = t - hh * tph;
     const int c0 = j < 2 ? gi * 32 + 16 * j : half + gi * 32 + 16 * (j - 2);
@@ -51,12 +54,13 @@ __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t,
       hl = hh - a.n_heads;
     }
     grp = (hl * hd + c0) >> 4;
-  } else if (a.map == MAP_GATEUP) {
-    base = j < 2 ? a.w0 : a.w1;
-    grp = 2 * t + (j & 1);
+  } else if (a.map == MAP_GATEUP) {  // JT/2 gate groups, then the same JT/2 of up
+    constexpr int HJ = JT / 2;
+    base = j < HJ ? a.w0 : a.w1;
+    grp = HJ * t + (j % HJ);
   } else {
     base = a.w0;
-    grp = 4 * t + j;
+    grp = JT * t + j;
     const int last = (a.N >> 4) - 1;  // padding columns re-read a valid group; output masked
     if (grp > last) grp = last;
   }
@@ -65,6 +69,7 @@ __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t,
 
 // Logical output column (index into biases and LayerNorm column sums) of
 // value r of sub-tile j in lane group q of tile t.
+template <int JT>
 __device__ __forceinline__ int out_col(const GemmArgs& a, int t, int j, int q, int r) {
   if (a.map == MAP_QKV) {
     const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
@@ -73,10 +78,11 @@ __device__ __forceinline__ int out_col(const GemmArgs& a, int t, int j, int q, i
     return hh * hd + dim;
   }
   if (a.map == MAP_GATEUP) {
-    const int f = 32 * t + 16 * (j & 1) + 4 * q + r;
-    return j < 2 ? f : (a.N >> 1) + f;
+    constexpr int HJ = JT / 2;
+    const int f = 16 * HJ * t + 16 * (j % HJ) + 4 * q + r;
+    return j < HJ ? f : (a.N >> 1) + f;
   }
-  return kTileN * t + 16 * j + 4 * q + r;
+  return 16 * JT * t + 16 * j + 4 * q + r;
 }
 
 // ---------------------------------------------------------------------------
@@ -301,23 +307,27 @@ __device__ void epi_resid(const GemmArgs& a, int t, int mt, const floatx4 (&acc)
   }
 }
 
-__device__ void epi_swiglu(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4], float* scr,
+template <int JT>
+__device__ void epi_swiglu(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[JT], float* scr,
                            float mu, float rs) {
+  constexpr int HJ = JT / 2;  // gate sub-tiles j < HJ pair with up sub-tiles j + HJ
   const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < HJ; ++j) {
     float act[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float g = normed(a, acc[j][r], mu, rs, out_col(a, t, j, q, r));
-      const float u = normed(a, acc[j + 2][r], mu, rs, out_col(a, t, j + 2, q, r));
+      const float g = normed(a, acc[j][r], mu, rs, out_col<JT>(a, t, j, q, r));
+      const float u = normed(a, acc[j + HJ][r], mu, rs, out_col<JT>(a, t, j + HJ, q, r));
       act[r] = silu(g) * u;
     }
     *reinterpret_cast<float4*>(scr + r16 * kScr + 16 * j + 4 * q) =
         make_float4(act[0], act[1], act[2], act[3]);
   }
   wave_lds_sync();
-  scratch_to_image(scr, 0, kUnitGain, a.M, mt, a.MT, t, a.act_img);
+#pragma unroll
+  for (int h = 0; h < HJ / 2; ++h)  // 16 HJ activation columns = HJ / 2 image k-steps
+    scratch_to_image(scr, 32 * h, kUnitGain, a.M, mt, a.MT, (HJ / 2) * t + h, a.act_img);
   wave_lds_sync();
 }
 
@@ -329,7 +339,7 @@ __device__ void epi_relu(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
     float v[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int col = out_col(a, t, j, q, r);
+      const int col = out_col<4>(a, t, j, q, r);
       float y = normed(a, acc[j][r], mu, rs, col);
       if (a.b0) y += bf2f(a.b0[col]);
       v[r] = fmaxf(y, 0.0f);
@@ -397,17 +407,19 @@ __device__ void epi_qkv(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4
 }
 
 // Per row of the tile: logits out, (max, sum exp), top-kappa rank keys.
-__device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4], float mu,
+template <int JT>
+__device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[JT], float mu,
                          float rs) {
+  constexpr int TW = 16 * JT;  // tile width
   const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
   const int m = 16 * mt + r16;
   const bool valid = m < a.M;
-  float v[4][4];
+  float v[JT][4];
   float mx = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int n0 = kTileN * t + 16 * j + 4 * q;
-    const bool cv = kTileN * t + 16 * j < a.N;  // N % 16 == 0: whole groups
+  for (int j = 0; j < JT; ++j) {
+    const int n0 = TW * t + 16 * j + 4 * q;
+    const bool cv = TW * t + 16 * j < a.N;  // N % 16 == 0: whole groups
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       v[j][r] = cv ? normed(a, acc[j][r], mu, rs, cv ? n0 + r : 0) : -INFINITY;
@@ -421,23 +433,23 @@ __device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
   mx = fmaxf(mx, __shfl_xor(mx, 32));
   float se = 0.0f;
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int j = 0; j < JT; ++j)
 #pragma unroll
     for (int r = 0; r < 4; ++r) se += v[j][r] == -INFINITY ? 0.0f : expf(v[j][r] - mx);
   se += __shfl_xor(se, 16);
   se += __shfl_xor(se, 32);
   if (q == 0 && valid) a.tile_ms[(size_t)t * a.M + m] = make_float2(mx, se);
-  uint64_t key[4][4];
+  uint64_t key[JT][4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int j = 0; j < JT; ++j)
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      key[j][r] = v[j][r] == -INFINITY ? 0ull : rank_key(v[j][r], kTileN * t + 16 * j + 4 * q + r);
+      key[j][r] = v[j][r] == -INFINITY ? 0ull : rank_key(v[j][r], TW * t + 16 * j + 4 * q + r);
   uint64_t* top = a.tile_top + ((size_t)t * a.M + (valid ? m : 0)) * a.kappa;
   for (int rr = 0; rr < a.kappa; ++rr) {
     uint64_t best = 0ull;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < JT; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) best = key[j][r] > best ? key[j][r] : best;
     uint64_t o = __shfl_xor(best, 16);
@@ -445,7 +457,7 @@ __device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
     o = __shfl_xor(best, 32);
     best = o > best ? o : best;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < JT; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) key[j][r] = key[j][r] == best ? 0ull : key[j][r];
     if (q == 0 && valid) top[rr] = best;
@@ -454,8 +466,8 @@ __device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
 
 // The epilogue of the finished tile. in1 holds the inputs of a single row
 // tile loaded ahead (MT == 1); otherwise each row tile loads its own here.
-template <int MT, int EPI>
-__device__ __forceinline__ void epilogue(const GemmArgs& a, int t, const floatx4 (&acc)[MT][4],
+template <int MT, int EPI, int JT>
+__device__ __forceinline__ void epilogue(const GemmArgs& a, int t, const floatx4 (&acc)[MT][JT],
                                          float* scr, const EpiIn& in1) {
   for (int mt = 0; mt < MT; ++mt) {
     EpiIn inl;
@@ -466,25 +478,29 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int t, const floatx4
     const EpiIn& in = MT == 1 ? in1 : inl;
     float mu = 0.0f, rs = 1.0f;
     if constexpr (has_norm<EPI>()) norm_finish(a, in, mu, rs);
-    if constexpr (EPI == EPI_RESID) epi_resid(a, t, mt, acc[mt], scr, in);
-    else if constexpr (EPI == EPI_QKV) epi_qkv(a, t, mt, acc[mt], mu, rs, in);
-    else if constexpr (EPI == EPI_SWIGLU) epi_swiglu(a, t, mt, acc[mt], scr, mu, rs);
-    else if constexpr (EPI == EPI_RELU) epi_relu(a, t, mt, acc[mt], scr, mu, rs);
-    else epi_head(a, t, mt, acc[mt], mu, rs);
+    if constexpr (EPI == EPI_SWIGLU) epi_swiglu<JT>(a, t, mt, acc[mt], scr, mu, rs);
+    else if constexpr (EPI == EPI_HEAD) epi_head<JT>(a, t, mt, acc[mt], mu, rs);
+    else if constexpr (JT == 4) {  // the other epilogues run on 64-column tiles only
+      if constexpr (EPI == EPI_RESID) epi_resid(a, t, mt, acc[mt], scr, in);
+      else if constexpr (EPI == EPI_QKV) epi_qkv(a, t, mt, acc[mt], mu, rs, in);
+      else epi_relu(a, t, mt, acc[mt], scr, mu, rs);
+    }
   }
 }
 
-template <int MT>
+template <int MT, int JT>
 struct KStep {
-  bf16x8 w[4];
+  bf16x8 w[JT];
   bf16x8 ah[MT], al[MT];
 };
 
-template <int MT, int NW, int EPI>
+template <int MT, int NW, int EPI, int JT>
 __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
-  constexpr int D = MT == 1 ? (NW == 8 ? 4 : 8) : (MT <= 3 ? 4 : 2);  // k-steps in flight per wave
+  // k-steps in flight per wave
+  constexpr int D = MT == 1 ? (JT == 8 ? 7 : (NW == 8 ? 4 : 8)) : (MT <= 3 ? 4 : 2);
   constexpr int RCH = MT < 3 ? MT : 3;  // row tiles per LDS reduction round
-  __shared__ floatx4 red[NW][RCH * 4][kWave];
+  constexpr int TF = MT * JT * 256;     // floats of one tile's partial
+  __shared__ floatx4 red[NW][RCH * JT][kWave];
   __shared__ __attribute__((aligned(16))) float scr[16 * kScr];
 
   const int lane = threadIdx.x & 63;
@@ -497,9 +513,9 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   const int kb = kb0 + nk * wave / NW, ke = kb0 + nk * (wave + 1) / NW;
   const int n = ke - kb;
 
-  const uint16_t* wp[4];
+  const uint16_t* wp[JT];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) wp[j] = weight_frag(a, t, j, lane);
+  for (int j = 0; j < JT; ++j) wp[j] = weight_frag<JT>(a, t, j, lane);
   const uint16_t* ap = a.a_img + lane * 8;
 
   // one row tile: the epilogue's inputs are loaded ahead (the sequence
@@ -507,16 +523,16 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   EpiIn in1;
   if constexpr (MT == 1 && EPI == EPI_QKV) in1.L = row_len(a, lane & 15);
 
-  floatx4 acc[MT][4];
+  floatx4 acc[MT][JT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < JT; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  KStep<MT> st[D];
-  auto issue = [&](KStep<MT>& x, int k) {
+  KStep<MT, JT> st[D];
+  auto issue = [&](KStep<MT, JT>& x, int k) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) x.w[j] = load16(wp[j] + (size_t)k * 512);
+    for (int j = 0; j < JT; ++j) x.w[j] = load16(wp[j] + (size_t)k * 512);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const uint16_t* p = ap + (size_t)(k * MT + mt) * 1024;
@@ -524,11 +540,11 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
       x.al[mt] = load16(p + 512);
     }
   };
-  auto compute = [&](const KStep<MT>& x) {
+  auto compute = [&](const KStep<MT, JT>& x) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < JT; ++j) {
         acc[mt][j] = mfma16x16x32(x.w[j], x.ah[mt], acc[mt][j]);
         acc[mt][j] = mfma16x16x32(x.w[j], x.al[mt], acc[mt][j]);
       }
@@ -577,17 +593,17 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
       for (int c = 0; c < RCH; ++c)
         if (m0 + c < MT)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) red[wave][c * 4 + j][lane] = acc[m0 + c][j];
+          for (int j = 0; j < JT; ++j) red[wave][c * JT + j][lane] = acc[m0 + c][j];
       __syncthreads();
       if (wave == 0) {
 #pragma unroll
         for (int c = 0; c < RCH; ++c)
           if (m0 + c < MT)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              floatx4 v = red[0][c * 4 + j][lane];
+            for (int j = 0; j < JT; ++j) {
+              floatx4 v = red[0][c * JT + j][lane];
 #pragma unroll
-              for (int w = 1; w < NW; ++w) v += red[w][c * 4 + j][lane];
+              for (int w = 1; w < NW; ++w) v += red[w][c * JT + j][lane];
               acc[m0 + c][j] = v;
             }
       }
@@ -598,12 +614,12 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 
   if (a.splits > 1) {
     // publish this split's tile; the last split to arrive sums all of them
-    float* slot = a.partial + ((size_t)t * a.splits + s) * (MT * 1024) + lane * 4;
+    float* slot = a.partial + ((size_t)t * a.splits + s) * TF + lane * 4;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float* p = slot + (mt * 4 + j) * 256;
+      for (int j = 0; j < JT; ++j) {
+        float* p = slot + (mt * JT + j) * 256;
         store_coherent2(p, acc[mt][j][0], acc[mt][j][1]);
         store_coherent2(p + 2, acc[mt][j][2], acc[mt][j][3]);
       }
@@ -615,20 +631,20 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const float* base = a.partial + (size_t)t * a.splits * (MT * 1024) + lane * 4;
+      for (int j = 0; j < JT; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const float* base = a.partial + (size_t)t * a.splits * TF + lane * 4;
     for (int sp0 = 0; sp0 < a.splits; sp0 += 2) {
       // two splits' tiles in flight, summed in split order
-      floatx4 part[2][MT][4];
+      floatx4 part[2][MT][JT];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int sp = sp0 + u < a.splits ? sp0 + u : sp0;
-        const float* src = base + (size_t)sp * (MT * 1024);
+        const float* src = base + (size_t)sp * TF;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float* p = src + (mt * 4 + j) * 256;
+          for (int j = 0; j < JT; ++j) {
+            const float* p = src + (mt * JT + j) * 256;
             const float2 v01 = load_coherent2(p), v23 = load_coherent2(p + 2);
             part[u][mt][j] = floatx4{v01.x, v01.y, v23.x, v23.y};
           }
@@ -639,27 +655,35 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[mt][j] += part[u][mt][j];
+            for (int j = 0; j < JT; ++j) acc[mt][j] += part[u][mt][j];
     }
     if (lane == 0) counter_reset(&a.counters[t]);
   }
 
-  epilogue<MT, EPI>(a, t, acc, scr, in1);
+  epilogue<MT, EPI, JT>(a, t, acc, scr, in1);
 }
 
-template <int MT, int NW, int EPI>
+template <int MT, int NW, int EPI, int JT>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_kernel<MT, NW, EPI>), dim3(a.n_tiles * a.splits), dim3(64 * NW), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<MT, NW, EPI, JT>), dim3(a.n_tiles * a.splits), dim3(64 * NW), 0, s, a);
   return hipGetLastError();
 }
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
+  if (a.jt == 8) {  // 128-column tiles: the SwiGLU FFN up projection with one row tile
+    if constexpr (EPI == EPI_SWIGLU) {
+      if (a.MT != 1 || a.waves != 2) return hipErrorInvalidValue;
+      return launch_cfg<1, 2, EPI, 8>(a, s);
+    }
+    return hipErrorInvalidValue;
+  }
+  if (a.jt != 4) return hipErrorInvalidValue;
   switch (a.MT) {
-    case 1: return a.waves == 8 ? launch_cfg<1, 8, EPI>(a, s) : launch_cfg<1, 4, EPI>(a, s);
-    case 2: return launch_cfg<2, 4, EPI>(a, s);
-    case 3: return launch_cfg<3, 4, EPI>(a, s);
-    case 9: return launch_cfg<9, 4, EPI>(a, s);
+    case 1: return a.waves == 8 ? launch_cfg<1, 8, EPI, 4>(a, s) : launch_cfg<1, 4, EPI, 4>(a, s);
+    case 2: return launch_cfg<2, 4, EPI, 4>(a, s);
+    case 3: return launch_cfg<3, 4, EPI, 4>(a, s);
+    case 9: return launch_cfg<9, 4, EPI, 4>(a, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -13,7 +13,7 @@ namespace msd {
 enum GemmMap : int32_t {
   MAP_PLAIN = 0,   // output column n <- row n of w0 (rows >= N are padding)
   MAP_QKV = 1,     // 64-wide tiles hold 32 rotary pairs of one q/k/v head
-  MAP_GATEUP = 2,  // 64-wide tiles: 32 rows of w0 (gate) then the same 32 of w1 (up)
+  MAP_GATEUP = 2,  // a tile: 8 jt rows of w0 (gate), then the same 8 jt rows of w1 (up)
 };
 
 enum GemmEpi : int32_t {
@@ -52,12 +52,14 @@ struct GemmArgs {
   const uint16_t* a_img;   // input image [K/32][MT][2][64][8]
   int32_t M, MT, K, N;     // N = logical output columns (padding masked)
   int32_t n_tiles, splits, waves;
+  int32_t jt;              // 16-column sub-tiles per tile: 4 (64 columns), or 8 (128
+                           // columns: EPI_SWIGLU with one row tile and 2 waves)
   int32_t map;
   const uint16_t* w0;
   const uint16_t* w1;
   const uint16_t* w2;
   int32_t n_heads, n_kv_heads, head_dim;  // MAP_QKV
-  float* partial;          // [n_tiles][splits][MT * 1024] (splits > 1)
+  float* partial;          // [n_tiles][splits][MT * jt * 256] (splits > 1)
   int32_t* counters;       // [n_tiles], zero on entry, left zero on exit
   RowNorm norm;
   const uint16_t* b0;      // bias of w0 (q / plain / up)

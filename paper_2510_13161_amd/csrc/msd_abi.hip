@@ -73,19 +73,22 @@ int splits_for(const msd_model* m, int n_tiles, int K, int waves) {
 }
 
 struct GemmShape {
-  int n_tiles, K, splits, waves;
+  int n_tiles, K, splits, waves, jt;
 };
 
 struct Shapes {
   GemmShape qkv, o, up, down, head;
 };
 
-// Waves per workgroup: with one row tile, a GEMM with fewer tiles than the
-// workgroup target runs split-K workgroups of m->waves (8) waves; one with
-// at least that many tiles (FFN up, LM head) runs whole-K workgroups of 4
-// waves, two of which fit a CU. Several row tiles: 4 waves.
+// Tiles and waves per workgroup. With one row tile, a GEMM with fewer
+// 64-column tiles than the workgroup target runs split-K workgroups of
+// m->waves (8) waves, one with more (the LM head) whole-K workgroups of 4
+// waves, and the SwiGLU FFN up projection whole-K 128-column tiles of 2
+// waves (216 workgroups at the 14B shape: at most one per CU). Several row
+// tiles: 64-column tiles, 4 waves.
 Shapes shapes(const msd_model* m, int M) {
   const msd_model_config& c = m->cfg;
+  const bool one = row_tiles(M) == 1;
   Shapes s;
   s.qkv.n_tiles = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim / kTileN;
   s.qkv.K = c.d_model;
@@ -98,9 +101,16 @@ Shapes shapes(const msd_model* m, int M) {
   s.head.n_tiles = (c.vocab + kTileN - 1) / kTileN;
   s.head.K = c.d_model;
   for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
-    g->waves = row_tiles(M) == 1 && g->n_tiles < m->target_wgs ? m->waves : 4;
-    g->splits = splits_for(m, g->n_tiles, g->K, g->waves);
+    g->jt = 4;
+    g->waves = one && g->n_tiles < m->target_wgs ? m->waves : 4;
   }
+  if (one && c.act == MSD_ACT_SWIGLU && c.d_ffn % 64 == 0) {
+    s.up.jt = 8;
+    s.up.n_tiles = c.d_ffn / 64;
+    s.up.waves = 2;
+  }
+  for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head})
+    g->splits = splits_for(m, g->n_tiles, g->K, g->waves);
   return s;
 }
 
@@ -140,7 +150,7 @@ Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacit
   int max_tiles = 0;
   for (const GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
     if (g->splits > 1) {
-      const size_t p = (size_t)g->n_tiles * g->splits * L.MT * 1024 * sizeof(float);
+      const size_t p = (size_t)g->n_tiles * g->splits * L.MT * g->jt * 256 * sizeof(float);
       part = p > part ? p : part;
       max_tiles = g->n_tiles > max_tiles ? g->n_tiles : max_tiles;
     }
@@ -207,6 +217,7 @@ GemmArgs gemm_base(const msd_model* m, const Layout& L, char* ws, int M, const G
   g.n_tiles = sh.n_tiles;
   g.splits = sh.splits;
   g.waves = sh.waves;
+  g.jt = sh.jt;
   g.partial = reinterpret_cast<float*>(ws + L.partial);
   g.counters = reinterpret_cast<int32_t*>(ws + L.counters);
   g.n_heads = m->cfg.n_heads;
