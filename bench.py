@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="time the steps without the per-launch HIP events")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--latency-law", action="store_true",
+                    help="measure the Sec. 3.4 latency law with a synthetic draft on a second stream")
     return ap.parse_args()
 
 
@@ -198,6 +200,197 @@ def after_accept(msd, torch, np, model, blk, acc, nxt, path, logits, lse, ids, w
             "tree": f"{kap} chains x {n} nodes on the early-exit top-{kap}"}
 
 
+def latency_law(args) -> dict:
+    """Sec. 3.4 latency law on one GPU: the 14B chain target step, and a
+    synthetic 0.6B-shaped draft that generates gamma tokens over the kappa
+    early-exit branches (kappa sequences decoded greedily in lockstep, the
+    roots taken from the early-exit top-kappa, each step's argmax feeding the
+    next) on a second stream that waits for the early-exit message's ready
+    event. Measures T_target, T^{1:l_e} (step start to the message), the
+    overlap budget Delta = T_target - T^{1:l_e}, T_draft alone, the overlapped
+    step, the law's prediction T^{1:l_e} + max(Delta, T_draft) and the
+    sequential (vanilla SD) T_target + T_draft. Both models share one GPU's
+    HBM, which two devices would not."""
+    import numpy as np
+    import torch
+    from paper_2510_13161_amd import msd, synth
+    w = synth.WORKLOADS["14b_chain"]
+    shape, dshape = w.model, synth.DRAFT06B
+    si = synth.step_inputs(w)
+    B, n, kap, gam = w.batch, w.n_slots, w.kappa, w.gamma
+    M = B * n
+    cap = int(-(-(int(si.ctx_len.max()) + n + 8) // 64) * 64)
+    model = msd.Model(shape, synth.device_weights(shape, w.seed), max_positions=cap)
+    cache = msd.Cache(shape, B, cap)
+    len0 = torch.from_numpy(si.ctx_len).cuda()
+    cache.len.copy_(len0)
+    synth.device_fill_ctx(shape, w.seed, cache.k, cache.v, cache.len)
+    tokens = torch.from_numpy(si.tokens).cuda()
+    blk = msd.make_block(tokens, None)
+    logits = torch.empty((M, shape.vocab), dtype=torch.float32, device="cuda")
+    argmax = torch.empty(M, dtype=torch.int32, device="cuda")
+    lse = torch.empty(M, dtype=torch.float32, device="cuda")
+    ids = torch.empty((M, kap), dtype=torch.int32, device="cuda")
+    logp = torch.empty((M, kap), dtype=torch.float32, device="cuda")
+    ws = torch.empty(msd.workspace_bytes(model.handle, B, n, kap, cap), dtype=torch.uint8, device="cuda")
+    acc = torch.empty(B, dtype=torch.int32, device="cuda")
+    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+    path = torch.empty((B, n), dtype=torch.int32, device="cuda")
+    ee = msd.EERequest(w.ee_layer, kap, ids.data_ptr(), logp.data_ptr(), None)
+
+    # draft: kappa sequences with the target's context length, one slot per step
+    dcap = int(-(-(int(si.ctx_len.max()) + gam + 8) // 64) * 64)
+    dmodel = msd.Model(dshape, synth.device_weights(dshape, w.seed + 50), max_positions=dcap)
+    dcache = msd.Cache(dshape, kap, dcap)
+    dlen0 = torch.full((kap,), int(si.ctx_len[0]), dtype=torch.int32, device="cuda")
+    dcache.len.copy_(dlen0)
+    synth.device_fill_ctx(dshape, w.seed + 50, dcache.k, dcache.v, dcache.len)
+    dargmax = [torch.empty(kap, dtype=torch.int32, device="cuda") for _ in range(gam)]
+    droots = ids[0].view(kap, 1)  # the early-exit top-kappa of the root row
+    dblks = [msd.make_block(droots if i == 0 else dargmax[i - 1].view(kap, 1), None) for i in range(gam)]
+    dws = torch.empty(msd.workspace_bytes(dmodel.handle, kap, 1, 1, dcap), dtype=torch.uint8, device="cuda")
+    dzero = torch.zeros(kap, dtype=torch.int32, device="cuda")
+    dpath = torch.zeros((kap, 1), dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+
+    def target_step():
+        msd.verify_block(model.handle, cache.c, blk, ee, logits, argmax, lse, ws)
+        msd.accept(model.handle, blk, logits, argmax, None, acc, nxt, path, cache.status)
+        msd.kv_commit(model.handle, cache.c, blk, acc, path)
+        cache.len.copy_(len0)  # every step sees the same context
+
+    def draft_gen():
+        for i in range(gam):
+            msd.verify_block(dmodel.handle, dcache.c, dblks[i], None, None, dargmax[i], None, dws)
+            msd.kv_commit(dmodel.handle, dcache.c, dblks[i], dzero, dpath)
+        dcache.len.copy_(dlen0)
+
+    def timed(fn, steps):
+        for _ in range(2):
+            fn(0)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for k in range(steps):
+            fn(k)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    steps = args.steps
+    ready = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    for e in ready + starts:  # torch only times events it has seen recorded once
+        e.record()
+    torch.cuda.synchronize()
+
+    def target_only(k):
+        target_step()
+
+    def target_with_ready(k):
+        ee.ready = ready[k].cuda_event
+        starts[k].record()
+        target_step()
+
+    t_target = timed(target_only, steps)
+    timed(target_with_ready, steps)
+    t_prefix = float(np.median([a.elapsed_time(b) for a, b in zip(starts, ready)]))
+    t_draft = timed(lambda k: draft_gen(), steps)
+
+    side = torch.cuda.Stream()
+    done = [torch.cuda.Event() for _ in range(steps)]
+
+    def overlapped(k):
+        ee.ready = ready[k].cuda_event
+        starts[k].record()
+        target_step()  # records ready[k] right after the early-exit message
+        side.wait_event(ready[k])
+        with torch.cuda.stream(side):
+            draft_gen()
+            done[k].record()
+        torch.cuda.current_stream().wait_event(done[k])
+
+    def sequential(k):
+        target_step()
+        draft_gen()
+
+    t_overlap = timed(overlapped, steps)
+    t_seq = timed(sequential, steps)
+
+    # the same with the CUs split between two masked streams (224 for the
+    # target, 32 for the draft): two "devices" that still share HBM
+    part = None
+    masked = cu_masked_streams(torch, [(0, 224), (224, 256)])
+    if masked is not None:
+        ts, ds = masked
+
+        def target_masked(k):
+            with torch.cuda.stream(ts):
+                target_step()
+
+        def draft_masked(k):
+            with torch.cuda.stream(ds):
+                draft_gen()
+
+        def overlapped_masked(k):
+            with torch.cuda.stream(ts):
+                ee.ready = ready[k].cuda_event
+                starts[k].record()
+                target_step()
+            ds.wait_event(ready[k])
+            with torch.cuda.stream(ds):
+                draft_gen()
+                done[k].record()
+            ts.wait_event(done[k])
+            torch.cuda.current_stream().wait_stream(ts)
+
+        ee.ready = None
+        pt = timed(target_masked, steps)
+        pd = timed(draft_masked, steps)
+        po = timed(overlapped_masked, steps)
+        pp = float(np.median([a.elapsed_time(b) for a, b in zip(starts, ready)]))
+        part = {"cus": [224, 32], "t_target_ms": round(pt, 4), "t_prefix_ms": round(pp, 4),
+                "t_draft_ms": round(pd, 4), "t_overlap_ms": round(po, 4),
+                "t_law_ms": round(pp + max(pt - pp, pd), 4)}
+    ee.ready = None
+    delta = t_target - t_prefix
+    return {"mode": "latency_law", "workload": w.name,
+            "draft": f"{dshape.n_layers}L d{dshape.d_model} {dshape.n_heads}/{dshape.n_kv_heads}x{dshape.head_dim} "
+                     f"F{dshape.d_ffn} V{dshape.vocab} tied; {kap} branches x {gam} greedy steps",
+            "steps": steps, "t_target_ms": round(t_target, 4), "t_prefix_ms": round(t_prefix, 4),
+            "delta_ms": round(delta, 4), "t_draft_ms": round(t_draft, 4),
+            "t_overlap_ms": round(t_overlap, 4), "t_law_ms": round(t_prefix + max(delta, t_draft), 4),
+            "t_sequential_ms": round(t_seq, 4), "cu_partition": part,
+            "note": "one GPU: the draft and the target suffix share HBM (and, unpartitioned, CUs)"}
+
+
+def cu_masked_streams(torch, ranges):
+    """Streams restricted to CU index ranges [lo, hi) (hipExtStreamCreateWithCUMask),
+    as torch external streams; None if the runtime refuses."""
+    import ctypes
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+    except OSError:
+        return None
+    fn = hip.hipExtStreamCreateWithCUMask
+    fn.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32, ctypes.POINTER(ctypes.c_uint32)]
+    fn.restype = ctypes.c_int
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    out = []
+    for lo, hi in ranges:
+        if hi > n_cu:
+            return None
+        words = (n_cu + 31) // 32
+        mask = (ctypes.c_uint32 * words)()
+        for c in range(lo, hi):
+            mask[c // 32] |= 1 << (c % 32)
+        h = ctypes.c_void_p()
+        if fn(ctypes.byref(h), words, mask) != 0:
+            return None
+        out.append(torch.cuda.ExternalStream(h.value))
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -213,6 +406,9 @@ def main():
         sys.exit(1)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.latency_law:
+        print(json.dumps(latency_law(args)), flush=True)
         return
     w = synth.WORKLOADS[args.workload]
     shape = w.model

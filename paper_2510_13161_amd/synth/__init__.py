@@ -120,6 +120,9 @@ QWEN14B = ModelShape("14b", 48, 5120, 40, 8, 128, 13824, 152064, rope_theta=1.0e
 OPT66B = ModelShape("66b", 64, 9216, 72, 72, 128, 36864, 50272, norm="layer", act="relu",
                     pos="learned", bias=True, tied_head=True, norm_eps=1.0e-5,
                     max_positions=4096)
+# a 0.6B-shaped draft decoder on the 14B target's vocabulary (tied head)
+DRAFT06B = ModelShape("0.6b", 28, 1024, 16, 8, 128, 3072, 152064, tied_head=True,
+                      rope_theta=1.0e6)
 
 WORKLOADS: Dict[str, Workload] = {
     "tiny_chain": Workload("tiny_chain", TINY, 1, (128, 128), "chain", 4, ee_layer=1, kappa=4,
