@@ -8,7 +8,8 @@
 // one 64-key block. A wave loads its block's K as MFMA operands and V rows
 // into its own LDS (16-byte writes, read back as P V operands with the
 // gfx950 transposing LDS read), then
-//   S^T[key][query] = K Q^T        MFMA 16x16x32; Q (fp32) as bf16 hi + lo;
+//   S^T[key][query] = K Q^T        MFMA 16x16x32; Q as bf16 hi + lo operands
+//                                  that the QKV epilogue wrote in MFMA order;
 //   block softmax statistics       one query per lane column: 2 shuffles;
 //   O[query][d] += P V             P stays in registers as the MFMA operand.
 // Scores are kept in base-2 units (the 1/sqrt(hd) scale times log2 e), so
@@ -66,7 +67,6 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   constexpr int KPI = 512 / HD;  // keys per V chunk iteration
   __shared__ __attribute__((aligned(16))) unsigned char region_all[4][Lds::kRegion];
   __shared__ float ml_sh[4][16][2];
-  __shared__ __attribute__((aligned(16))) uint16_t qs[KSTEPS * 2 * 512];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
@@ -92,8 +92,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int key_hi = min(T, k0 + 64);  // this wave's keys [k0, key_hi), maybe none
 
   // K fragments and V rows first (rows past the last key clamped to a valid
-  // row; their scores are masked), so that their round trip overlaps the
-  // query staging below
+  // row; their scores are masked)
   u32x4 vraw[VIT];
 #pragma unroll
   for (int it = 0; it < VIT; ++it) {
@@ -109,29 +108,23 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int kk = 0; kk < KSTEPS; ++kk) kf[j][kk] = load16(kbase + (size_t)pos * HD + kk * 32 + g * 8);
   }
 
-  // the query tile as split-bf16 MFMA operands, shared by the 4 waves
-  // through LDS: qs[k-step][hi / lo][lane][8]
-  for (int x = tid; x < KSTEPS * 64; x += blockDim.x) {
-    const int kk = x >> 6, l = x & 63;
-    const int qv = qt * 16 + (l & 15);
-    const bool qok = qv < Qn;
-    const int gq = qok ? qv / ns : 0;
-    const int slot = qok ? qv - gq * ns : 0;
-    const float* qp = a.q + ((size_t)(b * ns + slot) * a.n_heads + kvh * G + gq) * HD + kk * 32 + (l >> 4) * 8;
-    const u32x4 r0 = *reinterpret_cast<const u32x4*>(qp);
-    const u32x4 r1 = *reinterpret_cast<const u32x4*>(qp + 4);
-    const float qm = qok ? 1.0f : 0.0f;
-    float v[8];
+  // the query tile's split-bf16 operands, as the QKV epilogue wrote them,
+  // straight into registers; padding queries (past G * n_slots) are zeroed by
+  // selection, so whatever the workspace holds there never reaches a score
+  const uint16_t* qtile = a.q_img + (((size_t)b * a.n_kv_heads + kvh) * QT + qt) * (size_t)KSTEPS * 1024 + lane * 8;
+  const bool qok = qt * 16 + r16 < Qn;
+  bf16x8 qh[KSTEPS], ql[KSTEPS];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[i] = __uint_as_float(r0[i]) * qm;
-      v[4 + i] = __uint_as_float(r1[i]) * qm;
+  for (int kk = 0; kk < KSTEPS; ++kk) {
+    u32x4 h = *reinterpret_cast<const u32x4*>(qtile + (size_t)kk * 1024);
+    u32x4 l = *reinterpret_cast<const u32x4*>(qtile + (size_t)kk * 1024 + 512);
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      h[x] = qok ? h[x] : 0u;
+      l[x] = qok ? l[x] : 0u;
     }
-    u32x4 hw, lw;
-    split8_words(v, hw, lw);
-    uint16_t* dst = qs + (size_t)(kk * 2) * 512 + l * 8;
-    *reinterpret_cast<u32x4*>(dst) = hw;
-    *reinterpret_cast<u32x4*>(dst + 512) = lw;
+    qh[kk] = __builtin_bit_cast(bf16x8, h);
+    ql[kk] = __builtin_bit_cast(bf16x8, l);
   }
   // V rows into the wave's LDS as they are (16-byte writes), read back as
   // P V operands: lane l takes dim 16 ds + l%16 of keys 32 kb + 4 g + e and
@@ -141,7 +134,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int key = it * KPI + lane / (HD / 8);
     *reinterpret_cast<u32x4*>(vs + key * Lds::kVS + (lane % (HD / 8)) * 8) = vraw[it];
   }
-  __syncthreads();
+  wave_lds_sync();
   // transposing LDS reads: in each 16-lane group, lane i receives element
   // i % 4 of the 8-byte chunks addressed by lanes i / 4 + 4 k (k < 4), so
   // lane s of group g points at key 32 kb + 4 g + s / 4 (+ 16), dims
@@ -165,9 +158,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     sc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk) {
-      const uint16_t* qf = qs + (size_t)(kk * 2) * 512 + lane * 8;
-      sc[j] = mfma16x16x32(kf[j][kk], load16(qf), sc[j]);
-      sc[j] = mfma16x16x32(kf[j][kk], load16(qf + 512), sc[j]);
+      sc[j] = mfma16x16x32(kf[j][kk], qh[kk], sc[j]);
+      sc[j] = mfma16x16x32(kf[j][kk], ql[kk], sc[j]);
     }
   }
   // lane holds S^T[key 16j + 4g + r][query r16]: scale (base 2), mask, softmax

@@ -213,14 +213,6 @@ __device__ __forceinline__ float normed(const GemmArgs& a, float acc, float mu, 
   return a.norm.kind == 1 ? rs * acc : acc;
 }
 
-// make this wave's LDS writes visible to its own later LDS reads
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 constexpr int kScr = kTileN + 4;  // scratch row stride (floats)
 
 // Image of 32 consecutive columns [c0, c0 + 32) of a 16-row tile held in
@@ -392,9 +384,25 @@ __device__ void epi_qkv(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4
       }
     }
     if (which == 0) {
-      float* qp = a.q_out + ((size_t)m * H + hloc) * hd;
-      *reinterpret_cast<float4*>(qp + dlo) = make_float4(lo[0], lo[1], lo[2], lo[3]);
-      *reinterpret_cast<float4*>(qp + dhi) = make_float4(hi[0], hi[1], hi[2], hi[3]);
+      // the attention's operand image of this query row: head hloc is query
+      // gq of kv head kvh; four consecutive dims sit in one lane's 8
+      const int G = H / Hk, kvh = hloc / G, gq = hloc - kvh * G;
+      const int qv = gq * a.n_slots + slot, qt = qv >> 4, ql = qv & 15;
+      uint16_t* tile = a.q_img + (((size_t)b * Hk + kvh) * a.q_tiles + qt) * (size_t)(hd / 32) * 1024;
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int d0 = h2 == 0 ? dlo : dhi;
+        const float* v = h2 == 0 ? lo : hi;
+        uint16_t* dst = tile + (size_t)(d0 >> 5) * 1024 + (ql + 16 * ((d0 & 31) >> 3)) * 8 + (d0 & 7);
+        u32x2 hw, lw;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          hw[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
+          lw[e] = pack_bf16x2(v[2 * e] - bf_lo(hw[e]), v[2 * e + 1] - bf_hi(hw[e]));
+        }
+        *reinterpret_cast<u32x2*>(dst) = hw;
+        *reinterpret_cast<u32x2*>(dst + 512) = lw;
+      }
     } else {
       uint16_t* cache = which == 1 ? a.k_cache : a.v_cache;
       uint16_t* row = cache + (((size_t)b * Hk + hloc) * a.capacity + L + slot) * hd;

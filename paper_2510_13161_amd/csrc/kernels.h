@@ -70,7 +70,11 @@ struct GemmArgs {
   float2* stats_out;       // [n_tiles][M] (mean, M2) of the updated rows
   ImageOut img_out[2];     // images of the updated x (K = N)
   // EPI_QKV
-  float* q_out;            // [M][H * hd]
+  uint16_t* q_img;         // q as the attention's split-bf16 operand image:
+                           // [batch][Hkv][q_tiles][hd/32][hi|lo][64 lanes][8]; lane l
+                           // of tile qt: query qt*16 + l%16 (= gq*n_slots + slot of
+                           // head kvh*G + gq), dims 32 kk + 8 (l/16) .. +8
+  int32_t q_tiles;         // 16-query tiles per kv head: ceil(G * n_slots / 16)
   uint16_t* k_cache;       // this layer's [batch_cap][Hkv][cap][hd]
   uint16_t* v_cache;
   const int32_t* len;      // committed lengths [batch]
@@ -129,7 +133,7 @@ constexpr int kMaxCapacity = 32768;   // cache positions
 constexpr int kAttnChunk = 256;       // keys per workgroup (4 waves x 64)
 
 struct AttnArgs {
-  const float* q;           // fp32 [M][H][hd] (rotated)
+  const uint16_t* q_img;    // rotated q as operand image (GemmArgs::q_img), padding rows unset
   const uint16_t* k_cache;  // this layer [batch_cap][Hkv][cap][hd]
   const uint16_t* v_cache;
   const int32_t* len;

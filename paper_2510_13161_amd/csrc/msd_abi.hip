@@ -140,7 +140,10 @@ Layout layout(const msd_model* m, int batch, int n_slots, int kappa, int capacit
   };
   L.x = take((size_t)M * c.d_model * sizeof(float));
   L.stats = take((size_t)(c.d_model / kTileN) * M * sizeof(float2));
-  L.q = take((size_t)M * qd * sizeof(float));
+  // q as the attention's operand image: per sequence and kv head, the GQA
+  // group's queries in 16-row tiles, hi + lo bf16 parts
+  const int q_tiles = ((c.n_heads / c.n_kv_heads) * n_slots + 15) / 16;
+  L.q = take((size_t)batch * c.n_kv_heads * q_tiles * (c.head_dim / 32) * 1024 * sizeof(uint16_t));
   L.img_x = take(img_bytes(c.d_model, L.MT));
   L.img_h = take(img_bytes(c.d_model, L.MT));
   L.img_f = take(img_bytes(c.d_model, L.MT));
@@ -522,7 +525,8 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
   const int d = c.d_model, qd = c.n_heads * c.head_dim;
   float* x = reinterpret_cast<float*>(w + L.x);
   float2* stats = reinterpret_cast<float2*>(w + L.stats);
-  float* q = reinterpret_cast<float*>(w + L.q);
+  uint16_t* q_img = reinterpret_cast<uint16_t*>(w + L.q);
+  const int q_tiles = ((c.n_heads / c.n_kv_heads) * blk->n_slots + 15) / 16;
   uint16_t* img_x = reinterpret_cast<uint16_t*>(w + L.img_x);
   uint16_t* img_h = reinterpret_cast<uint16_t*>(w + L.img_h);
   uint16_t* img_f = reinterpret_cast<uint16_t*>(w + L.img_f);
@@ -570,7 +574,8 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
     g.b0 = LT(m, l, MSD_L_BQ);
     g.b1 = LT(m, l, MSD_L_BK);
     g.b2 = LT(m, l, MSD_L_BV);
-    g.q_out = q;
+    g.q_img = q_img;
+    g.q_tiles = q_tiles;
     g.k_cache = kc;
     g.v_cache = vc;
     g.len = kv->len;
@@ -585,7 +590,7 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
     MSD_HIP(prof_mark(m, MSD_K_QKV, l, false, stream));
 
     AttnArgs aa{};
-    aa.q = q;
+    aa.q_img = q_img;
     aa.k_cache = kc;
     aa.v_cache = vc;
     aa.len = kv->len;
