@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmsd.so")
 MSD_OK = 0
 MSD_ERR_INVALID_ARG, MSD_ERR_SHAPE, MSD_ERR_CAPACITY = -1, -2, -3
 MSD_ERR_UNSUPPORTED, MSD_ERR_WORKSPACE, MSD_ERR_HIP = -4, -5, -6
-MSD_DEV_CAPACITY, MSD_DEV_CANDIDATE = 1, 2
+MSD_DEV_CAPACITY, MSD_DEV_CANDIDATE, MSD_DEV_TOKEN = 1, 2, 4
 MSD_NORM_RMS, MSD_NORM_LAYER = 0, 1
 MSD_ACT_SWIGLU, MSD_ACT_RELU = 0, 1
 MSD_POS_ROPE, MSD_POS_LEARNED = 0, 1

@@ -93,8 +93,11 @@ class GpuCase:
             vr = np.empty_like(kr)
             for b in range(B):
                 L = int(si.ctx_len[b])
-                kr[b] = self.cache.k[l, b, :, L:L + n].view(torch.int16).cpu().numpy().view(np.uint16)
-                vr[b] = self.cache.v[l, b, :, L:L + n].view(torch.int16).cpu().numpy().view(np.uint16)
+                hi = min(L + n, self.capacity)  # a block that overflows the cache has no rows there
+                kr[b] = 0
+                vr[b] = 0
+                kr[b, :, :hi - L] = self.cache.k[l, b, :, L:hi].view(torch.int16).cpu().numpy().view(np.uint16)
+                vr[b, :, :hi - L] = self.cache.v[l, b, :, L:hi].view(torch.int16).cpu().numpy().view(np.uint16)
             k_rows.append(kr)
             v_rows.append(vr)
         acc = torch.empty(B, dtype=torch.int32, device=dev)

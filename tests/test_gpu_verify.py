@@ -225,6 +225,63 @@ def test_tiny_reuse_selection_and_fallback_statistics():
     assert st["trials"] == B and st["omega_trials"] == 0 and st["omega_sum"] == 0.0
 
 
+@pytest.mark.parametrize("name,ctx,topo,gamma,branches", [
+    ("root_only", 96, "chain", 0, 1),        # n_slots = 1: no draft token, A = 0
+    ("empty_context", 0, "chain", 4, 1),     # L = 0: the block attends only to itself
+    ("one_chunk", 251, "chain", 4, 1),       # L + n_slots = 256 keys: one attention chunk
+    ("chunk_plus_one", 252, "chain", 4, 1),  # 257 keys: a second chunk holding one key
+    ("max_tree", 40, "tree", 9, 7),          # 1 + 7 x 9 = 64 slots (ancestor bit 63, M = 64)
+])
+def test_tiny_degenerate_blocks(name, ctx, topo, gamma, branches):
+    """The method's degenerate and boundary blocks, element by element against the oracle."""
+    _torch()
+    w = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, ctx=(ctx, ctx), topology=topo, gamma=gamma,
+                                                 branches=branches, ee_layer=1, kappa=4, seed=21)
+    assert w.n_slots <= 64
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    rep = _compare(case, gr, {0: o})
+    print(name, rep)
+
+
+def test_tiny_ragged_batch():
+    """Sequences of different context lengths in one block batch (1 to 2 chunks)."""
+    _torch()
+    w = synth.WORKLOADS["14b_batch16"].with_model(synth.TINY, batch=5, ctx=(1, 400), ee_layer=1, kappa=4,
+                                                  seed=23)
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run()
+    weights = synth.host_weights(case.shape, w.seed)
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b, weights=weights) for b in range(w.batch)}
+    assert len(set(case.si.ctx_len.tolist())) > 1
+    print("ragged:", _compare(case, gr, seqs))
+
+
+def test_device_errors_are_flagged():
+    """Device-detected errors set the caller's status word: a block that does
+    not fit the cache (len + n_slots > capacity) and a token outside the
+    vocabulary; the cache rows past len are left as they were."""
+    torch = _torch()
+    from paper_2510_13161_amd import msd
+    w = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, ctx=(62, 62), seed=25)
+    case = H.GpuCase(w, capacity=64)     # 62 + 5 slots > 64
+    case.reset_len()
+    k_before = case.cache.k.clone()
+    gr = case.run(commit=False)
+    assert gr.status & msd.MSD_DEV_CAPACITY
+    assert torch.equal(case.cache.k, k_before)
+    w2 = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, seed=26)
+    si = synth.step_inputs(w2)
+    si.tokens[0, 2] = w2.model.vocab + 5
+    case2 = H.GpuCase(w2, inputs=si)
+    case2.reset_len()
+    gr2 = case2.run(commit=False)
+    assert gr2.status & msd.MSD_DEV_TOKEN
+
+
 def test_depth_reduced_14b_chain():
     """14B widths (d 5120, GQA 40/8, FFN 13824, vocab 152064) with 2 layers."""
     _torch()
