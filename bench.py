@@ -49,9 +49,11 @@ def parse():
 def step_bytes(shape, w, ctx_mean: float) -> dict:
     """Algorithmic HBM bytes of one step: every weight once, the LM head twice
     (early exit + final), cached K/V read once, block K/V written, logits out."""
+    import re
+    import numpy as np
     from paper_2510_13161_amd import synth
     specs = synth.tensor_specs(shape)
-    layer_w = sum(2 * int(__import__("numpy").prod(s.shape)) for s in specs if s.name.startswith("l"))
+    layer_w = sum(2 * int(np.prod(s.shape)) for s in specs if re.match(r"l\d+\.", s.name))
     head = 2 * shape.vocab * shape.d_model
     M = w.rows
     kv_read = shape.n_layers * 2 * shape.n_kv_heads * shape.head_dim * 2 * (ctx_mean + w.n_slots) * w.batch
