@@ -166,17 +166,19 @@ def copy_calibration(nbytes: int) -> None:
 def after_accept(msd, torch, np, model, blk, acc, nxt, path, logits, lse, ids, w, vocab, reps=50):
     """The step after acceptance (Sec. 3.1 reuse criterion and next-window
     selection, App. C statistics) on the last timed step's outputs, timed on
-    its own: the hypothesis tree has kappa chains of n_slots nodes rooted at
-    each sequence's early-exit top-kappa (root row), continuation tokens
-    drawn. Returns its mean launch time, the fallback frequency and the mean
-    overlap mass of the tree it decided on."""
+    its own: the hypothesis tree has kappa chains of gamma + 1 nodes (the
+    window's depth; fewer if kappa chains would exceed the tree's node limit)
+    rooted at each sequence's early-exit top-kappa (root row), continuation
+    tokens drawn. Returns its mean launch time, the fallback frequency and the
+    mean overlap mass of the tree it decided on."""
     B, n, kap = w.batch, w.n_slots, w.kappa
-    parent = [(-1 if d == 0 else r * n + d - 1) for r in range(kap) for d in range(n)]
+    nc_len = min(w.gamma + 1, msd.MSD_MAX_TREE_NODES // kap)
+    parent = [(-1 if d == 0 else r * nc_len + d - 1) for r in range(kap) for d in range(nc_len)]
     roots = ids.view(B, n, kap)[:, 0, :].cpu().numpy()
     rng = np.random.default_rng(w.seed + 100)
-    ttok = rng.integers(0, vocab, size=(B, kap * n)).astype(np.int32)
+    ttok = rng.integers(0, vocab, size=(B, kap * nc_len)).astype(np.int32)
     for r in range(kap):
-        ttok[:, r * n] = roots[:, r]
+        ttok[:, r * nc_len] = roots[:, r]
     tree = msd.hyp_tree(parent, torch.from_numpy(ttok).cuda())
     nc = torch.empty(B, dtype=torch.int32, device="cuda")
     nn_ = torch.empty(B, dtype=torch.int32, device="cuda")
@@ -199,7 +201,7 @@ def after_accept(msd, torch, np, model, blk, acc, nxt, path, logits, lse, ids, w
     return {"reuse_select_us": round(e0.elapsed_time(e1) * 1e3 / reps, 2),
             "fallback_frequency": r["fallbacks"] / max(r["trials"], 1),
             "mean_omega": round(r["omega_sum"] / max(r["omega_trials"], 1), 6),
-            "tree": f"{kap} chains x {n} nodes on the early-exit top-{kap}"}
+            "tree": f"{kap} chains x {nc_len} nodes on the early-exit top-{kap}"}
 
 
 def latency_law(args) -> dict:
@@ -356,13 +358,60 @@ def latency_law(args) -> dict:
                 "t_law_ms": round(pp + max(pt - pp, pd), 4)}
     ee.ready = None
     delta = t_target - t_prefix
+
+    # Speculative Streaming draft (Sec. 3.3, timing only): one draft forward
+    # carries, for each of the kappa branches, the main stream (the branch
+    # root) and gamma lookahead streams, stream j attending to the verified
+    # prefix and to streams 1..j: a chain of gamma + 1 slots per branch, i.e.
+    # a batch-kappa chain block, with the shared LM head over every stream.
+    # Trained stream embeddings would replace the token embeddings of the
+    # lookahead slots at the same cost. J = ceil(gamma / eta) such steps give
+    # gamma tokens when a step emits eta on average.
+    ss_n = gam + 1
+    ss_tok = torch.cat([droots, droots.expand(kap, gam)], dim=1).contiguous()
+    ss_blk = msd.make_block(ss_tok, None)
+    ss_arg = torch.empty(kap * ss_n, dtype=torch.int32, device="cuda")
+    ss_ws = torch.empty(msd.workspace_bytes(dmodel.handle, kap, ss_n, 1, dcap), dtype=torch.uint8, device="cuda")
+    ss_path = torch.zeros((kap, ss_n), dtype=torch.int32, device="cuda")
+
+    def ss_step():
+        msd.verify_block(dmodel.handle, dcache.c, ss_blk, None, None, ss_arg, None, ss_ws)
+        msd.kv_commit(dmodel.handle, dcache.c, ss_blk, dzero, ss_path)
+        dcache.len.copy_(dlen0)
+
+    t_ss = timed(lambda k: ss_step(), steps)
+    ss_laws = []
+    for eta in (1, 2, 4, gam):
+        J = -(-gam // eta)
+
+        def ss_gen(J=J):
+            for _ in range(J):
+                ss_step()
+
+        def ss_overlapped(k, J=J):
+            ee.ready = ready[k].cuda_event
+            starts[k].record()
+            target_step()
+            side.wait_event(ready[k])
+            with torch.cuda.stream(side):
+                ss_gen()
+                done[k].record()
+            torch.cuda.current_stream().wait_event(done[k])
+
+        t_ov = timed(ss_overlapped, steps)
+        ss_laws.append({"eta": eta, "J": J, "t_draft_ms": round(J * t_ss, 4),
+                        "t_law_ms": round(t_prefix + max(delta, J * t_ss), 4),
+                        "t_overlap_ms": round(t_ov, 4)})
+    ee.ready = None
+    ss = {"rows": kap * ss_n, "block": f"{kap} branches x (main + {gam} lookahead streams)",
+          "t_step_ms": round(t_ss, 4), "by_tokens_per_step": ss_laws}
     return {"mode": "latency_law", "workload": w.name,
             "draft": f"{dshape.n_layers}L d{dshape.d_model} {dshape.n_heads}/{dshape.n_kv_heads}x{dshape.head_dim} "
                      f"F{dshape.d_ffn} V{dshape.vocab} tied; {kap} branches x {gam} greedy steps",
             "steps": steps, "t_target_ms": round(t_target, 4), "t_prefix_ms": round(t_prefix, 4),
             "delta_ms": round(delta, 4), "t_draft_ms": round(t_draft, 4),
             "t_overlap_ms": round(t_overlap, 4), "t_law_ms": round(t_prefix + max(delta, t_draft), 4),
-            "t_sequential_ms": round(t_seq, 4), "cu_partition": part,
+            "t_sequential_ms": round(t_seq, 4), "cu_partition": part, "ss_draft": ss,
             "note": "one GPU: the draft and the target suffix share HBM (and, unpartitioned, CUs)"}
 
 

@@ -679,10 +679,15 @@ hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  if (a.jt == 8) {  // 128-column tiles: the SwiGLU FFN up projection with one row tile
+  if (a.jt == 8) {  // 128-column tiles: the SwiGLU FFN up projection, up to 3 row tiles
     if constexpr (EPI == EPI_SWIGLU) {
-      if (a.MT != 1 || a.waves != 2) return hipErrorInvalidValue;
-      return launch_cfg<1, 2, EPI, 8>(a, s);
+      if (a.waves != 2) return hipErrorInvalidValue;
+      switch (a.MT) {
+        case 1: return launch_cfg<1, 2, EPI, 8>(a, s);
+        case 2: return launch_cfg<2, 2, EPI, 8>(a, s);
+        case 3: return launch_cfg<3, 2, EPI, 8>(a, s);
+        default: return hipErrorInvalidValue;
+      }
     }
     return hipErrorInvalidValue;
   }

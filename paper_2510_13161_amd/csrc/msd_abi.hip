@@ -83,9 +83,9 @@ struct Shapes {
 // Tiles and waves per workgroup. With one row tile, a GEMM with fewer
 // 64-column tiles than the workgroup target runs split-K workgroups of
 // m->waves (8) waves, one with more (the LM head) whole-K workgroups of 4
-// waves, and the SwiGLU FFN up projection whole-K 128-column tiles of 2
-// waves (216 workgroups at the 14B shape: at most one per CU). Several row
-// tiles: 64-column tiles, 4 waves.
+// waves. Several row tiles: 64-column tiles, 4 waves. The SwiGLU FFN up
+// projection with up to 3 row tiles: whole-K 128-column tiles of 2 waves
+// (216 workgroups at the 14B shape, one dispatch round: at most one per CU).
 Shapes shapes(const msd_model* m, int M) {
   const msd_model_config& c = m->cfg;
   const bool one = row_tiles(M) == 1;
@@ -104,7 +104,7 @@ Shapes shapes(const msd_model* m, int M) {
     g->jt = 4;
     g->waves = one && g->n_tiles < m->target_wgs ? m->waves : 4;
   }
-  if (one && c.act == MSD_ACT_SWIGLU && c.d_ffn % 64 == 0) {
+  if (row_tiles(M) <= 3 && c.act == MSD_ACT_SWIGLU && c.d_ffn % 64 == 0) {
     s.up.jt = 8;
     s.up.n_tiles = c.d_ffn / 64;
     s.up.waves = 2;
