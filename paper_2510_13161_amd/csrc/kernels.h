@@ -145,6 +145,8 @@ struct AttnArgs {
   float* part_ml;           // [batch][Hkv][chunks][Qn][2] (max of score * log2 e, sum exp2)
   int32_t batch, n_heads, n_kv_heads, capacity, n_slots;
   int32_t max_chunks;       // 256-key chunks of the longest sequence
+  int32_t q_per_wg;         // query tiles a workgroup takes in turn (its K and V
+                            // operands loaded once for all of them)
   float scale;
   Topo topo;
 };

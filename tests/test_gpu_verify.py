@@ -293,6 +293,23 @@ def test_depth_reduced_14b_chain():
     print("14b L2 chain:", rep)
 
 
+def test_attention_query_tile_groups():
+    """Attention workgroups that take several query tiles in turn: GQA 16/4
+    with head_dim 64 and a 25-slot tree (7 query tiles of the 100 queries per
+    kv head), 4 sequences with contexts up to 4800 (19 key chunks merged
+    across workgroups): 19 x 4 x 4 x 7 workgroups exceed the grouping
+    threshold, so the tiles go 2 per workgroup with a ragged last group."""
+    _torch()
+    shape = synth.ModelShape("gqa64", 2, 1024, 16, 4, 64, 2048, 4096, rope_theta=1.0e4)
+    w = synth.Workload("gqa64_tree", shape, 4, (4600, 4800), "tree", 6, branches=4, ee_layer=1,
+                       kappa=4, seed=11)
+    case = H.GpuCase(w)
+    gr = case.run()
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b) for b in (0, 3)}
+    rep = _compare(case, gr, seqs)
+    print("query tile groups:", rep)
+
+
 def test_depth_reduced_66b_tree():
     """66B widths (MHA 72 heads, LayerNorm, learned positions, ReLU, biases, tied head), 2 layers."""
     _torch()
