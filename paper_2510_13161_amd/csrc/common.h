@@ -57,10 +57,13 @@ __device__ __forceinline__ bf16x8 round_vals(const float (&v)[8]) {
 }
 
 // LDS-only workgroup barrier: waits for this wave's LDS traffic, not for its
-// outstanding global loads (a full __syncthreads would drain those too).
+// outstanding global loads (a full __syncthreads would drain those too); the
+// empty asm statements keep the compiler from moving memory accesses across.
 __device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0), vmcnt/expcnt left open
   __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // 16-byte loads. Weights are streamed once per pass: non-temporal.

@@ -477,6 +477,9 @@ __device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
 template <int MT, int EPI, int JT>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, int t, const floatx4 (&acc)[MT][JT],
                                          float* scr, const EpiIn& in1) {
+  // unrolled: a runtime row-tile index into acc would make the compiler keep
+  // the whole accumulator array in scratch memory, k-loop included
+#pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     EpiIn inl;
     if constexpr (MT > 1) {

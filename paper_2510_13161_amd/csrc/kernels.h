@@ -53,7 +53,7 @@ struct GemmArgs {
   int32_t M, MT, K, N;     // N = logical output columns (padding masked)
   int32_t n_tiles, splits, waves;
   int32_t jt;              // 16-column sub-tiles per tile: 4 (64 columns), or 8 (128
-                           // columns: EPI_SWIGLU with one row tile and 2 waves)
+                           // columns: EPI_SWIGLU with up to 3 row tiles and 2 waves)
   int32_t map;
   const uint16_t* w0;
   const uint16_t* w1;
