@@ -162,6 +162,9 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 
   const float scale2 = a.scale * kLog2e;
   const size_t pbase = ((size_t)b * a.n_kv_heads + kvh) * a.max_chunks;
+  // this (sequence, kv head)'s chunk outputs: [max_chunks][Qn][HD] floats
+  const __amdgpu_buffer_rsrc_t pco =
+      coherent_region(a.part_o + pbase * Qn * HD, (uint32_t)((size_t)a.max_chunks * Qn * HD * 4));
   for (int qt = qt0; qt < qt1; ++qt) {
     if (MULTI && qt != qt0) load_q(qt);
     const int qv = qt * 16 + r16;
@@ -269,9 +272,9 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
         write_out<HD>(a, b, kvh, qg, c8, o8);
       } else {
         const size_t pidx = (pbase + c) * Qn + qg;
-        float* po = a.part_o + pidx * HD + 8 * c8;
-#pragma unroll
-        for (int e = 0; e < 8; e += 2) store_coherent2(po + e, o8[e], o8[e + 1]);
+        const uint32_t off = (uint32_t)((((size_t)c * Qn + qg) * HD + 8 * c8) * 4);
+        store_coherent4(pco, off, floatx4{o8[0], o8[1], o8[2], o8[3]});
+        store_coherent4(pco, off + 16, floatx4{o8[4], o8[5], o8[6], o8[7]});
         if (c8 == 0) store_coherent2(a.part_ml + 2 * pidx, M, S);
       }
     }
@@ -298,12 +301,12 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
           const int cc = c0 + u < nch ? c0 + u : c0;
           const size_t pidx = (pbase + cc) * Qn + qg;
           ml[u] = load_coherent2(a.part_ml + 2 * pidx);
-          const float* po = a.part_o + pidx * HD + 8 * c8;
+          const uint32_t off = (uint32_t)((((size_t)cc * Qn + qg) * HD + 8 * c8) * 4);
+          const floatx4 v0 = load_coherent4(pco, off), v1 = load_coherent4(pco, off + 16);
 #pragma unroll
-          for (int e = 0; e < 8; e += 2) {
-            const float2 t2 = load_coherent2(po + e);
-            v[u][e] = t2.x;
-            v[u][e + 1] = t2.y;
+          for (int e = 0; e < 4; ++e) {
+            v[u][e] = v0[e];
+            v[u][e + 4] = v1[e];
           }
         }
 #pragma unroll

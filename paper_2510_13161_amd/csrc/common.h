@@ -201,7 +201,12 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__device__ __forceinline__ void drain_stores() { __builtin_amdgcn_s_waitcnt(0); }
+// all of this wave's memory accesses complete; the compiler moves none across
+__device__ __forceinline__ void drain_stores() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0);
+  asm volatile("" ::: "memory");
+}
 __device__ __forceinline__ int counter_add(int32_t* c, int v) {
   return __hip_atomic_fetch_add(c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -218,6 +223,22 @@ __device__ __forceinline__ float2 load_coherent2(const float* p) {
   const uint64_t v = __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<float*>(p)),
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+}
+
+// 16-byte variants: buffer loads and stores with the same L2-coherent (sc1)
+// policy, through a resource that covers the hand-off region. A wave's
+// 16-byte-per-lane access to a contiguous 1 KB then moves whole cache lines;
+// the 8-byte accesses above write each line in two masked halves, which the
+// memory side pays for several times over.
+constexpr int kCoherentPolicy = 16;  // the SC1 cache-policy bit
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_region(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ void store_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, floatx4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, byte_off, 0, kCoherentPolicy);
+}
+__device__ __forceinline__ floatx4 load_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kCoherentPolicy);
 }
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }

@@ -625,15 +625,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 
   if (a.splits > 1) {
     // publish this split's tile; the last split to arrive sums all of them
-    float* slot = a.partial + ((size_t)t * a.splits + s) * TF + lane * 4;
+    // (the tile's partials: [splits][TF] floats, lane l's 4 values at 4 l)
+    const __amdgpu_buffer_rsrc_t part =
+        coherent_region(a.partial + (size_t)t * a.splits * TF, (uint32_t)(a.splits * TF * 4));
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int j = 0; j < JT; ++j) {
-        float* p = slot + (mt * JT + j) * 256;
-        store_coherent2(p, acc[mt][j][0], acc[mt][j][1]);
-        store_coherent2(p + 2, acc[mt][j][2], acc[mt][j][3]);
-      }
+      for (int j = 0; j < JT; ++j)
+        store_coherent4(part, (uint32_t)((s * TF + (mt * JT + j) * 256 + lane * 4) * 4), acc[mt][j]);
     drain_stores();
     int old = 0;
     if (lane == 0) old = counter_add(&a.counters[t], 1);
@@ -643,22 +642,17 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int j = 0; j < JT; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const float* base = a.partial + (size_t)t * a.splits * TF + lane * 4;
     for (int sp0 = 0; sp0 < a.splits; sp0 += 2) {
       // two splits' tiles in flight, summed in split order
-      floatx4 part[2][MT][JT];
+      floatx4 pv[2][MT][JT];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int sp = sp0 + u < a.splits ? sp0 + u : sp0;
-        const float* src = base + (size_t)sp * TF;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int j = 0; j < JT; ++j) {
-            const float* p = src + (mt * JT + j) * 256;
-            const float2 v01 = load_coherent2(p), v23 = load_coherent2(p + 2);
-            part[u][mt][j] = floatx4{v01.x, v01.y, v23.x, v23.y};
-          }
+          for (int j = 0; j < JT; ++j)
+            pv[u][mt][j] = load_coherent4(part, (uint32_t)((sp * TF + (mt * JT + j) * 256 + lane * 4) * 4));
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u)
@@ -666,7 +660,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int j = 0; j < JT; ++j) acc[mt][j] += part[u][mt][j];
+            for (int j = 0; j < JT; ++j) acc[mt][j] += pv[u][mt][j];
     }
     if (lane == 0) counter_reset(&a.counters[t]);
   }
