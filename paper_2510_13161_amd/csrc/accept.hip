@@ -4,8 +4,9 @@
 // One workgroup per sequence walks the block from the root. GREEDY reads the
 // final head's argmax. The stochastic rules need the target law at the
 // visited node, p = Softmax(z / T), over the whole vocabulary: its
-// logsumexp and the inverse-CDF draw are workgroup reductions in fp64
-// (contiguous id chunks per thread, chunk sums prefixed in id order). The
+// logsumexp and the inverse-CDF draw are workgroup reductions in fp64 over
+// 1024 threads (contiguous id chunks per thread, chunk sums prefixed in id
+// order). The
 // sparse draft law q lives on <= 64 candidate ids, so the rejection residual
 // r = normalise((r - q)^+) differs from a multiple f * p only on those ids:
 // the kernel keeps f and the candidate values, never a dense vocab vector.
@@ -15,7 +16,7 @@ namespace msd {
 namespace {
 
 constexpr int kMaxCand = 64;
-constexpr int kThreads = 256;
+constexpr int kThreads = 1024;  // 16 waves: the fp64 vocabulary passes are latency-bound
 
 struct Shared {
   double red[kThreads];
