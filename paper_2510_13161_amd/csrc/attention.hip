@@ -278,56 +278,57 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
         if (c8 == 0) store_coherent2(a.part_ml + 2 * pidx, M, S);
       }
     }
-    if (nch == 1) continue;
+  }
+  if (nch == 1) return;
 
-    // hand-off: the last chunk to arrive merges the chunks in chunk order
-    drain_stores();
-    __syncthreads();
-    int32_t* ctr = a.counters + ((size_t)b * a.n_kv_heads + kvh) * QT + qt;
-    if (tid == 0) last = counter_add(ctr, 1) == nch - 1;
-    __syncthreads();
-    if (!last) continue;
-    for (int x = tid; x < 16 * C8; x += blockDim.x) {
-      const int qloc = x / C8, c8 = x - qloc * C8;
-      const int qg = qt * 16 + qloc;
-      if (qg >= Qn) continue;
-      float M = -INFINITY, S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      constexpr int MB = MULTI ? 2 : 4;  // chunk partials in flight per merge round
-      for (int c0 = 0; c0 < nch; c0 += MB) {
-        float2 ml[MB];
-        float v[MB][8];
+  // hand-off, once per workgroup: the last chunk of the (sequence, kv head,
+  // tile group) to arrive merges every tile of the group in chunk order
+  drain_stores();
+  __syncthreads();
+  int32_t* ctr = a.counters + ((size_t)b * a.n_kv_heads + kvh) * QG + qgi;
+  if (tid == 0) last = counter_add(ctr, 1) == nch - 1;
+  __syncthreads();
+  if (!last) return;
+  constexpr int MB = 8;  // chunk partials in flight per merge round
+  for (int x = tid; x < (qt1 - qt0) * 16 * C8; x += blockDim.x) {
+    const int qloc = x / C8, c8 = x - qloc * C8;
+    const int qg = qt0 * 16 + qloc;
+    if (qg >= Qn) continue;
+    float M = -INFINITY, S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int c0 = 0; c0 < nch; c0 += MB) {
+      float2 ml[MB];
+      float v[MB][8];
 #pragma unroll
-        for (int u = 0; u < MB; ++u) {
-          const int cc = c0 + u < nch ? c0 + u : c0;
-          const size_t pidx = (pbase + cc) * Qn + qg;
-          ml[u] = load_coherent2(a.part_ml + 2 * pidx);
-          const uint32_t off = (uint32_t)((((size_t)cc * Qn + qg) * HD + 8 * c8) * 4);
-          const floatx4 v0 = load_coherent4(pco, off), v1 = load_coherent4(pco, off + 16);
+      for (int u = 0; u < MB; ++u) {
+        const int cc = c0 + u < nch ? c0 + u : c0;
+        const size_t pidx = (pbase + cc) * Qn + qg;
+        ml[u] = load_coherent2(a.part_ml + 2 * pidx);
+        const uint32_t off = (uint32_t)((((size_t)cc * Qn + qg) * HD + 8 * c8) * 4);
+        const floatx4 v0 = load_coherent4(pco, off), v1 = load_coherent4(pco, off + 16);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            v[u][e] = v0[e];
-            v[u][e + 4] = v1[e];
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < MB; ++u) {
-          if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
-          const float Mn = fmaxf(M, ml[u].x);
-          const float fa = M == -INFINITY ? 0.0f : exp2_hw(M - Mn);
-          const float fb = exp2_hw(ml[u].x - Mn);
-          S = S * fa + ml[u].y * fb;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) o8[e] = o8[e] * fa + v[u][e] * fb;
-          M = Mn;
+        for (int e = 0; e < 4; ++e) {
+          v[u][e] = v0[e];
+          v[u][e + 4] = v1[e];
         }
       }
-      const float inv = S > 0.0f ? 1.0f / S : 0.0f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o8[e] *= inv;
-      write_out<HD>(a, b, kvh, qg, c8, o8);
+      for (int u = 0; u < MB; ++u) {
+        if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
+        const float Mn = fmaxf(M, ml[u].x);
+        const float fa = M == -INFINITY ? 0.0f : exp2_hw(M - Mn);
+        const float fb = exp2_hw(ml[u].x - Mn);
+        S = S * fa + ml[u].y * fb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o8[e] = o8[e] * fa + v[u][e] * fb;
+        M = Mn;
+      }
     }
-    if (tid == 0) counter_reset(ctr);
+    const float inv = S > 0.0f ? 1.0f / S : 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o8[e] *= inv;
+    write_out<HD>(a, b, kvh, qg, c8, o8);
   }
+  if (tid == 0) counter_reset(ctr);
 }
 
 }  // namespace

@@ -140,7 +140,7 @@ struct AttnArgs {
   uint32_t* status;
   uint16_t* out_img;        // image of the output (K = H * hd)
   int32_t MT;
-  int32_t* counters;        // [batch][Hkv][query tiles]: zero on entry, left zero
+  int32_t* counters;        // [batch][Hkv][query-tile groups]: zero on entry, left zero
   float* part_o;            // [batch][Hkv][chunks][Qn][hd]
   float* part_ml;           // [batch][Hkv][chunks][Qn][2] (max of score * log2 e, sum exp2)
   int32_t batch, n_heads, n_kv_heads, capacity, n_slots;
