@@ -49,6 +49,27 @@ __device__ __forceinline__ void write_out(const AttnArgs& a, int b, int kvh, int
   *reinterpret_cast<u32x4*>(dst + 512) = lw;
 }
 
+// the same for 4 consecutive dims [4 c4, 4 c4 + 4): half of an image lane
+// (the same bf16 pairs as write_out, so the same bits)
+template <int HD>
+__device__ __forceinline__ void write_out4(const AttnArgs& a, int b, int kvh, int qg, int c4,
+                                           const float (&o)[4]) {
+  const int ns = a.n_slots, G = a.n_heads / a.n_kv_heads;
+  const int gq = qg / ns, slot = qg - gq * ns;
+  const int m = b * ns + slot, h = kvh * G + gq;
+  const int col = h * HD + 4 * c4;
+  const int ks = col >> 5, grp = (col >> 3) & 3;
+  u32x2 hw, lw;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    hw[i] = pack_bf16x2(o[2 * i], o[2 * i + 1]);
+    lw[i] = pack_bf16x2(o[2 * i] - bf_lo(hw[i]), o[2 * i + 1] - bf_hi(hw[i]));
+  }
+  uint16_t* dst = a.out_img + img_offset(ks, m >> 4, a.MT, 16 * grp + (m & 15)) + (col & 7);
+  *reinterpret_cast<u32x2*>(dst) = hw;
+  *reinterpret_cast<u32x2*>(dst + 512) = lw;
+}
+
 template <int HD>
 struct AttnLds {
   static constexpr int kVS = HD + 4;  // bf16 per LDS row of V (one key), conflict-free strides
@@ -66,6 +87,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   constexpr int KSTEPS = HD / 32;
   constexpr int DSUB = HD / 16;
   constexpr int C8 = HD / 8;
+  constexpr int C4 = HD / 4;
   constexpr int VIT = HD / 8;    // 16-byte V chunks per lane per 64-key block
   constexpr int KPI = 512 / HD;  // keys per V chunk iteration
   __shared__ __attribute__((aligned(16))) unsigned char region_all[4][Lds::kRegion];
@@ -240,42 +262,64 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     }
     __syncthreads();
     // merge the 4 waves (wave order), then output or publish the chunk
-    for (int x = tid; x < 16 * C8; x += blockDim.x) {
-      const int qloc = x / C8, c8 = x - qloc * C8;
-      const int qg = qt * 16 + qloc;
-      if (qg >= Qn) continue;
-      float M = -INFINITY;
+    if (nch == 1) {
+      for (int x = tid; x < 16 * C8; x += blockDim.x) {
+        const int qloc = x / C8, c8 = x - qloc * C8;
+        const int qg = qt * 16 + qloc;
+        if (qg >= Qn) continue;
+        float M = -INFINITY;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
-      float S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
+        float S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float mw = ml_sh[w][qloc][0];
-        const float f = mw == -INFINITY ? 0.0f : exp2_hw(mw - M);
-        S += ml_sh[w][qloc][1] * f;
-        const float* src = reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 8 * c8;
-        const float4 v0 = *reinterpret_cast<const float4*>(src);
-        const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
-        o8[0] += f * v0.x;
-        o8[1] += f * v0.y;
-        o8[2] += f * v0.z;
-        o8[3] += f * v0.w;
-        o8[4] += f * v1.x;
-        o8[5] += f * v1.y;
-        o8[6] += f * v1.z;
-        o8[7] += f * v1.w;
-      }
-      if (nch == 1) {
+        for (int w = 0; w < 4; ++w) {
+          const float mw = ml_sh[w][qloc][0];
+          const float f = mw == -INFINITY ? 0.0f : exp2_hw(mw - M);
+          S += ml_sh[w][qloc][1] * f;
+          const float* src = reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 8 * c8;
+          const float4 v0 = *reinterpret_cast<const float4*>(src);
+          const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
+          o8[0] += f * v0.x;
+          o8[1] += f * v0.y;
+          o8[2] += f * v0.z;
+          o8[3] += f * v0.w;
+          o8[4] += f * v1.x;
+          o8[5] += f * v1.y;
+          o8[6] += f * v1.z;
+          o8[7] += f * v1.w;
+        }
         const float inv = S > 0.0f ? 1.0f / S : 0.0f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) o8[e] *= inv;
         write_out<HD>(a, b, kvh, qg, c8, o8);
-      } else {
+      }
+    } else {
+      // 4 dims a thread, so that each 16-byte store of a wave covers one
+      // contiguous 1 KB of the chunk's [Qn][HD] partial: whole lines
+      for (int x = tid; x < 16 * C4; x += blockDim.x) {
+        const int qloc = x / C4, c4 = x - qloc * C4;
+        const int qg = qt * 16 + qloc;
+        if (qg >= Qn) continue;
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
+        float S = 0.0f;
+        floatx4 o4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float mw = ml_sh[w][qloc][0];
+          const float f = mw == -INFINITY ? 0.0f : exp2_hw(mw - M);
+          S += ml_sh[w][qloc][1] * f;
+          const float4 v0 = *reinterpret_cast<const float4*>(
+              reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 4 * c4);
+          o4[0] += f * v0.x;
+          o4[1] += f * v0.y;
+          o4[2] += f * v0.z;
+          o4[3] += f * v0.w;
+        }
         const size_t pidx = (pbase + c) * Qn + qg;
-        const uint32_t off = (uint32_t)((((size_t)c * Qn + qg) * HD + 8 * c8) * 4);
-        store_coherent4(pco, off, floatx4{o8[0], o8[1], o8[2], o8[3]});
-        store_coherent4(pco, off + 16, floatx4{o8[4], o8[5], o8[6], o8[7]});
-        if (c8 == 0) store_coherent2(a.part_ml + 2 * pidx, M, S);
+        store_coherent4(pco, (uint32_t)((((size_t)c * Qn + qg) * HD + 4 * c4) * 4), o4);
+        if (c4 == 0) store_coherent2(a.part_ml + 2 * pidx, M, S);
       }
     }
   }
@@ -290,26 +334,20 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   __syncthreads();
   if (!last) return;
   constexpr int MB = 8;  // chunk partials in flight per merge round
-  for (int x = tid; x < (qt1 - qt0) * 16 * C8; x += blockDim.x) {
-    const int qloc = x / C8, c8 = x - qloc * C8;
+  for (int x = tid; x < (qt1 - qt0) * 16 * C4; x += blockDim.x) {
+    const int qloc = x / C4, c4 = x - qloc * C4;
     const int qg = qt0 * 16 + qloc;
     if (qg >= Qn) continue;
-    float M = -INFINITY, S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float M = -INFINITY, S = 0.0f, o4[4] = {0.f, 0.f, 0.f, 0.f};
     for (int c0 = 0; c0 < nch; c0 += MB) {
       float2 ml[MB];
-      float v[MB][8];
+      floatx4 v[MB];
 #pragma unroll
       for (int u = 0; u < MB; ++u) {
         const int cc = c0 + u < nch ? c0 + u : c0;
         const size_t pidx = (pbase + cc) * Qn + qg;
         ml[u] = load_coherent2(a.part_ml + 2 * pidx);
-        const uint32_t off = (uint32_t)((((size_t)cc * Qn + qg) * HD + 8 * c8) * 4);
-        const floatx4 v0 = load_coherent4(pco, off), v1 = load_coherent4(pco, off + 16);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[u][e] = v0[e];
-          v[u][e + 4] = v1[e];
-        }
+        v[u] = load_coherent4(pco, (uint32_t)((((size_t)cc * Qn + qg) * HD + 4 * c4) * 4));
       }
 #pragma unroll
       for (int u = 0; u < MB; ++u) {
@@ -319,14 +357,14 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
         const float fb = exp2_hw(ml[u].x - Mn);
         S = S * fa + ml[u].y * fb;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o8[e] = o8[e] * fa + v[u][e] * fb;
+        for (int e = 0; e < 4; ++e) o4[e] = o4[e] * fa + v[u][e] * fb;
         M = Mn;
       }
     }
     const float inv = S > 0.0f ? 1.0f / S : 0.0f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o8[e] *= inv;
-    write_out<HD>(a, b, kvh, qg, c8, o8);
+    for (int e = 0; e < 4; ++e) o4[e] *= inv;
+    write_out4<HD>(a, b, kvh, qg, c4, o4);
   }
   if (tid == 0) counter_reset(ctr);
 }
