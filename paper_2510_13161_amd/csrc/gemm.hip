@@ -693,6 +693,7 @@ hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
     case 1: return a.waves == 8 ? launch_cfg<1, 8, EPI, 4>(a, s) : launch_cfg<1, 4, EPI, 4>(a, s);
     case 2: return launch_cfg<2, 4, EPI, 4>(a, s);
     case 3: return launch_cfg<3, 4, EPI, 4>(a, s);
+    case 5: return launch_cfg<5, 4, EPI, 4>(a, s);
     case 9: return launch_cfg<9, 4, EPI, 4>(a, s);
     default: return hipErrorInvalidValue;
   }

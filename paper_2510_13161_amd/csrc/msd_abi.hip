@@ -55,10 +55,11 @@ inline const uint16_t* head_w(const msd_model* m) {
 
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Row tiles of the kernels for M rows: 1, 2 or 3, else the 9-tile variant.
+// Row tiles of the kernels for M rows: 1, 2 or 3, else 5 (up to 80 rows),
+// else the 9-tile variant.
 inline int row_tiles(int M) {
   const int mt = (M + 15) / 16;
-  return mt <= 3 ? mt : kMaxMT;
+  return mt <= 3 ? mt : (mt <= 5 ? 5 : kMaxMT);
 }
 
 // Split-K factor: about target_wgs workgroups per GEMM, each wave keeping at
