@@ -33,7 +33,7 @@ namespace {
 // ks holding rows 16G..16G+15 x columns 32ks..32ks+31 in MFMA operand order
 // (lane l: row 16G + l%16, columns 32ks + 8(l/16) .. +8).
 // A tile is JT sub-tiles of 16 output columns (JT = 4: 64 columns; JT = 8:
-// 128 columns, for the SwiGLU FFN up projection with one row tile).
+// 128 columns, for the SwiGLU FFN up projection with up to 3 row tiles).
 // Returns the lane's pointer into fragment 0 of the group feeding sub-tile j.
 template <int JT>
 __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t, int j, int lane) {
