@@ -132,7 +132,12 @@ typedef struct msd_model msd_model;
  * 1 KB MFMA operands along K), so the verify pass reads HBM sequentially.
  * After the call those tensors are opaque to the caller, and one set of
  * tensors can back only one model. The call synchronises the device and
- * briefly allocates a temporary buffer the size of the largest matrix. */
+ * briefly allocates a temporary buffer the size of the largest matrix.
+ * Launch-shape overrides, read from the environment here (tuning and tests;
+ * results differ only by floating-point summation order): MSD_GEMM_TARGET_WGS
+ * (split-K sizing, workgroups per GEMM), MSD_GEMM_WAVES (4 or 8) and
+ * MSD_ATTN_SPANS (256-key spans per attention workgroup: 1 forces the
+ * one-span kernel, 2 or more the streaming one; unset, chosen per call). */
 msd_status msd_model_create(const msd_model_config* cfg, const void* const* tensors,
                             int32_t n_tensors, msd_model** out);
 void msd_model_destroy(msd_model* model);

@@ -79,6 +79,154 @@ struct AttnLds {
   static constexpr int kRegion = kVBytes > kOBytes ? kVBytes : kOBytes;
 };
 
+// Publish a wave's (max, sum, output) of one query tile to its LDS region: o[ds][r]
+// holds query 4 g + r, dim 16 ds + lane % 16; the statistics are replicated
+// over g. The first barrier orders the region's earlier use (V rows, the
+// previous tile's merge) before the writes.
+template <int HD>
+__device__ __forceinline__ void publish_tile(unsigned char (*region_all)[AttnLds<HD>::kRegion],
+                                             float (*ml_sh)[16][2], const floatx4* o, float mx, float ls) {
+  using Lds = AttnLds<HD>;
+  constexpr int DSUB = HD / 16;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  float* os = reinterpret_cast<float*>(region_all[wave]);
+  __syncthreads();
+#pragma unroll
+  for (int ds = 0; ds < DSUB; ++ds)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) os[(4 * g + r) * Lds::kOS + ds * 16 + r16] = o[ds][r];
+  if (g == 0) {
+    ml_sh[wave][r16][0] = mx;
+    ml_sh[wave][r16][1] = ls;
+  }
+  __syncthreads();
+}
+
+// Merge the 4 published waves of query tile qt in wave order; a chunk that
+// covers the whole sequence writes the normalised output into the image,
+// any other publishes its partial (4 dims a thread, so that each 16-byte
+// store of a wave covers one contiguous 1 KB of the chunk's [Qn][HD]
+// partial: whole lines).
+template <int HD>
+__device__ __forceinline__ void merge_waves(const AttnArgs& a, unsigned char (*region_all)[AttnLds<HD>::kRegion],
+                                            float (*ml_sh)[16][2], int b, int kvh, int qt, int Qn, int nch,
+                                            int c, size_t pbase, __amdgpu_buffer_rsrc_t pco) {
+  using Lds = AttnLds<HD>;
+  constexpr int C8 = HD / 8;
+  constexpr int C4 = HD / 4;
+  const int tid = threadIdx.x;
+  if (nch == 1) {
+    for (int x = tid; x < 16 * C8; x += blockDim.x) {
+      const int qloc = x / C8, c8 = x - qloc * C8;
+      const int qg = qt * 16 + qloc;
+      if (qg >= Qn) continue;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
+      float S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float mw = ml_sh[w][qloc][0];
+        const float f = mw == -INFINITY ? 0.0f : exp2_hw(mw - M);
+        S += ml_sh[w][qloc][1] * f;
+        const float* src = reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 8 * c8;
+        const float4 v0 = *reinterpret_cast<const float4*>(src);
+        const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
+        o8[0] += f * v0.x;
+        o8[1] += f * v0.y;
+        o8[2] += f * v0.z;
+        o8[3] += f * v0.w;
+        o8[4] += f * v1.x;
+        o8[5] += f * v1.y;
+        o8[6] += f * v1.z;
+        o8[7] += f * v1.w;
+      }
+      const float inv = S > 0.0f ? 1.0f / S : 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o8[e] *= inv;
+      write_out<HD>(a, b, kvh, qg, c8, o8);
+    }
+  } else {
+    for (int x = tid; x < 16 * C4; x += blockDim.x) {
+      const int qloc = x / C4, c4 = x - qloc * C4;
+      const int qg = qt * 16 + qloc;
+      if (qg >= Qn) continue;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
+      float S = 0.0f;
+      floatx4 o4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float mw = ml_sh[w][qloc][0];
+        const float f = mw == -INFINITY ? 0.0f : exp2_hw(mw - M);
+        S += ml_sh[w][qloc][1] * f;
+        const float4 v0 = *reinterpret_cast<const float4*>(
+            reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 4 * c4);
+        o4[0] += f * v0.x;
+        o4[1] += f * v0.y;
+        o4[2] += f * v0.z;
+        o4[3] += f * v0.w;
+      }
+      const size_t pidx = (pbase + c) * Qn + qg;
+      store_coherent4(pco, (uint32_t)((((size_t)c * Qn + qg) * HD + 4 * c4) * 4), o4);
+      if (c4 == 0) store_coherent2(a.part_ml + 2 * pidx, M, S);
+    }
+  }
+}
+
+// The chunk hand-off, once per workgroup after its partials are stored: the
+// last chunk of the (sequence, kv head, tile group) to arrive merges tiles
+// [qt0, qt1) over all nch chunks in chunk order and writes the normalised
+// output; it leaves the counter zero.
+template <int HD>
+__device__ __forceinline__ void merge_chunks(const AttnArgs& a, int* last, int32_t* ctr, int b, int kvh,
+                                             int qt0, int qt1, int Qn, int nch, size_t pbase,
+                                             __amdgpu_buffer_rsrc_t pco) {
+  constexpr int C4 = HD / 4;
+  const int tid = threadIdx.x;
+  drain_stores();
+  __syncthreads();
+  if (tid == 0) *last = counter_add(ctr, 1) == nch - 1;
+  __syncthreads();
+  if (!*last) return;
+  constexpr int MB = 8;  // chunk partials in flight per merge round
+  for (int x = tid; x < (qt1 - qt0) * 16 * C4; x += blockDim.x) {
+    const int qloc = x / C4, c4 = x - qloc * C4;
+    const int qg = qt0 * 16 + qloc;
+    if (qg >= Qn) continue;
+    float M = -INFINITY, S = 0.0f, o4[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int c0 = 0; c0 < nch; c0 += MB) {
+      float2 ml[MB];
+      floatx4 v[MB];
+#pragma unroll
+      for (int u = 0; u < MB; ++u) {
+        const int cc = c0 + u < nch ? c0 + u : c0;
+        const size_t pidx = (pbase + cc) * Qn + qg;
+        ml[u] = load_coherent2(a.part_ml + 2 * pidx);
+        v[u] = load_coherent4(pco, (uint32_t)((((size_t)cc * Qn + qg) * HD + 4 * c4) * 4));
+      }
+#pragma unroll
+      for (int u = 0; u < MB; ++u) {
+        if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
+        const float Mn = fmaxf(M, ml[u].x);
+        const float fa = M == -INFINITY ? 0.0f : exp2_hw(M - Mn);
+        const float fb = exp2_hw(ml[u].x - Mn);
+        S = S * fa + ml[u].y * fb;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o4[e] = o4[e] * fa + v[u][e] * fb;
+        M = Mn;
+      }
+    }
+    const float inv = S > 0.0f ? 1.0f / S : 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o4[e] *= inv;
+    write_out4<HD>(a, b, kvh, qg, c4, o4);
+  }
+  if (tid == 0) counter_reset(ctr);
+}
+
 // MULTI: the workgroup takes several query tiles in turn (K and V operands
 // stay in registers across them); otherwise exactly one.
 template <int HD, bool MULTI>
@@ -86,8 +234,6 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   using Lds = AttnLds<HD>;
   constexpr int KSTEPS = HD / 32;
   constexpr int DSUB = HD / 16;
-  constexpr int C8 = HD / 8;
-  constexpr int C4 = HD / 4;
   constexpr int VIT = HD / 8;    // 16-byte V chunks per lane per 64-key block
   constexpr int KPI = 512 / HD;  // keys per V chunk iteration
   __shared__ __attribute__((aligned(16))) unsigned char region_all[4][Lds::kRegion];
@@ -112,7 +258,6 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   const int nch = (T + kAttnChunk - 1) / kAttnChunk;
   if (c >= nch) return;
   uint16_t* vs = reinterpret_cast<uint16_t*>(region_all[wave]);  // [64 keys][kVS]
-  float* os = reinterpret_cast<float*>(region_all[wave]);        // [16 queries][kOS]
   const size_t row0 = ((size_t)b * a.n_kv_heads + kvh) * a.capacity;
   const uint16_t* kbase = a.k_cache + row0 * HD;
   const uint16_t* vbase = a.v_cache + row0 * HD;
@@ -248,125 +393,256 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
       }
     }
 
-    // publish the wave's (max, sum, output) to its LDS region: every wave's
-    // V reads, and the previous tile's merge, are done once all have passed
-    // this barrier
-    __syncthreads();
-#pragma unroll
-    for (int ds = 0; ds < DSUB; ++ds)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) os[(4 * g + r) * Lds::kOS + ds * 16 + r16] = o[ds][r];
-    if (g == 0) {
-      ml_sh[wave][r16][0] = mx;
-      ml_sh[wave][r16][1] = ls;
-    }
-    __syncthreads();
-    // merge the 4 waves (wave order), then output or publish the chunk
-    if (nch == 1) {
-      for (int x = tid; x < 16 * C8; x += blockDim.x) {
-        const int qloc = x / C8, c8 = x - qloc * C8;
-        const int qg = qt * 16 + qloc;
-        if (qg >= Qn) continue;
-        float M = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
-        float S = 0.0f, o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float mw = ml_sh[w][qloc][0];
-          const float f = mw == -INFINITY ? 0.0f : exp2_hw(mw - M);
-          S += ml_sh[w][qloc][1] * f;
-          const float* src = reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 8 * c8;
-          const float4 v0 = *reinterpret_cast<const float4*>(src);
-          const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
-          o8[0] += f * v0.x;
-          o8[1] += f * v0.y;
-          o8[2] += f * v0.z;
-          o8[3] += f * v0.w;
-          o8[4] += f * v1.x;
-          o8[5] += f * v1.y;
-          o8[6] += f * v1.z;
-          o8[7] += f * v1.w;
-        }
-        const float inv = S > 0.0f ? 1.0f / S : 0.0f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o8[e] *= inv;
-        write_out<HD>(a, b, kvh, qg, c8, o8);
-      }
-    } else {
-      // 4 dims a thread, so that each 16-byte store of a wave covers one
-      // contiguous 1 KB of the chunk's [Qn][HD] partial: whole lines
-      for (int x = tid; x < 16 * C4; x += blockDim.x) {
-        const int qloc = x / C4, c4 = x - qloc * C4;
-        const int qg = qt * 16 + qloc;
-        if (qg >= Qn) continue;
-        float M = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_sh[w][qloc][0]);
-        float S = 0.0f;
-        floatx4 o4 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float mw = ml_sh[w][qloc][0];
-          const float f = mw == -INFINITY ? 0.0f : exp2_hw(mw - M);
-          S += ml_sh[w][qloc][1] * f;
-          const float4 v0 = *reinterpret_cast<const float4*>(
-              reinterpret_cast<const float*>(region_all[w]) + qloc * Lds::kOS + 4 * c4);
-          o4[0] += f * v0.x;
-          o4[1] += f * v0.y;
-          o4[2] += f * v0.z;
-          o4[3] += f * v0.w;
-        }
-        const size_t pidx = (pbase + c) * Qn + qg;
-        store_coherent4(pco, (uint32_t)((((size_t)c * Qn + qg) * HD + 4 * c4) * 4), o4);
-        if (c4 == 0) store_coherent2(a.part_ml + 2 * pidx, M, S);
-      }
-    }
+    // every wave's V reads, and the previous tile's merge, are done once all
+    // have passed publish_tile's first barrier
+    publish_tile<HD>(region_all, ml_sh, o, mx, ls);
+    merge_waves<HD>(a, region_all, ml_sh, b, kvh, qt, Qn, nch, c, pbase, pco);
   }
   if (nch == 1) return;
+  merge_chunks<HD>(a, &last, a.counters + ((size_t)b * a.n_kv_heads + kvh) * QG + qgi, b, kvh, qt0, qt1, Qn,
+                   nch, pbase, pco);
+}
 
-  // hand-off, once per workgroup: the last chunk of the (sequence, kv head,
-  // tile group) to arrive merges every tile of the group in chunk order
-  drain_stores();
-  __syncthreads();
-  int32_t* ctr = a.counters + ((size_t)b * a.n_kv_heads + kvh) * QG + qgi;
-  if (tid == 0) last = counter_add(ctr, 1) == nch - 1;
-  __syncthreads();
-  if (!last) return;
-  constexpr int MB = 8;  // chunk partials in flight per merge round
-  for (int x = tid; x < (qt1 - qt0) * 16 * C4; x += blockDim.x) {
-    const int qloc = x / C4, c4 = x - qloc * C4;
-    const int qg = qt0 * 16 + qloc;
-    if (qg >= Qn) continue;
-    float M = -INFINITY, S = 0.0f, o4[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int c0 = 0; c0 < nch; c0 += MB) {
-      float2 ml[MB];
-      floatx4 v[MB];
+// Long contexts: a workgroup owns a chunk of nb consecutive 256-key spans and
+// takes them in turn, each wave its 64-key block of every span. Per query tile
+// of the group a wave keeps a running (max, sum, output), rescaled at each
+// block (the online softmax), and it issues the loads of its next block
+// before the arithmetic of the current one, so that its K and V stream while
+// it computes. The group's query tiles sit in LDS, shared by the 4 waves.
+// The 4-wave merge, the chunk hand-off and the final merge are those of the
+// kernel above, once per chunk of nb spans instead of once per span.
+template <int HD, int QPW>
+__global__ __launch_bounds__(256, 1) void attn_stream_kernel(AttnArgs a) {
+  using Lds = AttnLds<HD>;
+  constexpr int KSTEPS = HD / 32;
+  constexpr int DSUB = HD / 16;
+  constexpr int VIT = HD / 8;
+  constexpr int KPI = 512 / HD;
+  __shared__ __attribute__((aligned(16))) unsigned char region_all[4][Lds::kRegion];
+  __shared__ __attribute__((aligned(16))) uint16_t q_sh[QPW * KSTEPS * 1024];
+  __shared__ float ml_sh[4][16][2];
+  __shared__ int last;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int G = a.n_heads / a.n_kv_heads;
+  const int ns = a.n_slots;
+  const int Qn = G * ns;
+  const int QT = (Qn + 15) >> 4;
+  const int QG = (QT + QPW - 1) / QPW;
+  const int b = blockIdx.z, kvh = blockIdx.y / QG, qgi = blockIdx.y - kvh * QG, c = blockIdx.x;
+  const int qt0 = qgi * QPW, ntile = min(QPW, QT - qt0);
+  const int L = a.len[b];
+  const int T = L + ns;
+  if (T > a.capacity) {
+    if (c == 0 && blockIdx.y == 0 && tid == 0) atomicOr(a.status, 1u);
+    return;
+  }
+  const int nch = (T + a.nb * kAttnChunk - 1) / (a.nb * kAttnChunk);
+  if (c >= nch) return;
+  const int sp0 = c * a.nb;                                              // first 256-key span
+  const int nsp = min(a.nb, (T + kAttnChunk - 1) / kAttnChunk - sp0);  // spans with keys, >= 1
+  uint16_t* vs = reinterpret_cast<uint16_t*>(region_all[wave]);  // [64 keys][kVS]
+  const size_t row0 = ((size_t)b * a.n_kv_heads + kvh) * a.capacity;
+  const uint16_t* kbase = a.k_cache + row0 * HD;
+  const uint16_t* vbase = a.v_cache + row0 * HD;
+
+  // one 64-key block: V rows and K fragments (rows past the last key clamped
+  // to a valid row; their scores are masked)
+  u32x4 vraw[VIT];
+  bf16x8 kf[4][KSTEPS];
+  auto load_block = [&](int k0) {
 #pragma unroll
-      for (int u = 0; u < MB; ++u) {
-        const int cc = c0 + u < nch ? c0 + u : c0;
-        const size_t pidx = (pbase + cc) * Qn + qg;
-        ml[u] = load_coherent2(a.part_ml + 2 * pidx);
-        v[u] = load_coherent4(pco, (uint32_t)((((size_t)cc * Qn + qg) * HD + 4 * c4) * 4));
+    for (int it = 0; it < VIT; ++it) {
+      const int pos = min(k0 + it * KPI + lane / (HD / 8), T - 1);
+      vraw[it] = *reinterpret_cast<const u32x4*>(vbase + (size_t)pos * HD + (lane % (HD / 8)) * 8);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int pos = min(k0 + 16 * j + r16, T - 1);
+#pragma unroll
+      for (int kk = 0; kk < KSTEPS; ++kk) kf[j][kk] = load16(kbase + (size_t)pos * HD + kk * 32 + g * 8);
+    }
+  };
+  load_block(sp0 * kAttnChunk + 64 * wave);
+  {
+    // the group's query tiles (the QKV epilogue's split-bf16 operand image,
+    // tiles of one kv head contiguous) into LDS
+    const u32x4* src = reinterpret_cast<const u32x4*>(
+        a.q_img + (((size_t)b * a.n_kv_heads + kvh) * QT + qt0) * (size_t)KSTEPS * 1024);
+    u32x4* dst = reinterpret_cast<u32x4*>(q_sh);
+    // 16-byte piece i is lane (i % 64) of a 512-element part: query row
+    // (i % 16) of its tile; padding queries (past G * n_slots) and tiles past
+    // the group's last are zero, so whatever the workspace holds there never
+    // reaches a score
+    for (int i = tid; i < QPW * KSTEPS * 128; i += blockDim.x) {
+      const int t = i / (KSTEPS * 128);
+      const bool ok = t < ntile && (qt0 + t) * 16 + (i & 15) < Qn;
+      dst[i] = ok ? src[i] : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  uint64_t anc[QPW];
+#pragma unroll
+  for (int t = 0; t < QPW; ++t) {
+    const int qv = (qt0 + t) * 16 + r16;
+    anc[t] = t < ntile && qv < Qn ? a.topo.anc[qv % ns] : 0ull;
+  }
+  __syncthreads();
+
+  const float scale2 = a.scale * kLog2e;
+  float mrun[QPW], lrun[QPW];
+  floatx4 o[QPW][DSUB];
+#pragma unroll
+  for (int t = 0; t < QPW; ++t) {
+    mrun[t] = -INFINITY;
+    lrun[t] = 0.0f;
+#pragma unroll
+    for (int ds = 0; ds < DSUB; ++ds) o[t][ds] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int sp = 0; sp < nsp; ++sp) {
+    const int k0 = (sp0 + sp) * kAttnChunk + 64 * wave;
+    const int key_hi = min(T, k0 + 64);  // this wave's keys [k0, key_hi), maybe none
+    // V rows into the wave's LDS (its previous block's reads are done: one
+    // wave's LDS accesses complete in order)
+    wave_lds_sync();
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int key = it * KPI + lane / (HD / 8);
+      *reinterpret_cast<u32x4*>(vs + key * Lds::kVS + (lane % (HD / 8)) * 8) = vraw[it];
+    }
+    bf16x8 kc[4][KSTEPS];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int kk = 0; kk < KSTEPS; ++kk) kc[j][kk] = kf[j][kk];
+    wave_lds_sync();
+    if (sp + 1 < nsp) load_block(k0 + kAttnChunk);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // the tiles phase by phase, so that one tile's latencies (LDS reads,
+    // lane exchanges) overlap the others' arithmetic: scores of every tile
+    floatx4 sc[QPW][4];
+#pragma unroll
+    for (int t = 0; t < QPW; ++t) {
+      bf16x8 qh[KSTEPS], ql[KSTEPS];
+#pragma unroll
+      for (int kk = 0; kk < KSTEPS; ++kk) {
+        qh[kk] = *reinterpret_cast<const bf16x8*>(q_sh + (t * KSTEPS + kk) * 1024 + lane * 8);
+        ql[kk] = *reinterpret_cast<const bf16x8*>(q_sh + (t * KSTEPS + kk) * 1024 + 512 + lane * 8);
       }
 #pragma unroll
-      for (int u = 0; u < MB; ++u) {
-        if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
-        const float Mn = fmaxf(M, ml[u].x);
-        const float fa = M == -INFINITY ? 0.0f : exp2_hw(M - Mn);
-        const float fb = exp2_hw(ml[u].x - Mn);
-        S = S * fa + ml[u].y * fb;
+      for (int j = 0; j < 4; ++j) {
+        sc[t][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o4[e] = o4[e] * fa + v[u][e] * fb;
-        M = Mn;
+        for (int kk = 0; kk < KSTEPS; ++kk) {
+          sc[t][j] = mfma16x16x32(kc[j][kk], qh[kk], sc[t][j]);
+          sc[t][j] = mfma16x16x32(kc[j][kk], ql[kk], sc[t][j]);
+        }
       }
     }
-    const float inv = S > 0.0f ? 1.0f / S : 0.0f;
+    // lane holds S^T[key 16j + 4g + r][query r16]: scale (base 2), mask (a
+    // block wholly inside the cached context is visible to every query: a
+    // branch the whole wave takes), block max, running statistics of query
+    // r16, P as bf16 hi + lo
+    const bool open = k0 + 64 <= L;
+    u32x4 ph[QPW][2], pl[QPW][2];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o4[e] *= inv;
-    write_out4<HD>(a, b, kvh, qg, c4, o4);
+    for (int t = 0; t < QPW; ++t) {
+      float mx = -INFINITY;
+      if (open) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            sc[t][j][r] *= scale2;
+            mx = fmaxf(mx, sc[t][j][r]);
+          }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int pos = k0 + 16 * j + 4 * g + r;
+            const bool anc_bit = (anc[t] >> ((pos - L) & 63)) & 1ull;
+            const bool vis = (pos < key_hi) & ((pos < L) | anc_bit);
+            sc[t][j][r] = vis ? sc[t][j][r] * scale2 : -INFINITY;
+            mx = fmaxf(mx, sc[t][j][r]);
+          }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      // The reference of the running sums moves up only when a block max
+      // exceeds it by more than 2^8 (or on the first visible block): the
+      // sums and P are exact for any reference at or above the true max
+      // minus 8, and the rescale of the output, the costly part, is skipped
+      // for most blocks. The decision is the wave's, so the branch is too.
+      if (__builtin_amdgcn_read_exec() & __ballot(mx > mrun[t] + 8.0f)) {
+        const float mnew = fmaxf(mrun[t], mx);
+        const float alpha = mrun[t] == -INFINITY ? 0.0f : exp2_hw(mrun[t] - mnew);
+        lrun[t] *= alpha;
+        mrun[t] = mnew;
+        // o[t][ds][r] belongs to query 4 g + r, whose factor lane 4 g + r holds
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float ar = __shfl(alpha, 4 * g + r);
+#pragma unroll
+          for (int ds = 0; ds < DSUB; ++ds) o[t][ds][r] *= ar;
+        }
+      }
+      const float mref = mrun[t] == -INFINITY ? 0.0f : mrun[t];
+      float ls = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          sc[t][j][r] = exp2_hw(sc[t][j][r] - mref);
+          ls += sc[t][j][r];
+        }
+      ls += __shfl_xor(ls, 16);
+      ls += __shfl_xor(ls, 32);
+      lrun[t] += ls;
+      // P in the k order of the V operand: keys 4 g + r of the two 16-key tiles
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const float p0 = sc[t][2 * kb + (x >> 1)][2 * (x & 1)];
+          const float p1 = sc[t][2 * kb + (x >> 1)][2 * (x & 1) + 1];
+          ph[t][kb][x] = pack_bf16x2(p0, p1);
+          pl[t][kb][x] = pack_bf16x2(p0 - bf_lo(ph[t][kb][x]), p1 - bf_hi(ph[t][kb][x]));
+        }
+    }
+    // O += P V: each V operand read once (the transposing LDS read of the
+    // kernel above: dim 16 ds + lane % 16 of keys 32 kb + 4 g + e and
+    // 32 kb + 16 + 4 g + e) for every tile
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int ds = 0; ds < DSUB; ++ds) {
+        const uint16_t* p0 = vs + (32 * kb + 4 * g + (r16 >> 2)) * Lds::kVS + 16 * ds + 4 * (r16 & 3);
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p0);
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0 + 16 * Lds::kVS));
+        const bf16x8 vb = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int t = 0; t < QPW; ++t) {
+          o[t][ds] = mfma16x16x32(__builtin_bit_cast(bf16x8, ph[t][kb]), vb, o[t][ds]);
+          o[t][ds] = mfma16x16x32(__builtin_bit_cast(bf16x8, pl[t][kb]), vb, o[t][ds]);
+        }
+      }
   }
-  if (tid == 0) counter_reset(ctr);
+
+  const size_t pbase = ((size_t)b * a.n_kv_heads + kvh) * a.max_chunks;
+  const __amdgpu_buffer_rsrc_t pco =
+      coherent_region(a.part_o + pbase * Qn * HD, (uint32_t)((size_t)a.max_chunks * Qn * HD * 4));
+#pragma unroll
+  for (int t = 0; t < QPW; ++t) {
+    if (t >= ntile) break;
+    publish_tile<HD>(region_all, ml_sh, o[t], mrun[t], lrun[t]);
+    merge_waves<HD>(a, region_all, ml_sh, b, kvh, qt0 + t, Qn, nch, c, pbase, pco);
+  }
+  if (nch == 1) return;
+  merge_chunks<HD>(a, &last, a.counters + ((size_t)b * a.n_kv_heads + kvh) * QG + qgi, b, kvh, qt0,
+                   qt0 + ntile, Qn, nch, pbase, pco);
 }
 
 }  // namespace
@@ -374,18 +650,34 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s) {
   if (a.max_chunks > kMaxAttnChunks || a.max_chunks < 1) return hipErrorInvalidValue;
   if (a.max_chunks > 1 && !a.counters) return hipErrorInvalidValue;
+  if (head_dim != 128 && head_dim != 64) return hipErrorInvalidValue;
   const int qt = (a.n_heads / a.n_kv_heads * a.n_slots + 15) / 16;
-  if (a.q_per_wg < 1) return hipErrorInvalidValue;
-  const dim3 grid(a.max_chunks, a.n_kv_heads * ((qt + a.q_per_wg - 1) / a.q_per_wg), a.batch);
+  if (a.q_per_wg < 1 || a.nb < 1) return hipErrorInvalidValue;
+  const int qg = (qt + a.q_per_wg - 1) / a.q_per_wg;
+  if (a.nb > 1) {
+    // the streaming kernel: up to 3 query tiles a workgroup, chunks of nb spans
+    if (a.q_per_wg > 3) return hipErrorInvalidValue;
+    const dim3 grid((a.max_chunks + a.nb - 1) / a.nb, a.n_kv_heads * qg, a.batch);
+    const int qpw = a.q_per_wg;
+    if (head_dim == 128) {
+      if (qpw == 1) hipLaunchKernelGGL((attn_stream_kernel<128, 1>), grid, dim3(256), 0, s, a);
+      else if (qpw == 2) hipLaunchKernelGGL((attn_stream_kernel<128, 2>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((attn_stream_kernel<128, 3>), grid, dim3(256), 0, s, a);
+    } else {
+      if (qpw == 1) hipLaunchKernelGGL((attn_stream_kernel<64, 1>), grid, dim3(256), 0, s, a);
+      else if (qpw == 2) hipLaunchKernelGGL((attn_stream_kernel<64, 2>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((attn_stream_kernel<64, 3>), grid, dim3(256), 0, s, a);
+    }
+    return hipGetLastError();
+  }
+  const dim3 grid(a.max_chunks, a.n_kv_heads * qg, a.batch);
   const bool multi = a.q_per_wg > 1 && qt > 1;
   if (head_dim == 128) {
     if (multi) hipLaunchKernelGGL((attn_kernel<128, true>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((attn_kernel<128, false>), grid, dim3(256), 0, s, a);
-  } else if (head_dim == 64) {
+  } else {
     if (multi) hipLaunchKernelGGL((attn_kernel<64, true>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((attn_kernel<64, false>), grid, dim3(256), 0, s, a);
-  } else {
-    return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

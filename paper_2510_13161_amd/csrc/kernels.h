@@ -147,6 +147,8 @@ struct AttnArgs {
   int32_t max_chunks;       // 256-key chunks of the longest sequence
   int32_t q_per_wg;         // query tiles a workgroup takes in turn (its K and V
                             // operands loaded once for all of them)
+  int32_t nb;               // 256-key spans per workgroup chunk: 1, or more for the
+                            // streaming kernel (then q_per_wg <= 3)
   float scale;
   Topo topo;
 };

@@ -293,21 +293,90 @@ def test_depth_reduced_14b_chain():
     print("14b L2 chain:", rep)
 
 
-def test_attention_query_tile_groups():
-    """Attention workgroups that take several query tiles in turn: GQA 16/4
-    with head_dim 64 and a 25-slot tree (7 query tiles of the 100 queries per
-    kv head), 4 sequences with contexts up to 4800 (19 key chunks merged
-    across workgroups): 19 x 4 x 4 x 7 workgroups exceed the grouping
-    threshold, so the tiles go 2 per workgroup with a ragged last group."""
-    _torch()
+def _gqa64_tree():
     shape = synth.ModelShape("gqa64", 2, 1024, 16, 4, 64, 2048, 4096, rope_theta=1.0e4)
-    w = synth.Workload("gqa64_tree", shape, 4, (4600, 4800), "tree", 6, branches=4, ee_layer=1,
-                       kappa=4, seed=11)
+    return synth.Workload("gqa64_tree", shape, 4, (4600, 4800), "tree", 6, branches=4, ee_layer=1,
+                          kappa=4, seed=11)
+
+
+def test_attention_query_tile_groups(monkeypatch):
+    """Attention workgroups that take several query tiles in turn (the
+    one-span kernel, forced): GQA 16/4 with head_dim 64 and a 25-slot tree
+    (7 query tiles of the 100 queries per kv head), 4 sequences with contexts
+    up to 4800 (19 key chunks merged across workgroups): 19 x 4 x 4 x 7
+    workgroups exceed the grouping threshold, so the tiles go 2 per
+    workgroup with a ragged last group."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_SPANS", "1")
+    w = _gqa64_tree()
     case = H.GpuCase(w)
     gr = case.run()
     seqs = {b: H.oracle_sequence(case.shape, w, case.si, b) for b in (0, 3)}
     rep = _compare(case, gr, seqs)
     print("query tile groups:", rep)
+
+
+def test_attention_streaming_chosen():
+    """The same workload with the launch shape the library picks: the
+    streaming kernel (19 one-span chunks x 4 kv heads x 4 sequences x 3 tile
+    groups exceed one workgroup per compute unit, so a workgroup walks 4
+    spans with an online softmax), 3 query tiles a workgroup with a ragged
+    last group of 1, head_dim 64, the tree mask in the last span."""
+    _torch()
+    w = _gqa64_tree()
+    case = H.GpuCase(w)
+    gr = case.run()
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b) for b in (0, 3)}
+    rep = _compare(case, gr, seqs)
+    print("streaming attention:", rep)
+
+
+@pytest.mark.parametrize("spans", [2, 3])
+def test_attention_streaming_ragged_batch(monkeypatch, spans):
+    """Streaming kernel forced on a ragged batch (contexts 1 to 1000, one
+    query tile): sequences whose keys fit one chunk of `spans` spans write
+    their output directly, longer ones merge two chunks; waves whose blocks
+    lie past the last key contribute nothing."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_SPANS", str(spans))
+    w = synth.WORKLOADS["14b_batch16"].with_model(synth.TINY, batch=6, ctx=(1, 1000), ee_layer=1, kappa=4,
+                                                  seed=27)
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run()
+    weights = synth.host_weights(case.shape, w.seed)
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b, weights=weights) for b in range(w.batch)}
+    lens = case.si.ctx_len + w.n_slots
+    assert lens.min() <= 256 * spans < lens.max()
+    print("streaming ragged:", _compare(case, gr, seqs))
+
+
+def test_attention_streaming_max_tree(monkeypatch):
+    """Streaming kernel forced on the 64-slot tree (4 query tiles: a group of
+    3 and a group of 1) after a 700-key context: the tree rows straddle two
+    64-key blocks of the last span, so both take the masked path."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_SPANS", "2")
+    w = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, ctx=(700, 700), topology="tree", gamma=9,
+                                                 branches=7, ee_layer=1, kappa=4, seed=29)
+    assert w.n_slots == 64
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    print("streaming max tree:", _compare(case, gr, {0: o}))
+
+
+def test_attention_streaming_14b_widths(monkeypatch):
+    """Streaming kernel forced at 14B widths (head_dim 128, GQA 40/8: 3 query
+    tiles in one group), 2 layers, a 1024-key context in 3 chunks of 2 spans."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_SPANS", "2")
+    w = synth.WORKLOADS["14b_chain"].with_model(synth.QWEN14B)
+    case = H.GpuCase(w, n_layers=2)
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    print("streaming 14b L2 chain:", _compare(case, gr, {0: o}))
 
 
 def test_depth_reduced_66b_tree():
