@@ -57,12 +57,22 @@ def build_synth_dev(verbose: bool = False) -> str:
     return out
 
 
+# Per-source compiler options. gemm.hip: MFMA accumulators in architectural
+# VGPRs. In the accumulator-register form the allocator let the multi-row-tile
+# k-loops write each product to a different register than it read and undo
+# the rotation with ~1.6 register moves per MFMA on every iteration (each
+# waiting for the MFMA before it); in this form those loops have none, and
+# the 3- and 5-row-tile variants fit two waves per SIMD.
+SRC_FLAGS = {"gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+
+
 def build_lib(verbose: bool = False, jobs: int = 8) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
     objs = [os.path.join(BUILD_DIR, os.path.basename(s) + ".o") for s in srcs]
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        futs = [ex.submit(_run, [HIPCC, *HIP_FLAGS, "-c", s, "-o", o], verbose)
+        futs = [ex.submit(_run, [HIPCC, *HIP_FLAGS, *SRC_FLAGS.get(os.path.basename(s), []), "-c", s,
+                                 "-o", o], verbose)
                 for s, o in zip(srcs, objs)]
         for f in futs:
             f.result()

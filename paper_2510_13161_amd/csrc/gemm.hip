@@ -540,6 +540,17 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < JT; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+  // Several row tiles: a wave takes its k-steps from a point rotated by the
+  // tile index, so that workgroups running at the same time read different
+  // k-steps of the activation image, which every workgroup shares (the same
+  // k-step requested by every CU at once would queue on a few L2 channels).
+  // The order is fixed per tile: sums stay bit-reproducible.
+  const int rot = MT > 1 && n > 0 ? (int)((int64_t)n * (t & 15) / 16) : 0;
+  auto kstep = [&](int i) {
+    if constexpr (MT == 1) return kb + i;
+    const int x = i + rot;
+    return kb + (x >= n ? x - n : x);
+  };
   KStep<MT, JT> st[D];
   auto issue = [&](KStep<MT, JT>& x, int k) {
 #pragma unroll
@@ -566,20 +577,20 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   // batch and a short run (n < D: every load issued up front) come after.
   if (n >= D) {
 #pragma unroll
-    for (int d = 0; d < D; ++d) issue(st[d], kb + d);
+    for (int d = 0; d < D; ++d) issue(st[d], kstep(d));
     const int nfull = (n - D) / D;
     for (int b = 0; b < nfull; ++b) {
 #pragma unroll
       for (int d = 0; d < D; ++d) {
         compute(st[d]);
-        issue(st[d], kb + (b + 1) * D + d);
+        issue(st[d], kstep((b + 1) * D + d));
       }
     }
     const int done = (nfull + 1) * D, r = n - done;  // 0 <= r < D steps left after this batch
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       compute(st[d]);
-      if (d < r) issue(st[d], kb + done + d);
+      if (d < r) issue(st[d], kstep(done + d));
     }
 #pragma unroll
     for (int d = 0; d < D; ++d)
@@ -587,7 +598,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   } else {
 #pragma unroll
     for (int d = 0; d < D; ++d)
-      if (d < n) issue(st[d], kb + d);
+      if (d < n) issue(st[d], kstep(d));
 #pragma unroll
     for (int d = 0; d < D; ++d)
       if (d < n) compute(st[d]);
