@@ -21,6 +21,11 @@
 // their partials with coherent stores and the last chunk of the (sequence,
 // kv head, query tile) to arrive merges all of them in chunk order. All
 // statistics in fp32; no floating-point atomics: bit-reproducible.
+//
+// Long contexts (grids of one-span chunks larger than the chip holds at
+// once): attn_stream_kernel, where a workgroup walks several 256-key spans
+// with an online softmax and streams its next block while it computes; the
+// merges above run once per chunk of spans.
 #include "kernels.h"
 
 namespace msd {
