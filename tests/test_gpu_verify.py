@@ -379,6 +379,25 @@ def test_attention_streaming_14b_widths(monkeypatch):
     print("streaming 14b L2 chain:", _compare(case, gr, {0: o}))
 
 
+def test_streaming_attention_is_deterministic(monkeypatch):
+    """Two steps over the same inputs through the streaming attention kernel
+    (forced, 3 spans a chunk, ragged contexts: direct writes and two-chunk
+    merges, the lazily moved softmax reference) give bit-identical outputs."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_SPANS", "3")
+    w = synth.WORKLOADS["14b_batch16"].with_model(synth.TINY, batch=6, ctx=(1, 1000), ee_layer=1, kappa=4,
+                                                  seed=27)
+    case = H.GpuCase(w)
+    case.reset_len()
+    a = case.run(commit=False)
+    case.reset_len()
+    b = case.run(commit=False)
+    assert np.array_equal(a.logits, b.logits)
+    assert np.array_equal(a.ee_logp, b.ee_logp) and np.array_equal(a.ee_ids, b.ee_ids)
+    for l in range(case.shape.n_layers):
+        assert np.array_equal(a.k_rows[l], b.k_rows[l]) and np.array_equal(a.v_rows[l], b.v_rows[l])
+
+
 def test_depth_reduced_66b_tree():
     """66B widths (MHA 72 heads, LayerNorm, learned positions, ReLU, biases, tied head), 2 layers."""
     _torch()
