@@ -476,11 +476,12 @@ __device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
 // tile loaded ahead (MT == 1); otherwise each row tile loads its own here.
 template <int MT, int EPI, int JT>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, int t, const floatx4 (&acc)[MT][JT],
-                                         float* scr, const EpiIn& in1) {
+                                         float* scr, const EpiIn& in1, int owner = 0, int owners = 1) {
   // unrolled: a runtime row-tile index into acc would make the compiler keep
   // the whole accumulator array in scratch memory, k-loop included
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
+    if (owners > 1 && mt % owners != owner) continue;  // another wave's row tile
     EpiIn inl;
     if constexpr (MT > 1) {
       if constexpr (EPI == EPI_QKV) inl.L = row_len(a, 16 * mt + (threadIdx.x & 15));
@@ -512,7 +513,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   constexpr int RCH = MT < 3 ? MT : 3;  // row tiles per LDS reduction round
   constexpr int TF = MT * JT * 256;     // floats of one tile's partial
   __shared__ floatx4 red[NW][RCH * JT][kWave];
-  __shared__ __attribute__((aligned(16))) float scr[16 * kScr];
+  // epilogue scratch: one region, or one a wave when the waves share the row
+  // tiles' epilogues
+  __shared__ __attribute__((aligned(16))) float scr_all[(MT == 1 ? 1 : NW) * 16 * kScr];
+  __shared__ int last_sh;
 
   const int lane = threadIdx.x & 63;
   // wave-uniform (scalar) so that the k-loop branches and waits are scalar
@@ -608,8 +612,83 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
     if (wave == 0) epi_load<EPI>(a, t, 0, in1);
   }
 
-  // fixed-order sum of the waves' tiles
-  if constexpr (NW > 1) {
+  if constexpr (MT == 1) {
+    // fixed-order sum of the waves' tiles
+    if constexpr (NW > 1) {
+      for (int m0 = 0; m0 < MT; m0 += RCH) {
+  #pragma unroll
+        for (int c = 0; c < RCH; ++c)
+          if (m0 + c < MT)
+  #pragma unroll
+            for (int j = 0; j < JT; ++j) red[wave][c * JT + j][lane] = acc[m0 + c][j];
+        __syncthreads();
+        if (wave == 0) {
+  #pragma unroll
+          for (int c = 0; c < RCH; ++c)
+            if (m0 + c < MT)
+  #pragma unroll
+              for (int j = 0; j < JT; ++j) {
+                floatx4 v = red[0][c * JT + j][lane];
+  #pragma unroll
+                for (int w = 1; w < NW; ++w) v += red[w][c * JT + j][lane];
+                acc[m0 + c][j] = v;
+              }
+        }
+        __syncthreads();
+      }
+      if (wave != 0) return;
+    }
+
+    if (a.splits > 1) {
+      // publish this split's tile; the last split to arrive sums all of them
+      // (the tile's partials: [splits][TF] floats, lane l's 4 values at 4 l)
+      const __amdgpu_buffer_rsrc_t part =
+          coherent_region(a.partial + (size_t)t * a.splits * TF, (uint32_t)(a.splits * TF * 4));
+  #pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+  #pragma unroll
+        for (int j = 0; j < JT; ++j)
+          store_coherent4(part, (uint32_t)((s * TF + (mt * JT + j) * 256 + lane * 4) * 4), acc[mt][j]);
+      drain_stores();
+      int old = 0;
+      if (lane == 0) old = counter_add(&a.counters[t], 1);
+      old = __shfl(old, 0);
+      if (old != a.splits - 1) return;
+  #pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+  #pragma unroll
+        for (int j = 0; j < JT; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int sp0 = 0; sp0 < a.splits; sp0 += 2) {
+        // two splits' tiles in flight, summed in split order
+        floatx4 pv[2][MT][JT];
+  #pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int sp = sp0 + u < a.splits ? sp0 + u : sp0;
+  #pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+  #pragma unroll
+            for (int j = 0; j < JT; ++j)
+              pv[u][mt][j] = load_coherent4(part, (uint32_t)((sp * TF + (mt * JT + j) * 256 + lane * 4) * 4));
+        }
+  #pragma unroll
+        for (int u = 0; u < 2; ++u)
+          if (sp0 + u < a.splits)
+  #pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+  #pragma unroll
+              for (int j = 0; j < JT; ++j) acc[mt][j] += pv[u][mt][j];
+      }
+      if (lane == 0) counter_reset(&a.counters[t]);
+    }
+
+    epilogue<MT, EPI, JT>(a, t, acc, scr_all, in1);
+  } else {
+    // Several row tiles: row tile mt belongs to wave mt % NW, which sums it
+    // over the waves (in wave order, as above) and finishes it, so that the
+    // row tiles' hand-offs and epilogues run on all waves at once instead of
+    // one after another on wave 0.
+    auto mine = [&](int mt) { return mt % NW == wave; };
+#pragma unroll
     for (int m0 = 0; m0 < MT; m0 += RCH) {
 #pragma unroll
       for (int c = 0; c < RCH; ++c)
@@ -617,66 +696,60 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 #pragma unroll
           for (int j = 0; j < JT; ++j) red[wave][c * JT + j][lane] = acc[m0 + c][j];
       __syncthreads();
-      if (wave == 0) {
 #pragma unroll
-        for (int c = 0; c < RCH; ++c)
-          if (m0 + c < MT)
+      for (int c = 0; c < RCH; ++c)
+        if (m0 + c < MT && mine(m0 + c))
 #pragma unroll
-            for (int j = 0; j < JT; ++j) {
-              floatx4 v = red[0][c * JT + j][lane];
+          for (int j = 0; j < JT; ++j) {
+            floatx4 v = red[0][c * JT + j][lane];
 #pragma unroll
-              for (int w = 1; w < NW; ++w) v += red[w][c * JT + j][lane];
-              acc[m0 + c][j] = v;
-            }
-      }
+            for (int w = 1; w < NW; ++w) v += red[w][c * JT + j][lane];
+            acc[m0 + c][j] = v;
+          }
       __syncthreads();
     }
-    if (wave != 0) return;
-  }
-
-  if (a.splits > 1) {
-    // publish this split's tile; the last split to arrive sums all of them
-    // (the tile's partials: [splits][TF] floats, lane l's 4 values at 4 l)
-    const __amdgpu_buffer_rsrc_t part =
-        coherent_region(a.partial + (size_t)t * a.splits * TF, (uint32_t)(a.splits * TF * 4));
+    if (a.splits > 1) {
+      // each wave publishes its row tiles of this split's tile; the
+      // workgroup arrives once; the last split to arrive sums all of them
+      // in split order, each wave its own row tiles
+      const __amdgpu_buffer_rsrc_t part =
+          coherent_region(a.partial + (size_t)t * a.splits * TF, (uint32_t)(a.splits * TF * 4));
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int j = 0; j < JT; ++j)
-        store_coherent4(part, (uint32_t)((s * TF + (mt * JT + j) * 256 + lane * 4) * 4), acc[mt][j]);
-    drain_stores();
-    int old = 0;
-    if (lane == 0) old = counter_add(&a.counters[t], 1);
-    old = __shfl(old, 0);
-    if (old != a.splits - 1) return;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int j = 0; j < JT; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int sp0 = 0; sp0 < a.splits; sp0 += 2) {
-      // two splits' tiles in flight, summed in split order
-      floatx4 pv[2][MT][JT];
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int sp = sp0 + u < a.splits ? sp0 + u : sp0;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
+        if (mine(mt))
 #pragma unroll
           for (int j = 0; j < JT; ++j)
-            pv[u][mt][j] = load_coherent4(part, (uint32_t)((sp * TF + (mt * JT + j) * 256 + lane * 4) * 4));
+            store_coherent4(part, (uint32_t)((s * TF + (mt * JT + j) * 256 + lane * 4) * 4), acc[mt][j]);
+      drain_stores();
+      __syncthreads();
+      if (threadIdx.x == 0) last_sh = counter_add(&a.counters[t], 1) == a.splits - 1;
+      __syncthreads();
+      if (!last_sh) return;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        if (!mine(mt)) continue;
+#pragma unroll
+        for (int j = 0; j < JT; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int sp0 = 0; sp0 < a.splits; sp0 += 2) {
+          floatx4 pv[2][JT];
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const int sp = sp0 + u < a.splits ? sp0 + u : sp0;
+#pragma unroll
+            for (int j = 0; j < JT; ++j)
+              pv[u][j] = load_coherent4(part, (uint32_t)((sp * TF + (mt * JT + j) * 256 + lane * 4) * 4));
+          }
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+            if (sp0 + u < a.splits)
+#pragma unroll
+              for (int j = 0; j < JT; ++j) acc[mt][j] += pv[u][j];
+        }
       }
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-        if (sp0 + u < a.splits)
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int j = 0; j < JT; ++j) acc[mt][j] += pv[u][mt][j];
+      if (threadIdx.x == 0) counter_reset(&a.counters[t]);
     }
-    if (lane == 0) counter_reset(&a.counters[t]);
+    epilogue<MT, EPI, JT>(a, t, acc, scr_all + wave * 16 * kScr, in1, wave, NW);
   }
-
-  epilogue<MT, EPI, JT>(a, t, acc, scr, in1);
 }
 
 template <int MT, int NW, int EPI, int JT>
