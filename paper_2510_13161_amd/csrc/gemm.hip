@@ -472,31 +472,58 @@ __device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
   }
 }
 
-// The epilogue of the finished tile. in1 holds the inputs of a single row
-// tile loaded ahead (MT == 1); otherwise each row tile loads its own here.
+// The epilogue of row tile mt of a finished tile; `in` holds its inputs
+// when they were loaded ahead (one row tile), otherwise they are loaded here.
+template <int EPI, int JT, bool AHEAD>
+__device__ __forceinline__ void epilogue_tile(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[JT],
+                                              float* scr, const EpiIn& in1) {
+  EpiIn inl;
+  if constexpr (!AHEAD) {
+    if constexpr (EPI == EPI_QKV) inl.L = row_len(a, 16 * mt + (threadIdx.x & 15));
+    epi_load<EPI>(a, t, mt, inl);
+  }
+  const EpiIn& in = AHEAD ? in1 : inl;
+  float mu = 0.0f, rs = 1.0f;
+  if constexpr (has_norm<EPI>()) norm_finish(a, in, mu, rs);
+  if constexpr (EPI == EPI_SWIGLU) epi_swiglu<JT>(a, t, mt, acc, scr, mu, rs);
+  else if constexpr (EPI == EPI_HEAD) epi_head<JT>(a, t, mt, acc, mu, rs);
+  else if constexpr (JT == 4) {  // the other epilogues run on 64-column tiles only
+    if constexpr (EPI == EPI_RESID) epi_resid(a, t, mt, acc, scr, in);
+    else if constexpr (EPI == EPI_QKV) epi_qkv(a, t, mt, acc, mu, rs, in);
+    else epi_relu(a, t, mt, acc, scr, mu, rs);
+  }
+}
+
+// The epilogues of the row tiles a wave owns (row tile mt belongs to wave
+// mt % owners). At 9 row tiles one copy of the per-tile code runs in a loop
+// (unrolled, the 9 copies made the kernel 3.8 times larger and slower by a
+// little); each pass picks its row tile's accumulators by compile-time
+// index, so acc is never indexed at run time (that would put it in scratch
+// memory).
 template <int MT, int EPI, int JT>
-__device__ __forceinline__ void epilogue(const GemmArgs& a, int t, const floatx4 (&acc)[MT][JT],
-                                         float* scr, const EpiIn& in1, int owner = 0, int owners = 1) {
-  // unrolled: a runtime row-tile index into acc would make the compiler keep
-  // the whole accumulator array in scratch memory, k-loop included
+__device__ __forceinline__ void epilogue_rows(const GemmArgs& a, int t, const floatx4 (&acc)[MT][JT],
+                                              float* scr, int owner, int owners) {
+  if constexpr (MT <= 5) {
+    // up to 5 row tiles: unrolled (the compact loop below costs these
+    // variants their second wave per SIMD)
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    if (owners > 1 && mt % owners != owner) continue;  // another wave's row tile
-    EpiIn inl;
-    if constexpr (MT > 1) {
-      if constexpr (EPI == EPI_QKV) inl.L = row_len(a, 16 * mt + (threadIdx.x & 15));
-      epi_load<EPI>(a, t, mt, inl);
+    for (int mt = 0; mt < MT; ++mt) {
+      if (mt % owners != owner) continue;
+      EpiIn none;
+      epilogue_tile<EPI, JT, false>(a, t, mt, acc[mt], scr, none);
     }
-    const EpiIn& in = MT == 1 ? in1 : inl;
-    float mu = 0.0f, rs = 1.0f;
-    if constexpr (has_norm<EPI>()) norm_finish(a, in, mu, rs);
-    if constexpr (EPI == EPI_SWIGLU) epi_swiglu<JT>(a, t, mt, acc[mt], scr, mu, rs);
-    else if constexpr (EPI == EPI_HEAD) epi_head<JT>(a, t, mt, acc[mt], mu, rs);
-    else if constexpr (JT == 4) {  // the other epilogues run on 64-column tiles only
-      if constexpr (EPI == EPI_RESID) epi_resid(a, t, mt, acc[mt], scr, in);
-      else if constexpr (EPI == EPI_QKV) epi_qkv(a, t, mt, acc[mt], mu, rs, in);
-      else epi_relu(a, t, mt, acc[mt], scr, mu, rs);
-    }
+    return;
+  }
+#pragma clang loop unroll(disable)
+  for (int mt = owner; mt < MT; mt += owners) {
+    floatx4 cur[JT];
+#pragma unroll
+    for (int mm = 0; mm < MT; ++mm)
+      if (mm == mt)
+#pragma unroll
+        for (int j = 0; j < JT; ++j) cur[j] = acc[mm][j];
+    EpiIn none;
+    epilogue_tile<EPI, JT, false>(a, t, mt, cur, scr, none);
   }
 }
 
@@ -681,7 +708,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
       if (lane == 0) counter_reset(&a.counters[t]);
     }
 
-    epilogue<MT, EPI, JT>(a, t, acc, scr_all, in1);
+    epilogue_tile<EPI, JT, true>(a, t, 0, acc[0], scr_all, in1);
   } else {
     // Several row tiles: row tile mt belongs to wave mt % NW, which sums it
     // over the waves (in wave order, as above) and finishes it, so that the
@@ -748,7 +775,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
       }
       if (threadIdx.x == 0) counter_reset(&a.counters[t]);
     }
-    epilogue<MT, EPI, JT>(a, t, acc, scr_all + wave * 16 * kScr, in1, wave, NW);
+    epilogue_rows<MT, EPI, JT>(a, t, acc, scr_all + wave * 16 * kScr, wave, NW);
   }
 }
 
