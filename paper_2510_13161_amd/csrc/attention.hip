@@ -196,38 +196,61 @@ __device__ __forceinline__ void merge_chunks(const AttnArgs& a, int* last, int32
   if (tid == 0) *last = counter_add(ctr, 1) == nch - 1;
   __syncthreads();
   if (!*last) return;
-  constexpr int MB = 8;  // chunk partials in flight per merge round
-  for (int x = tid; x < (qt1 - qt0) * 16 * C4; x += blockDim.x) {
-    const int qloc = x / C4, c4 = x - qloc * C4;
-    const int qg = qt0 * 16 + qloc;
-    if (qg >= Qn) continue;
-    float M = -INFINITY, S = 0.0f, o4[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int c0 = 0; c0 < nch; c0 += MB) {
-      float2 ml[MB];
-      floatx4 v[MB];
+  constexpr int MB = 8;  // chunk partials in flight per item and merge round
+  constexpr int IT = 2;  // items of a thread whose loads are in flight together
+  const int n_items = (qt1 - qt0) * 16 * C4;
+  for (int x0 = tid; x0 < n_items; x0 += IT * blockDim.x) {
+    int qg[IT], c4[IT];
+    bool ok[IT];
+    float M[IT], S[IT], o4[IT][4];
 #pragma unroll
-      for (int u = 0; u < MB; ++u) {
-        const int cc = c0 + u < nch ? c0 + u : c0;
-        const size_t pidx = (pbase + cc) * Qn + qg;
-        ml[u] = load_coherent2(a.part_ml + 2 * pidx);
-        v[u] = load_coherent4(pco, (uint32_t)((((size_t)cc * Qn + qg) * HD + 4 * c4) * 4));
-      }
+    for (int i = 0; i < IT; ++i) {
+      const int x = x0 + i * blockDim.x;
+      const int qloc = x / C4;
+      c4[i] = x - qloc * C4;
+      qg[i] = qt0 * 16 + qloc;
+      ok[i] = x < n_items && qg[i] < Qn;
+      if (!ok[i]) qg[i] = 0, c4[i] = 0;  // loads stay in bounds; results unused
+      M[i] = -INFINITY;
+      S[i] = 0.0f;
 #pragma unroll
-      for (int u = 0; u < MB; ++u) {
-        if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
-        const float Mn = fmaxf(M, ml[u].x);
-        const float fa = M == -INFINITY ? 0.0f : exp2_hw(M - Mn);
-        const float fb = exp2_hw(ml[u].x - Mn);
-        S = S * fa + ml[u].y * fb;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o4[e] = o4[e] * fa + v[u][e] * fb;
-        M = Mn;
-      }
+      for (int e = 0; e < 4; ++e) o4[i][e] = 0.0f;
     }
-    const float inv = S > 0.0f ? 1.0f / S : 0.0f;
+    for (int c0 = 0; c0 < nch; c0 += MB) {
+      float2 ml[IT][MB];
+      floatx4 v[IT][MB];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o4[e] *= inv;
-    write_out4<HD>(a, b, kvh, qg, c4, o4);
+      for (int i = 0; i < IT; ++i)
+#pragma unroll
+        for (int u = 0; u < MB; ++u) {
+          const int cc = c0 + u < nch ? c0 + u : c0;
+          const size_t pidx = (pbase + cc) * Qn + qg[i];
+          ml[i][u] = load_coherent2(a.part_ml + 2 * pidx);
+          v[i][u] = load_coherent4(pco, (uint32_t)((((size_t)cc * Qn + qg[i]) * HD + 4 * c4[i]) * 4));
+        }
+#pragma unroll
+      for (int i = 0; i < IT; ++i)
+#pragma unroll
+        for (int u = 0; u < MB; ++u) {
+          if (c0 + u >= nch || ml[i][u].x == -INFINITY) continue;
+          const float Mn = fmaxf(M[i], ml[i][u].x);
+          const float fa = M[i] == -INFINITY ? 0.0f : exp2_hw(M[i] - Mn);
+          const float fb = exp2_hw(ml[i][u].x - Mn);
+          S[i] = S[i] * fa + ml[i][u].y * fb;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o4[i][e] = o4[i][e] * fa + v[i][u][e] * fb;
+          M[i] = Mn;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      if (!ok[i]) continue;
+      const float inv = S[i] > 0.0f ? 1.0f / S[i] : 0.0f;
+      float out[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) out[e] = o4[i][e] * inv;
+      write_out4<HD>(a, b, kvh, qg[i], c4[i], out);
+    }
   }
   if (tid == 0) counter_reset(ctr);
 }
@@ -351,17 +374,30 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
         sc[j] = mfma16x16x32(kf[j][kk], ql[kk], sc[j]);
       }
     }
-    // lane holds S^T[key 16j + 4g + r][query r16]: scale (base 2), mask, softmax
+    // lane holds S^T[key 16j + 4g + r][query r16]: scale (base 2), mask (a
+    // block wholly inside the cached context is visible to every query: a
+    // branch the whole wave takes; otherwise without branches), softmax
     float mx = -INFINITY;
+    if (k0 + 64 <= L) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int pos = k0 + 16 * j + 4 * g + r;
-        const bool vis = pos < key_hi && (pos < L || ((anc >> (pos - L)) & 1ull));
-        sc[j][r] = vis ? sc[j][r] * scale2 : -INFINITY;
-        mx = fmaxf(mx, sc[j][r]);
-      }
+        for (int r = 0; r < 4; ++r) {
+          sc[j][r] *= scale2;
+          mx = fmaxf(mx, sc[j][r]);
+        }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int pos = k0 + 16 * j + 4 * g + r;
+          const bool anc_bit = (anc >> ((pos - L) & 63)) & 1ull;
+          const bool vis = (pos < key_hi) & ((pos < L) | anc_bit);
+          sc[j][r] = vis ? sc[j][r] * scale2 : -INFINITY;
+          mx = fmaxf(mx, sc[j][r]);
+        }
+    }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float mref = mx == -INFINITY ? 0.0f : mx;
