@@ -367,6 +367,22 @@ def test_attention_streaming_max_tree(monkeypatch):
     print("streaming max tree:", _compare(case, gr, {0: o}))
 
 
+def test_attention_streaming_two_query_tiles(monkeypatch):
+    """Streaming kernel forced with two query tiles a workgroup: the 25-slot
+    tree (4 x 6) at one query head per kv head is 2 query tiles, after a
+    900-key context (3 chunks of 2 spans; the tree rows in the last span,
+    under the tree mask), in rejection mode."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_SPANS", "2")
+    w = synth.WORKLOADS["14b_tree"].with_model(synth.TINY, ee_layer=1, kappa=4, seed=37, ctx=(900, 900))
+    assert (w.model.n_heads // w.model.n_kv_heads * w.n_slots + 15) // 16 == 2
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    print("streaming two query tiles:", _compare(case, gr, {0: o}))
+
+
 def test_attention_streaming_14b_widths(monkeypatch):
     """Streaming kernel forced at 14B widths (head_dim 128, GQA 40/8: 3 query
     tiles in one group), 2 layers, a 1024-key context in 3 chunks of 2 spans."""
