@@ -425,6 +425,20 @@ def test_depth_reduced_66b_tree():
     print("66b L2 tree:", rep)
 
 
+def test_depth_reduced_66b_chain():
+    """66B widths on a 9-slot chain (one row tile), 2 layers: the QKV (432
+    tiles) and ReLU up (576 tiles) projections run whole-K 4-wave
+    workgroups, the narrow ones 8-wave split-K workgroups, the tied head
+    4-wave workgroups over 786 tiles (the last one partial)."""
+    _torch()
+    w = synth.WORKLOADS["66b_tree"].with_model(synth.OPT66B, topology="chain", gamma=8, branches=1, seed=41)
+    assert w.n_slots == 9
+    case = H.GpuCase(w, n_layers=2)
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    print("66b L2 chain:", _compare(case, gr, {0: o}))
+
+
 def test_step_is_deterministic(tiny_case):
     case = tiny_case
     case.si = synth.step_inputs(case.w)
