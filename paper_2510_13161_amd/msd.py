@@ -284,8 +284,9 @@ def make_block(tokens: torch.Tensor, parent=None) -> Block:
     """tokens: device int32 [batch][n_slots]; parent: host sequence or None (chain)."""
     assert tokens.dtype == torch.int32 and tokens.dim() == 2
     b = Block(tokens.shape[0], tokens.shape[1], _ptr(tokens), None)
+    b._keep = (tokens,)  # the block holds only the address: keep the tensor alive with it
     if parent is not None:
         arr = (ctypes.c_int32 * len(parent))(*[int(p) for p in parent])
         b.parent = ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32))
-        b._keep = arr
+        b._keep = (tokens, arr)
     return b

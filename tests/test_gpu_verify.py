@@ -451,6 +451,72 @@ def test_step_is_deterministic(tiny_case):
     assert np.array_equal(a.k_rows[0], b.k_rows[0])
 
 
+def test_step_replays_under_graph_capture():
+    """verify + accept (rejection, a 16-slot tree) captured in one HIP graph:
+    neither allocates, clears memory with a memset or waits on the host, so
+    every replay, each after an eager step on outputs of its own and with the
+    graph's outputs poisoned, matches the eager step bit for bit."""
+    torch = _torch()
+    from paper_2510_13161_amd import msd
+    w = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, ctx=(300, 300), topology="tree", gamma=5,
+                                                 branches=3, ee_layer=1, kappa=4, seed=43,
+                                                 mode="rejection")
+    case = H.GpuCase(w)
+    case.reset_len()
+    si, dev = case.si, "cuda"
+    B, n, V, M = w.batch, w.n_slots, case.shape.vocab, w.batch * w.n_slots
+    # a temporary tokens tensor: the block keeps it alive (the allocations
+    # below would otherwise reuse its memory)
+    blk = msd.make_block(torch.from_numpy(si.tokens).to(dev), si.parent)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    cid, cq, ua, us = t(si.cand_ids), t(si.cand_q), t(si.u_accept), t(si.u_sample)
+    smp = msd.Sampling(msd.MODES["rejection"], float(w.temperature), si.cand_ids.shape[-1],
+                       cid.data_ptr(), cq.data_ptr(), ua.data_ptr(), us.data_ptr())
+    nb = msd.workspace_bytes(case.model.handle, B, n, w.kappa, case.capacity)
+    ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+
+    def outputs():
+        e = lambda shape, dt: torch.empty(shape, dtype=dt, device=dev)
+        return dict(logits=e((M, V), torch.float32), argmax=e(M, torch.int32), lse=e(M, torch.float32),
+                    ids=e((M, w.kappa), torch.int32), logp=e((M, w.kappa), torch.float32),
+                    acc=e(B, torch.int32), nxt=e(B, torch.int32), path=e((B, n), torch.int32))
+
+    def step(o):
+        req = msd.EERequest(w.ee_layer, w.kappa, o["ids"].data_ptr(), o["logp"].data_ptr(), None)
+        msd.verify_block(case.model.handle, case.cache.c, blk, req, o["logits"], o["argmax"], o["lse"], ws)
+        msd.accept(case.model.handle, blk, o["logits"], o["argmax"], smp, o["acc"], o["nxt"], o["path"],
+                   case.cache.status)
+
+    ref = outputs()
+    step(ref)
+    cap = outputs()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(cap)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(cap)
+    torch.cuda.synchronize()
+    for r in range(3):
+        for v in cap.values():
+            v.fill_(-7)
+        eager = outputs()
+        step(eager)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in ref:
+            assert torch.equal(eager[k], ref[k]), ("eager", r, k)
+            assert torch.equal(cap[k], ref[k]), ("replay", r, k)
+    assert int(case.cache.status.item()) == 0
+    gr = case.run(commit=False)  # the harness's own step, tokens held by the harness
+    assert np.array_equal(gr.logits, ref["logits"].cpu().numpy())
+    print("graph replays bit-identical; A =", ref["acc"].tolist())
+
+
 # ---------------------------------------------------------------------------
 # full-depth workloads (the shapes the benchmark times)
 # ---------------------------------------------------------------------------
