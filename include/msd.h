@@ -25,9 +25,15 @@
  *  - Every pointer marked "device" is HIP device memory owned by the caller;
  *    "host" pointers are read during the call only. The library never takes
  *    ownership of caller memory; it allocates device memory only in
- *    msd_model_create (a small rotary table) and never per call.
+ *    msd_model_create (the rotary table; for LayerNorm models the column
+ *    sums of the matrices that consume a LayerNorm output; a staging buffer
+ *    for the weight rearrangement, freed before it returns) and never per
+ *    call.
  *  - All work is enqueued asynchronously on the caller's `stream`; nothing
- *    blocks, nothing throws across the ABI. Calls are graph-capturable.
+ *    blocks, nothing throws across the ABI. The per-step calls (everything
+ *    but msd_model_create / msd_model_destroy) allocate nothing, issue no
+ *    memset and never wait on the host, so they can be captured in a HIP
+ *    graph; msd_model_create synchronises the device and cannot.
  *  - Host-checkable errors (NULL pointers, sizes out of range, topology that
  *    is not a forest in slot order, workspace too small) return a negative
  *    msd_status and enqueue nothing; msd_last_error() then describes it.
