@@ -224,6 +224,7 @@ enum { MSD_GREEDY = 0, MSD_REJECTION = 1, MSD_MATCH = 2 };
  * child this is Leviathan et al. 2023; it leaves the target law intact.
  * MATCH: the paper's sample-and-compare (Sec. 3.1, App. B): y is drawn from p
  * with u_sample[node]; descend to the child carrying y, else y is next.
+ * tol_logit: logit tolerance of the near-tie flags (any mode; >= 0).
  */
 typedef struct {
   int32_t mode;
@@ -233,6 +234,7 @@ typedef struct {
   const float* cand_q;      /* device [batch][n_slots][n_cand], rows sum 1 */
   const float* u_accept;    /* device [batch][n_slots] in [0, 1)           */
   const float* u_sample;    /* device [batch][n_slots] in [0, 1)           */
+  float tol_logit;
 } msd_sampling;
 
 /*
@@ -241,14 +243,24 @@ typedef struct {
  *  next_tok device int32 [batch]  correction (mismatch) or bonus token
  *  path     device int32 [batch][n_slots]; path[b][r] = slot accepted at depth r,
  *           path[b][0] = 0; entries after A_b are -1
+ *  near_tie device uint8 [batch] or NULL: 1 when some decision of the walk
+ *           lies where a logit error of tol_logit could flip it, else 0.
+ *           Bands: GREEDY, a visited row whose top-1 minus top-2 logit is
+ *           below 2 tol; REJECTION, an accept test with |u - alpha| <
+ *           2 tol alpha / T; an inverse-CDF draw (REJECTION, MATCH) with
+ *           |u - c| < 4 tol min(c, 1 - c) at either edge c (cumulative
+ *           fraction) of the drawn id's bin. tol is sampling->tol_logit (0
+ *           when sampling is NULL: nothing is flagged); GREEDY flags read
+ *           logits.
  * GREEDY reads argmax only (children tried in slot order); the stochastic
  * modes read logits (fp32 [M][vocab]). sampling may be NULL for GREEDY.
- * status: device word for MSD_DEV_CANDIDATE, may be NULL.
+ * status: device word for MSD_DEV_CANDIDATE, may be NULL for GREEDY and MATCH.
+ * ws / ws_bytes are unused (NULL / 0 allowed).
  */
 msd_status msd_accept(const msd_model* model, const msd_block* block, const float* logits,
                       const int32_t* argmax, const msd_sampling* sampling, int32_t* acc_len,
-                      int32_t* next_tok, int32_t* path, uint32_t* status, void* ws,
-                      size_t ws_bytes, hipStream_t stream);
+                      int32_t* next_tok, int32_t* path, uint8_t* near_tie, uint32_t* status,
+                      void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Commit / rollback (Sec. 2): for every layer, row len[b] + path[b][r] of

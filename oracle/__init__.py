@@ -74,7 +74,7 @@ def lib():
         L.msdo_head.argtypes = [P, P, i32, P, P]
         L.msdo_topk.argtypes = [i32, i32, P, i32, P, P, P]
         L.msdo_accept.argtypes = [i32, P, P, i32, P, i32, ctypes.c_double, i32, P, P, P, P,
-                                  P, P, P]
+                                  ctypes.c_double, P, P, P, P, P]
         L.msdo_accept.restype = i32
         L.msdo_kv_commit.argtypes = [i32, i32, i32, i32, P, P, i32, i32, P]
         L.msdo_kv_commit.restype = i32
@@ -252,7 +252,13 @@ class Oracle:
 
     @staticmethod
     def accept(parent, tokens, logits, mode="greedy", temperature=1.0, cand_ids=None,
-               cand_q=None, u_accept=None, u_sample=None):
+               cand_q=None, u_accept=None, u_sample=None, tol_logit: float = 0.0,
+               return_tie: bool = False):
+        """App. B acceptance over one sequence's block: (A, next token, path).
+        With return_tie, also (tie_depth, tie_next): the depth of the first
+        node where a decision choosing the way down lies in a near-tie band
+        of tol_logit (-1 if none), and whether the decision that produced the
+        next token does (bands in msdo.c)."""
         parent = np.ascontiguousarray(parent, dtype=np.int32)
         tokens = np.ascontiguousarray(tokens, dtype=np.int32)
         logits = np.ascontiguousarray(logits, dtype=np.float64)
@@ -265,13 +271,18 @@ class Oracle:
         u_sample = None if u_sample is None else np.ascontiguousarray(u_sample, dtype=np.float32)
         A = np.zeros(1, dtype=np.int32)
         nxt = np.zeros(1, dtype=np.int32)
+        tie = np.zeros(1, dtype=np.int32)
+        tie_next = np.zeros(1, dtype=np.int32)
         path = np.zeros(n + 1, dtype=np.int32)
         rc = lib().msdo_accept(n, _p(parent), _p(tokens), V, _p(logits), md, float(temperature),
                                n_cand, _p(cand_ids), _p(cand_q), _p(u_accept), _p(u_sample),
-                               _p(A), _p(nxt), _p(path))
+                               float(tol_logit), _p(A), _p(nxt), _p(path), _p(tie),
+                               _p(tie_next))
         if rc != 0:
             raise ValueError("draft token outside its parent's candidate set")
         a = int(A[0])
+        if return_tie:
+            return a, int(nxt[0]), path[:a + 1].copy(), int(tie[0]), bool(tie_next[0])
         return a, int(nxt[0]), path[:a + 1].copy()
 
     @staticmethod
@@ -287,11 +298,13 @@ class Oracle:
     # -- brute force ----------------------------------------------------------------
     def decode_greedy(self, root_token: int, start_pos: int, steps: int,
                       ctx: Optional[Callable[[int], Tuple[np.ndarray, np.ndarray]]] = None,
-                      n_ctx: int = 0):
+                      n_ctx: int = 0, return_kv: bool = False):
         """Token-by-token argmax decoding (Sec. 2 AR factorisation) from a root.
 
         Returns the tokens y_1..y_steps and the per-step logits; every step is
         a one-row forward whose earlier rows are committed as extra cache rows.
+        With return_kv, also the rows each step wrote: per layer fp64
+        [steps][n_kv_heads][head_dim] keys and values (row s at start_pos + s).
         """
         L = self.m.n_layers
         extra_k: List[List[np.ndarray]] = [[] for _ in range(L)]
@@ -312,7 +325,12 @@ class Oracle:
             tok = int(np.argmax(z))
             out.append(tok)
             all_logits.append(z)
-        return np.array(out, dtype=np.int32), np.stack(all_logits)
+        y, zs = np.array(out, dtype=np.int32), np.stack(all_logits)
+        if return_kv:
+            ks = [np.concatenate(extra_k[l], 0) for l in range(L)]
+            vs = [np.concatenate(extra_v[l], 0) for l in range(L)]
+            return y, zs, ks, vs
+        return y, zs
 
 
 def depths(parent: np.ndarray) -> np.ndarray:

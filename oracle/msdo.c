@@ -313,8 +313,9 @@ void msdo_topk(int32_t n, int32_t V, const double* logits, int32_t kappa, int32_
 }
 
 /* Inverse-CDF draw: the smallest id k with sum_{y<=k} r(y) > u * sum_y r(y),
- * sums in ascending id order. */
-static int sample_icdf(int V, const double* r, double u) {
+ * sums in ascending id order. *c_lo / *c_hi receive the cumulative fractions
+ * of the mass at the lower and upper edge of the chosen id's bin. */
+static int sample_icdf(int V, const double* r, double u, double* c_lo, double* c_hi) {
   double total = 0.0;
   for (int y = 0; y < V; ++y) total += r[y];
   const double target = u * total;
@@ -322,11 +323,41 @@ static int sample_icdf(int V, const double* r, double u) {
   int last = -1;
   for (int y = 0; y < V; ++y) {
     if (r[y] <= 0.0) continue;
+    const double before = cum;
     cum += r[y];
     last = y;
+    *c_lo = before / total;
+    *c_hi = cum / total;
     if (cum > target) return y;
   }
   return last;
+}
+
+/* Near-tie bands (a decision a logit error of tol could flip):
+ *  argmax        top-1 minus top-2 logit below 2 tol;
+ *  accept test   |u - alpha| < 2 tol alpha / T (alpha moves by a factor
+ *                exp(+-2 tol / T) when z_x and the normaliser each move by tol);
+ *  inverse CDF   |u - c| < 4 tol min(c, 1 - c) at either edge c of the
+ *                chosen bin (the cumulative mass below an edge moves by that
+ *                relative amount).
+ * Bands are open intervals, so tol = 0 flags nothing. */
+static int argmax_near_tie(int V, const double* z, double tol) {
+  double t1 = -INFINITY, t2 = -INFINITY;
+  for (int y = 0; y < V; ++y) {
+    if (z[y] > t1) {
+      t2 = t1;
+      t1 = z[y];
+    } else if (z[y] > t2) {
+      t2 = z[y];
+    }
+  }
+  return t1 - t2 < 2.0 * tol;
+}
+
+static int icdf_near_tie(double u, double c_lo, double c_hi, double tol) {
+  const double blo = 4.0 * tol * (c_lo < 1.0 - c_lo ? c_lo : 1.0 - c_lo);
+  const double bhi = 4.0 * tol * (c_hi < 1.0 - c_hi ? c_hi : 1.0 - c_hi);
+  return fabs(u - c_lo) < blo || fabs(u - c_hi) < bhi;
 }
 
 /* p_s = Softmax(z_s / T) as a dense vector. */
@@ -359,9 +390,12 @@ static int argmax_row(int V, const double* z) {
 int32_t msdo_accept(int32_t n, const int32_t* parent, const int32_t* tokens, int32_t V,
                     const double* logits, int32_t mode, double temperature, int32_t n_cand,
                     const int32_t* cand_ids, const float* cand_q, const float* u_accept,
-                    const float* u_sample, int32_t* acc_len, int32_t* next_tok, int32_t* path) {
+                    const float* u_sample, double tol_logit, int32_t* acc_len, int32_t* next_tok,
+                    int32_t* path, int32_t* tie_depth, int32_t* tie_next) {
   int cur = 0, depth = 0;
   path[0] = 0;
+  *tie_depth = -1;
+  *tie_next = 0;
   double* r = NULL;
   double* q = NULL;
   if (mode != MSDO_GREEDY) {
@@ -373,14 +407,20 @@ int32_t msdo_accept(int32_t n, const int32_t* parent, const int32_t* tokens, int
     const double* z = logits + (size_t)cur * V;
     int next_child = -1;
     int out_tok = -1;
+    int tie = 0;       /* a decision choosing the way down is in a band */
+    int tie_draw = 0;  /* REJECTION: the final draw is in a band        */
+    double c_lo = 0.0, c_hi = 1.0;
     if (mode == MSDO_GREEDY) {
       const int a = argmax_row(V, z);
+      tie = argmax_near_tie(V, z, tol_logit);
       for (int ch = cur + 1; ch < n; ++ch)
         if (parent[ch] == cur && tokens[ch] == a) { next_child = ch; break; }
       if (next_child < 0) out_tok = a;
     } else if (mode == MSDO_MATCH) {
       probs(V, z, temperature, r);
-      const int y = sample_icdf(V, r, (double)u_sample[cur]);
+      const double u = (double)u_sample[cur];
+      const int y = sample_icdf(V, r, u, &c_lo, &c_hi);
+      tie = icdf_near_tie(u, c_lo, c_hi, tol_logit);
       for (int ch = cur + 1; ch < n; ++ch)
         if (parent[ch] == cur && tokens[ch] == y) { next_child = ch; break; }
       if (next_child < 0) out_tok = y;
@@ -395,7 +435,9 @@ int32_t msdo_accept(int32_t n, const int32_t* parent, const int32_t* tokens, int
         if (!(q[x] > 0.0)) { status = -1; break; }
         const double ratio = r[x] / q[x];
         const double alpha = ratio < 1.0 ? ratio : 1.0;
-        if ((double)u_accept[ch] < alpha) { next_child = ch; break; }
+        const double u = (double)u_accept[ch];
+        tie |= fabs(u - alpha) < 2.0 * tol_logit * alpha / temperature;
+        if (u < alpha) { next_child = ch; break; }
         /* rejected: residual target and draft law without x */
         double zr = 0.0;
         for (int y = 0; y < V; ++y) {
@@ -411,10 +453,16 @@ int32_t msdo_accept(int32_t n, const int32_t* parent, const int32_t* tokens, int
           for (int y = 0; y < V; ++y) q[y] /= (1.0 - qx);
       }
       if (status) break;
-      if (next_child < 0) out_tok = sample_icdf(V, r, (double)u_sample[cur]);
+      if (next_child < 0) {
+        const double u = (double)u_sample[cur];
+        out_tok = sample_icdf(V, r, u, &c_lo, &c_hi);
+        tie_draw = icdf_near_tie(u, c_lo, c_hi, tol_logit);
+      }
     }
+    if (tie && *tie_depth < 0) *tie_depth = depth;
     if (next_child < 0) {
       *next_tok = out_tok;
+      *tie_next = tie || tie_draw;
       break;
     }
     cur = next_child;

@@ -108,14 +108,19 @@ enum { MSDO_GREEDY = 0, MSDO_REJECTION = 1, MSDO_MATCH = 2 };
  *  cand_ids/q  [n][n_cand] sparse draft law at each node (REJECTION only).
  *  u_accept    [n] uniform used when child c is tested (REJECTION).
  *  u_sample    [n] uniform used when sampling at node s (REJECTION/MATCH).
+ *  tol_logit   logit tolerance of the near-tie bands (0: none flagged).
  * Out: *acc_len = A, *next_tok, path[0..A] (slot of the accepted node at each
- * depth; path[0] = 0). Returns 0, or -1 if a child token has no draft mass at
- * its parent (REJECTION).
+ * depth; path[0] = 0). Near-tie bands (see msdo.c): *tie_depth = depth of
+ * the first node where a decision choosing the way down (an argmax, a MATCH
+ * draw, a REJECTION accept test) falls in a band, -1 if none; *tie_next = 1
+ * if the decision that produced the next token falls in one. Returns 0, or
+ * -1 if a child token has no draft mass at its parent (REJECTION).
  */
 int32_t msdo_accept(int32_t n, const int32_t* parent, const int32_t* tokens, int32_t V,
                     const double* logits, int32_t mode, double temperature, int32_t n_cand,
                     const int32_t* cand_ids, const float* cand_q, const float* u_accept,
-                    const float* u_sample, int32_t* acc_len, int32_t* next_tok, int32_t* path);
+                    const float* u_sample, double tol_logit, int32_t* acc_len, int32_t* next_tok,
+                    int32_t* path, int32_t* tie_depth, int32_t* tie_next);
 
 /*
  * Commit for ONE sequence on bf16 caches [n_layers][n_kv_heads][cap][head_dim]:

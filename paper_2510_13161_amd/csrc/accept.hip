@@ -10,6 +10,13 @@
 // sparse draft law q lives on <= 64 candidate ids, so the rejection residual
 // r = normalise((r - q)^+) differs from a multiple f * p only on those ids:
 // the kernel keeps f and the candidate values, never a dense vocab vector.
+//
+// Near-tie flags (optional): a decision that a logit error of tol_logit could
+// flip marks the sequence. Bands: an argmax whose top-1 minus top-2 logit is
+// below 2 tol; an accept test with |u - alpha| < 2 tol alpha / T (alpha moves
+// by a factor exp(+-2 tol / T) when z_x and the normaliser each move by tol);
+// an inverse-CDF draw with |u - c| < 4 tol min(c, 1 - c) at either edge c
+// (cumulative fraction) of the chosen id's bin.
 #include "kernels.h"
 
 namespace msd {
@@ -20,7 +27,9 @@ constexpr int kThreads = 1024;  // 16 waves: the fp64 vocabulary passes are late
 
 struct Shared {
   double red[kThreads];
+  double red2[kThreads];
   double pre[kThreads + 1];
+  double c_lo, c_hi;       // cumulative fractions at the edges of the drawn id's bin
   int cid[kMaxCand];       // candidate ids sorted ascending
   double rc[kMaxCand];     // residual mass at each sorted candidate
   double qc[kMaxCand];     // draft mass at each sorted candidate
@@ -53,6 +62,41 @@ __device__ double block_reduce_sum(double v, Shared& sh) {
   return r;
 }
 
+// Top-1 minus top-2 value of a logit row (a repeated maximum gives 0).
+__device__ double row_top2_gap(const float* z, int V, Shared& sh) {
+  double t1 = -INFINITY, t2 = -INFINITY;
+  for (int y = threadIdx.x; y < V; y += kThreads) {
+    const double v = (double)z[y];
+    if (v > t1) {
+      t2 = t1;
+      t1 = v;
+    } else if (v > t2) {
+      t2 = v;
+    }
+  }
+  sh.red[threadIdx.x] = t1;
+  sh.red2[threadIdx.x] = t2;
+  __syncthreads();
+  for (int o = kThreads / 2; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      const double a1 = sh.red[threadIdx.x], a2 = sh.red2[threadIdx.x];
+      const double b1 = sh.red[threadIdx.x + o], b2 = sh.red2[threadIdx.x + o];
+      sh.red[threadIdx.x] = fmax(a1, b1);
+      sh.red2[threadIdx.x] = fmax(fmin(a1, b1), fmax(a2, b2));
+    }
+    __syncthreads();
+  }
+  const double g = sh.red[0] - sh.red2[0];
+  __syncthreads();
+  return g;
+}
+
+__device__ bool icdf_near_tie(double u, double c_lo, double c_hi, double tol) {
+  const double blo = 4.0 * tol * fmin(c_lo, 1.0 - c_lo);
+  const double bhi = 4.0 * tol * fmin(c_hi, 1.0 - c_hi);
+  return fabs(u - c_lo) < blo || fabs(u - c_hi) < bhi;
+}
+
 // log sum_y exp(z_y / T)
 __device__ double row_lse(const float* z, int V, double invT, Shared& sh) {
   double mx = -INFINITY;
@@ -66,7 +110,8 @@ __device__ double row_lse(const float* z, int V, double invT, Shared& sh) {
 
 // Inverse-CDF draw from w(y) = f * exp(z_y/T - lse) off the candidates and
 // sh.rc[j] on candidate sh.cid[j]: the smallest id whose cumulative mass
-// exceeds u * total. Returns the id (all threads).
+// exceeds u * total. Returns the id (all threads); sh.c_lo / sh.c_hi get the
+// cumulative fractions at the edges of its bin.
 __device__ int row_sample(const float* z, int V, double invT, double lse, double f, double u,
                           Shared& sh) {
   const int t = threadIdx.x;
@@ -105,9 +150,12 @@ __device__ int row_sample(const float* z, int V, double invT, double lse, double
       if (j < sh.n_c && sh.cid[j] == y) w = sh.rc[j++];
       else w = f * exp((double)z[y] * invT - lse);
       if (w <= 0.0) continue;
+      const double before = cum;
       cum += w;
       if (cum > target) {
         pick = y;
+        sh.c_lo = before / sh.pre[kThreads];
+        sh.c_hi = cum / sh.pre[kThreads];
         break;
       }
     }
@@ -128,6 +176,7 @@ __device__ int row_sample(const float* z, int V, double invT, double lse, double
         break;
       }
     }
+    sh.c_lo = sh.c_hi = u;  // drawn at the rounding edge: inside every band
   }
   __syncthreads();
   const int r = sh.result;
@@ -144,31 +193,62 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
   for (int i = t; i < ns; i += kThreads) path[i] = i == 0 ? 0 : -1;
   __syncthreads();
 
+  const double tol = (double)a.tol_logit;
+  const bool flags = a.near_tie != nullptr;
   if (a.mode == 0) {  // GREEDY
-    if (t == 0) {
-      int cur = 0, depth = 0;
-      for (;;) {
-        const int want = a.argmax[(size_t)b * ns + cur];
-        int nxt = -1;
-        for (int ch = cur + 1; ch < ns; ++ch)
-          if (a.topo.parent[ch] == cur && tok[ch] == want) {
-            nxt = ch;
+    if (!flags) {
+      if (t == 0) {
+        int cur = 0, depth = 0;
+        for (;;) {
+          const int want = a.argmax[(size_t)b * ns + cur];
+          int nxt = -1;
+          for (int ch = cur + 1; ch < ns; ++ch)
+            if (a.topo.parent[ch] == cur && tok[ch] == want) {
+              nxt = ch;
+              break;
+            }
+          if (nxt < 0) {
+            a.next_tok[b] = want;
             break;
           }
-        if (nxt < 0) {
-          a.next_tok[b] = want;
+          cur = nxt;
+          path[++depth] = cur;
+        }
+        a.acc_len[b] = depth;
+      }
+      return;
+    }
+    // with near-tie flags every thread walks (the top-2 gap of each visited
+    // row is a workgroup reduction over the logits)
+    int cur = 0, depth = 0;
+    bool tie = false;
+    for (;;) {
+      const int want = a.argmax[(size_t)b * ns + cur];
+      tie |= row_top2_gap(a.logits + ((size_t)b * ns + cur) * a.vocab, a.vocab, sh) < 2.0 * tol;
+      int nxt = -1;
+      for (int ch = cur + 1; ch < ns; ++ch)
+        if (a.topo.parent[ch] == cur && tok[ch] == want) {
+          nxt = ch;
           break;
         }
-        cur = nxt;
-        path[++depth] = cur;
+      if (nxt < 0) {
+        if (t == 0) a.next_tok[b] = want;
+        break;
       }
+      cur = nxt;
+      ++depth;
+      if (t == 0) path[depth] = cur;
+    }
+    if (t == 0) {
       a.acc_len[b] = depth;
+      a.near_tie[b] = tie ? 1 : 0;
     }
     return;
   }
 
   const double invT = 1.0 / (double)a.temperature;
   int cur = 0, depth = 0;
+  bool tie = false;
   for (;;) {
     const float* z = a.logits + ((size_t)b * ns + cur) * a.vocab;
     const double lse = row_lse(z, a.vocab, invT, sh);
@@ -176,7 +256,9 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
     if (a.mode == 2) {  // MATCH: y ~ p, descend to the child carrying y
       if (t == 0) sh.n_c = 0;
       __syncthreads();
-      const int y = row_sample(z, a.vocab, invT, lse, 1.0, (double)a.u_sample[(size_t)b * ns + cur], sh);
+      const double u = (double)a.u_sample[(size_t)b * ns + cur];
+      const int y = row_sample(z, a.vocab, invT, lse, 1.0, u, sh);
+      tie |= icdf_near_tie(u, sh.c_lo, sh.c_hi, tol);
       for (int ch = cur + 1; ch < ns; ++ch)
         if (a.topo.parent[ch] == cur && tok[ch] == y) {
           next_child = ch;
@@ -212,7 +294,9 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
         }
         const double ratio = sh.rc[jx] / sh.qc[jx];
         const double alpha = ratio < 1.0 ? ratio : 1.0;
-        if ((double)a.u_accept[(size_t)b * ns + ch] < alpha) {
+        const double u = (double)a.u_accept[(size_t)b * ns + ch];
+        tie |= fabs(u - alpha) < 2.0 * tol * alpha * invT;
+        if (u < alpha) {
           next_child = ch;
           break;
         }
@@ -248,11 +332,15 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
         if (t == 0) {
           a.acc_len[b] = depth;
           a.next_tok[b] = -1;
+          if (flags) a.near_tie[b] = 1;
         }
         return;
       }
-      if (next_child < 0)
-        out_tok = row_sample(z, a.vocab, invT, lse, f, (double)a.u_sample[(size_t)b * ns + cur], sh);
+      if (next_child < 0) {
+        const double u = (double)a.u_sample[(size_t)b * ns + cur];
+        out_tok = row_sample(z, a.vocab, invT, lse, f, u, sh);
+        tie |= icdf_near_tie(u, sh.c_lo, sh.c_hi, tol);
+      }
     }
     if (next_child < 0) {
       if (t == 0) a.next_tok[b] = out_tok;
@@ -262,7 +350,10 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
     ++depth;
     if (t == 0) path[depth] = cur;
   }
-  if (t == 0) a.acc_len[b] = depth;
+  if (t == 0) {
+    a.acc_len[b] = depth;
+    if (flags) a.near_tie[b] = tie ? 1 : 0;
+  }
 }
 
 // Move accepted rows len + path[r] -> len + r (r = 1..A) of every layer and

@@ -188,6 +188,8 @@ struct AcceptArgs {
   int32_t* acc_len;
   int32_t* next_tok;
   int32_t* path;             // [batch][n_slots]
+  uint8_t* near_tie;         // [batch] or null
+  float tol_logit;           // half-width scale of the near-tie bands
   uint32_t* status;
   Topo topo;
 };

@@ -744,8 +744,8 @@ msd_status msd_early_exit_topk(const msd_model* m, const float* hidden, int32_t 
 
 msd_status msd_accept(const msd_model* m, const msd_block* blk, const float* logits,
                       const int32_t* argmax, const msd_sampling* smp, int32_t* acc_len,
-                      int32_t* next_tok, int32_t* path, uint32_t* status, void* ws,
-                      size_t ws_bytes, hipStream_t stream) {
+                      int32_t* next_tok, int32_t* path, uint8_t* near_tie, uint32_t* status,
+                      void* ws, size_t ws_bytes, hipStream_t stream) {
   (void)ws;
   (void)ws_bytes;
   msd_status st = check_block(m, blk);
@@ -770,6 +770,11 @@ msd_status msd_accept(const msd_model* m, const msd_block* blk, const float* log
   } else {
     return fail(MSD_ERR_UNSUPPORTED, "unknown acceptance mode");
   }
+  const float tol = smp ? smp->tol_logit : 0.0f;
+  if (!(tol >= 0.0f) || !std::isfinite(tol)) return fail(MSD_ERR_INVALID_ARG, "tol_logit must be finite and >= 0");
+  if (near_tie && !logits) return fail(MSD_ERR_INVALID_ARG, "near-tie flags need logits");
+  a.near_tie = near_tie;
+  a.tol_logit = tol;
   a.temperature = smp ? smp->temperature : 1.0f;
   a.batch = blk->batch;
   a.n_slots = blk->n_slots;

@@ -71,7 +71,7 @@ class Sampling(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("temperature", ctypes.c_float),
                 ("n_cand", ctypes.c_int32), ("cand_ids", ctypes.c_void_p),
                 ("cand_q", ctypes.c_void_p), ("u_accept", ctypes.c_void_p),
-                ("u_sample", ctypes.c_void_p)]
+                ("u_sample", ctypes.c_void_p), ("tol_logit", ctypes.c_float)]
 
 
 class HypTree(ctypes.Structure):
@@ -106,7 +106,7 @@ def lib() -> ctypes.CDLL:
         L.msd_workspace_bytes.restype = ctypes.c_size_t
         L.msd_verify_block.argtypes = [P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.msd_early_exit_topk.argtypes = [P, P, i32, i32, P, P, P, ctypes.c_size_t, P]
-        L.msd_accept.argtypes = [P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+        L.msd_accept.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.msd_kv_commit.argtypes = [P, P, P, P, P, P]
         L.msd_set_profile.argtypes = [P, i32, P, P, i32]
         L.msd_reuse_select.argtypes = [P, P, P, P, P, P, P, P, P, i32, P, P, P, P, P]
@@ -171,11 +171,13 @@ def early_exit_topk(handle, hidden: torch.Tensor, kappa: int, ids, logp, ws: tor
 
 
 def accept(handle, block: Block, logits, argmax, sampling: Optional[Sampling], acc_len, next_tok,
-           path, status, ws: Optional[torch.Tensor] = None, stream=None) -> None:
+           path, status, ws: Optional[torch.Tensor] = None, stream=None, near_tie=None) -> None:
+    """near_tie: optional device uint8 [batch] of near-tie flags (msd.h)."""
     _check(lib().msd_accept(handle, ctypes.byref(block), _ptr(logits), _ptr(argmax),
                             ctypes.byref(sampling) if sampling is not None else None,
-                            _ptr(acc_len), _ptr(next_tok), _ptr(path), _ptr(status),
-                            _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+                            _ptr(acc_len), _ptr(next_tok), _ptr(path), _ptr(near_tie),
+                            _ptr(status), _ptr(ws), 0 if ws is None else ws.numel(),
+                            _stream(stream)))
 
 
 def kv_commit(handle, kv: KVCache, block: Block, acc_len, path, stream=None) -> None:

@@ -31,7 +31,7 @@ def test_binding_structs_match_header_sizes():
     assert ctypes.sizeof(msd.ModelConfig) == 13 * 4 + 2 * 4
     assert ctypes.sizeof(msd.KVCache) == 4 * 8 + 2 * 4
     assert ctypes.sizeof(msd.Block) == 2 * 4 + 2 * 8
-    assert ctypes.sizeof(msd.Sampling) == 4 + 4 + 4 + 4 + 4 * 8
+    assert ctypes.sizeof(msd.Sampling) == 4 + 4 + 4 + 4 + 4 * 8 + 4 + 4
 
 
 def test_tensor_slot_layout():
@@ -81,7 +81,7 @@ def test_entry_points_reject_null_model_and_bad_blocks():
     assert lib.msd_verify_block(None, ctypes.byref(kv), ctypes.byref(blk), None, None, None, None,
                                 None, 0, None) == msd.MSD_ERR_INVALID_ARG
     assert lib.msd_accept(None, ctypes.byref(blk), None, None, None, None, None, None, None, None,
-                          0, None) == msd.MSD_ERR_INVALID_ARG
+                          None, 0, None) == msd.MSD_ERR_INVALID_ARG
     assert lib.msd_kv_commit(None, ctypes.byref(kv), ctypes.byref(blk), None, None,
                              None) == msd.MSD_ERR_INVALID_ARG
     assert lib.msd_early_exit_topk(None, None, 9, 8, None, None, None, 0, None) == msd.MSD_ERR_INVALID_ARG

@@ -216,6 +216,78 @@ def test_layernorm_learned_positions_relu_biases_tied_head():
     assert np.max(np.abs(r.logits - logits)) < 1e-12
 
 
+def test_value_bias_closed_form():
+    """Projection biases of the attention block (66B-style shape): with
+    W_v = 0 every block value row is b_v, so over an empty cache each row's
+    attention output is b_v whatever its scores; with W_o = I, W_down = 0
+    the block gives x' = x + b_v + b_o + b_down."""
+    m = TINY_OPT
+    w = synth.host_weights(m, 7)
+    g = np.random.default_rng(1)
+    for n in ("l0.bv", "l0.bo", "l0.b_down"):
+        w[n] = b16(g.normal(0.0, 1.0, 256))
+    w["l0.wv"] = zeros(256, 256)
+    w["l0.wo"] = eye(256, 256)
+    w["l0.w_down"] = zeros(256, 1024)
+    o = orc.Oracle(m, w, kv_cache_bf16=False)
+    tok, pos = np.array([11, 12, 13, 14]), np.array([3, 4, 4, 5])
+    r = o.forward(tok, pos, np.array([-1, 0, 0, 2]))
+    want = (f64(w["embed"])[tok] + f64(w["pos_embed"])[pos] + f64(w["l0.bv"]) + f64(w["l0.bo"])
+            + f64(w["l0.b_down"]))
+    assert np.max(np.abs(r.x_final - want)) < 1e-12
+
+
+@pytest.mark.parametrize("rotary", [False, True])
+def test_query_key_bias_closed_form(rotary):
+    """Query and key biases: with W_q = W_k = W_v = 0 a row's query is b_q and
+    every block key b_k (rotated to the row's position when the model uses
+    rotary positions, bias first); the scores against the cached keys and the
+    visible block keys, softmax (scipy) and the value average (block values
+    b_v) give the attention output exactly. A dropped or misplaced b_q or b_k
+    changes every score."""
+    m = TINY_OPT if not rotary else dataclasses.replace(TINY1, name="tiny-bias", bias=True)
+    seed = 8
+    w = synth.host_weights(m, seed)
+    g = np.random.default_rng(2)
+    for n in ("l0.bq", "l0.bk", "l0.bv"):
+        w[n] = b16(g.normal(0.0, 1.0, 256))
+    for n in ("l0.wq", "l0.wk", "l0.wv"):
+        w[n] = zeros(256, 256)
+    w["l0.wo"] = eye(256, 256)
+    w["l0.w_down"] = zeros(256, 1024)
+    if m.bias:
+        w["l0.bo"] = np.zeros(256, np.uint16)
+        w["l0.b_down"] = np.zeros(256, np.uint16)
+    o = orc.Oracle(m, w, kv_cache_bf16=False)
+    n_ctx = 6
+    ctx = ctx_fn(m, seed, n_ctx)
+    parent = np.array([-1, 0, 1, 0])
+    tok = np.array([21, 22, 23, 24])
+    pos = n_ctx + orc.depths(parent)
+    r = o.forward(tok, pos, parent, ctx, n_ctx)
+    hd, H = m.head_dim, m.n_heads
+    bq = f64(w["l0.bq"]).reshape(H, hd)
+    bk = f64(w["l0.bk"]).reshape(H, hd)
+    bv = f64(w["l0.bv"]).reshape(H, hd)
+    kc, vc = (f64(a) for a in ctx(0))            # [H][n_ctx][hd]
+    anc = {0: [0], 1: [0, 1], 2: [0, 1, 2], 3: [0, 3]}
+    e = f64(w["embed"])[tok]
+    if m.pos == "learned":
+        e = e + f64(w["pos_embed"])[pos]
+    for i in range(4):
+        for h in range(H):
+            q = bq[h][None]
+            kb = np.repeat(bk[h][None], 4, 0)
+            if rotary:
+                q = _rope_complex(q, np.array([pos[i]], np.float64), m.rope_theta)
+                kb = _rope_complex(kb, pos.astype(np.float64), m.rope_theta)
+            keys = np.concatenate([kc[h, :n_ctx], kb[anc[i]]])
+            vals = np.concatenate([vc[h, :n_ctx], np.repeat(bv[h][None], len(anc[i]), 0)])
+            p = scipy.special.softmax(keys @ q[0] / np.sqrt(hd))
+            got = r.x_final[i, h * hd:(h + 1) * hd] - e[i, h * hd:(h + 1) * hd]
+            assert np.max(np.abs(got - p @ vals)) < 1e-12, (i, h)
+
+
 # ---------------------------------------------------------------------------
 # invariants of the method
 # ---------------------------------------------------------------------------
@@ -370,6 +442,52 @@ def test_greedy_ties_go_to_the_smaller_id():
     z[0, 3] = z[0, 7] = 5.0
     A, nxt, _ = orc.Oracle.accept(np.array([-1, 0]), np.array([0, 7]), z)
     assert (A, nxt) == (0, 3)
+
+
+def test_near_tie_bands_closed_forms():
+    """Near-tie bands of the acceptance decisions, each on a hand-computed case
+    (tol 0.02). Argmax: top-1 minus top-2 of 0.03 lies in the 2 tol band, 0.05
+    does not. Inverse CDF on p = (0.7, 0.3): id 0's bin is [0, 0.7], so
+    u = 0.69 lies within 4 tol min(c, 1 - c) = 0.024 of its upper edge, u =
+    0.5 does not. Accept test with p(x) = 0.3, q(x) = 0.6 (alpha = 0.5): u =
+    0.51 lies within 2 tol alpha / T = 0.02, u = 0.9 does not."""
+    tol = 0.02
+    par2 = np.array([-1, 0])
+    # greedy: the flag sits at the depth of the row, and covers the next token
+    for gap, flagged in ((0.03, True), (0.05, False)):
+        z = np.zeros((2, 6))
+        z[0, 2] = 1.0
+        z[1, 4] = 1.0
+        z[1, 1] = 1.0 - gap
+        A, nxt, path, td, tn = orc.Oracle.accept(par2, np.array([9, 2]), z, tol_logit=tol, return_tie=True)
+        assert (A, nxt, list(path)) == (1, 4, [0, 1])
+        assert (td, tn) == ((1, True) if flagged else (-1, False))
+    # MATCH draw on (0.7, 0.3): id 0 drawn, no child carries it
+    zr = np.log(np.array([[0.7, 0.3], [0.5, 0.5]]))
+    for u, flagged in ((0.69, True), (0.5, False)):
+        A, nxt, _, td, tn = orc.Oracle.accept(par2, np.array([0, 1]), zr, "match", 1.0,
+                                              u_sample=np.array([u, 0.5], np.float32),
+                                              tol_logit=tol, return_tie=True)
+        assert (A, nxt) == (0, 0)
+        assert (td, tn) == ((0, True) if flagged else (-1, False))
+    # REJECTION accept test of child x = 1: p(1) = 0.3, q(1) = 0.6, alpha = 0.5
+    cid = np.array([[1, 0], [1, 0]], np.int32)
+    cq = np.array([[0.6, 0.4], [0.6, 0.4]], np.float32)
+    for u, flagged, acc in ((0.51, True, 0), (0.49, True, 1), (0.9, False, 0)):
+        A, nxt, _, td, tn = orc.Oracle.accept(par2, np.array([0, 1]), zr, "rejection", 1.0, cid, cq,
+                                              np.array([0.0, u], np.float32),
+                                              np.array([0.5, 0.5], np.float32),
+                                              tol_logit=tol, return_tie=True)
+        assert A == acc
+        assert td == (0 if flagged else -1)
+        if acc == 0:
+            # rejected: r = normalise((p - q)^+) = (1, 0), so id 0 whatever u
+            assert nxt == 0
+    # no tolerance: nothing is flagged, not even an exact tie (the smaller id wins)
+    z = np.zeros((2, 6))
+    z[0, 2] = z[0, 3] = 1.0
+    assert orc.Oracle.accept(par2, np.array([9, 2]), z, tol_logit=0.0, return_tie=True)[3:] == (-1, False)
+    assert orc.Oracle.accept(par2, np.array([9, 2]), z, tol_logit=1e-9, return_tie=True)[3:] == (0, True)
 
 
 def _first_token_law(p_root, q, cands, n_children, mode, n_samples, seed, V):
