@@ -165,7 +165,8 @@ typedef struct {
  * parent == NULL means a chain (parent[i] = i - 1); otherwise parent[0] = -1
  * and 0 <= parent[i] < i. */
 typedef struct {
-  int32_t batch, n_slots;   /* 1 <= n_slots <= 64, batch <= batch_cap      */
+  int32_t batch, n_slots;   /* 1 <= n_slots <= 64, batch <= batch_cap;
+                               batch * n_slots <= 144 for msd_verify_block */
   const int32_t* tokens;    /* device [batch][n_slots]                     */
   const int32_t* parent;    /* host [n_slots] or NULL                      */
 } msd_block;

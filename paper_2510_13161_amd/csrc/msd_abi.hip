@@ -202,12 +202,14 @@ msd_status make_topo(const msd_block* blk, Topo* topo) {
   return MSD_OK;
 }
 
-msd_status check_block(const msd_model* m, const msd_block* blk) {
+// row_limit: the block's rows go through the GEMMs (at most kMaxMT row
+// tiles); acceptance and commit work per sequence and take any batch.
+msd_status check_block(const msd_model* m, const msd_block* blk, bool row_limit = true) {
   if (!m || !blk) return fail(MSD_ERR_INVALID_ARG, "null model or block");
   if (blk->n_slots < 1 || blk->n_slots > kMaxSlots)
     return fail(MSD_ERR_SHAPE, "n_slots must lie in [1, 64]");
   if (blk->batch < 1) return fail(MSD_ERR_SHAPE, "batch must be >= 1");
-  if ((size_t)blk->batch * blk->n_slots > (size_t)kMaxMT * 16)
+  if (row_limit && (size_t)blk->batch * blk->n_slots > (size_t)kMaxMT * 16)
     return fail(MSD_ERR_SHAPE, "batch * n_slots must be <= 144");
   if (!blk->tokens) return fail(MSD_ERR_INVALID_ARG, "null tokens");
   return MSD_OK;
@@ -748,7 +750,7 @@ msd_status msd_accept(const msd_model* m, const msd_block* blk, const float* log
                       void* ws, size_t ws_bytes, hipStream_t stream) {
   (void)ws;
   (void)ws_bytes;
-  msd_status st = check_block(m, blk);
+  msd_status st = check_block(m, blk, false);
   if (st != MSD_OK) return st;
   if (!acc_len || !next_tok || !path) return fail(MSD_ERR_INVALID_ARG, "null output");
   Topo topo;
@@ -799,7 +801,7 @@ msd_status msd_accept(const msd_model* m, const msd_block* blk, const float* log
 
 msd_status msd_kv_commit(const msd_model* m, msd_kv_cache* kv, const msd_block* blk,
                          const int32_t* acc_len, const int32_t* path, hipStream_t stream) {
-  msd_status st = check_block(m, blk);
+  msd_status st = check_block(m, blk, false);
   if (st != MSD_OK) return st;
   if (!kv || !kv->k || !kv->v || !kv->len) return fail(MSD_ERR_INVALID_ARG, "null kv cache field");
   if (!acc_len || !path) return fail(MSD_ERR_INVALID_ARG, "null acc_len or path");

@@ -35,6 +35,9 @@ class GpuResult:
     status: int
     k_rows: List[np.ndarray]       # per layer [B][Hkv][n_slots][hd] bf16 bits (after verify)
     v_rows: List[np.ndarray]
+    near_tie: Optional[np.ndarray] = None   # [B] flags of msd_accept
+    k_commit: Optional[List[np.ndarray]] = None  # per layer [B][Hkv][n_slots][hd] rows at
+    v_commit: Optional[List[np.ndarray]] = None  # len_before + r after the commit (first 1 + A valid)
 
 
 class GpuCase:
@@ -62,6 +65,26 @@ class GpuCase:
         self.cache.len.copy_(self.torch.from_numpy(self.si.ctx_len))
         self.cache.status.zero_()
 
+    def _rows(self, start: np.ndarray, count: np.ndarray):
+        """Cache rows [start_b, start_b + count_b) of every layer (bf16 bits,
+        zero past count_b), per layer [B][Hkv][n_slots][hd]."""
+        torch = self.torch
+        B, n = self.w.batch, self.w.n_slots
+        ks, vs = [], []
+        for l in range(self.shape.n_layers):
+            kr = np.zeros((B, self.shape.n_kv_heads, n, self.shape.head_dim), np.uint16)
+            vr = np.zeros_like(kr)
+            for b in range(B):
+                L = int(start[b])
+                hi = min(L + int(count[b]), self.capacity)  # a block that overflows the cache has no rows there
+                if hi <= L:
+                    continue
+                kr[b, :, :hi - L] = self.cache.k[l, b, :, L:hi].view(torch.int16).cpu().numpy().view(np.uint16)
+                vr[b, :, :hi - L] = self.cache.v[l, b, :, L:hi].view(torch.int16).cpu().numpy().view(np.uint16)
+            ks.append(kr)
+            vs.append(vr)
+        return ks, vs
+
     def run(self, ee: bool = True, want_logits: bool = True, commit: bool = True,
             mode: Optional[str] = None) -> GpuResult:
         torch, msd = self.torch, self.msd
@@ -87,19 +110,7 @@ class GpuCase:
         ws = torch.empty(nb, dtype=torch.uint8, device=dev)
         msd.verify_block(self.model.handle, self.cache.c, blk, req, logits, argmax, lse, ws)
         # block rows written by the verify pass
-        k_rows, v_rows = [], []
-        for l in range(self.shape.n_layers):
-            kr = np.empty((B, self.shape.n_kv_heads, n, self.shape.head_dim), np.uint16)
-            vr = np.empty_like(kr)
-            for b in range(B):
-                L = int(si.ctx_len[b])
-                hi = min(L + n, self.capacity)  # a block that overflows the cache has no rows there
-                kr[b] = 0
-                vr[b] = 0
-                kr[b, :, :hi - L] = self.cache.k[l, b, :, L:hi].view(torch.int16).cpu().numpy().view(np.uint16)
-                vr[b, :, :hi - L] = self.cache.v[l, b, :, L:hi].view(torch.int16).cpu().numpy().view(np.uint16)
-            k_rows.append(kr)
-            v_rows.append(vr)
+        k_rows, v_rows = self._rows(si.ctx_len, np.full(B, n))
         acc = torch.empty(B, dtype=torch.int32, device=dev)
         nxt = torch.empty(B, dtype=torch.int32, device=dev)
         path = torch.empty((B, n), dtype=torch.int32, device=dev)
@@ -111,10 +122,17 @@ class GpuCase:
             ua, us = t(si.u_accept), t(si.u_sample)
             keep += [cid, cq, ua, us]
             smp = msd.Sampling(msd.MODES[mode], float(w.temperature), si.cand_ids.shape[-1],
-                               cid.data_ptr(), cq.data_ptr(), ua.data_ptr(), us.data_ptr())
-        msd.accept(self.model.handle, blk, logits, argmax, smp, acc, nxt, path, self.cache.status)
+                               cid.data_ptr(), cq.data_ptr(), ua.data_ptr(), us.data_ptr(), TOL_LOGIT)
+        else:
+            smp = msd.Sampling(msd.MSD_GREEDY, 1.0, 0, None, None, None, None, TOL_LOGIT)
+        tie = torch.empty(B, dtype=torch.uint8, device=dev) if want_logits else None
+        msd.accept(self.model.handle, blk, logits, argmax, smp, acc, nxt, path, self.cache.status,
+                   near_tie=tie)
+        k_com = v_com = None
         if commit:
             msd.kv_commit(self.model.handle, self.cache.c, blk, acc, path)
+            torch.cuda.synchronize()
+            k_com, v_com = self._rows(si.ctx_len, 1 + acc.cpu().numpy())
         torch.cuda.synchronize()
         return GpuResult(
             logits=logits.cpu().numpy() if logits is not None else None,
@@ -122,7 +140,8 @@ class GpuCase:
             ee_ids=ids.cpu().numpy() if ee else None, ee_logp=logp.cpu().numpy() if ee else None,
             acc_len=acc.cpu().numpy(), next_tok=nxt.cpu().numpy(), path=path.cpu().numpy(),
             len_after=self.cache.len.cpu().numpy(), status=int(self.cache.status.item()),
-            k_rows=k_rows, v_rows=v_rows)
+            k_rows=k_rows, v_rows=v_rows, near_tie=tie.cpu().numpy() if tie is not None else None,
+            k_commit=k_com, v_commit=v_com)
 
 
 @dataclasses.dataclass
@@ -136,6 +155,9 @@ class OracleSeq:
     acc: int
     nxt: int
     path: np.ndarray
+    tie_depth: int = -1            # first depth with a path decision in a near-tie band
+    tie_next: bool = False         # the next-token decision is in a band
+    ee_logits: Optional[np.ndarray] = None  # [n, V] early-exit head logits
 
 
 def oracle_sequence(shape, w: synth.Workload, si: synth.StepInputs, b: int, ee: bool = True,
@@ -155,7 +177,7 @@ def oracle_sequence(shape, w: synth.Workload, si: synth.StepInputs, b: int, ee: 
     pos = L + orc.depths(si.parent)
     ee_layer = min(w.ee_layer, shape.n_layers - 1) if ee else None
     r = o.forward(si.tokens[b], pos, si.parent, ctx, L, ee_layer=ee_layer)
-    ids = logp = marg = None
+    ids = logp = marg = z_ee = None
     if ee:
         z_ee = o.head(r.x_ee)
         ids, logp, _ = orc.Oracle.topk(z_ee, w.kappa)
@@ -165,8 +187,9 @@ def oracle_sequence(shape, w: synth.Workload, si: synth.StepInputs, b: int, ee: 
     if mode != "greedy":
         kw = dict(cand_ids=si.cand_ids[b], cand_q=si.cand_q[b], u_accept=si.u_accept[b],
                   u_sample=si.u_sample[b])
-    A, nxt, path = o.accept(si.parent, si.tokens[b], r.logits, mode, w.temperature, **kw)
-    return OracleSeq(r.logits, ids, logp, marg, r.blk_k, r.blk_v, A, nxt, path)
+    A, nxt, path, td, tn = o.accept(si.parent, si.tokens[b], r.logits, mode, w.temperature,
+                                    tol_logit=TOL_LOGIT, return_tie=True, **kw)
+    return OracleSeq(r.logits, ids, logp, marg, r.blk_k, r.blk_v, A, nxt, path, td, tn, z_ee)
 
 
 def margins(z: np.ndarray, k: int) -> np.ndarray:
@@ -175,11 +198,11 @@ def margins(z: np.ndarray, k: int) -> np.ndarray:
     return np.min(part[..., :-1] - part[..., 1:], axis=-1)
 
 
-def streaming_oracle(shape, seed: int) -> orc.Oracle:
+def streaming_oracle(shape, seed: int, kv_cache_bf16: bool = True) -> orc.Oracle:
     """Oracle whose layer weights are regenerated on the host layer by layer."""
     glob = synth.host_weights(shape, seed, layers=[], with_globals=True)
     src = lambda l: synth.host_weights(shape, seed, layers=[l], with_globals=False)
-    return orc.Oracle(shape, glob, layer_source=src)
+    return orc.Oracle(shape, glob, layer_source=src, kv_cache_bf16=kv_cache_bf16)
 
 
 def chain_inputs(si: synth.StepInputs, b: int, slots) -> synth.StepInputs:
@@ -188,3 +211,55 @@ def chain_inputs(si: synth.StepInputs, b: int, slots) -> synth.StepInputs:
     toks = si.tokens[b, slots][None].astype(np.int32)
     par = np.arange(-1, len(slots) - 1, dtype=np.int32)
     return synth.StepInputs(parent=par, tokens=toks, ctx_len=si.ctx_len[b:b + 1].copy())
+
+
+def oracle_runs(shape, w: synth.Workload, si: synth.StepInputs, specs, ee: bool = True,
+                mode: Optional[str] = None) -> Dict[tuple, OracleSeq]:
+    """Oracle steps for several (sequence b, kv_cache_bf16) pairs in lockstep
+    over the layers, so each layer's weights are generated on the host once
+    for all of them (full-depth workloads). Returns {(b, kv_cache_bf16): OracleSeq}."""
+    glob = synth.host_weights(shape, w.seed, layers=[], with_globals=True)
+    memo: Dict[int, Dict[str, np.ndarray]] = {}
+
+    def src(l):
+        if l not in memo:
+            memo.clear()
+            memo[l] = synth.host_weights(shape, w.seed, layers=[l], with_globals=False)
+        return memo[l]
+
+    oracles = {m: orc.Oracle(shape, glob, layer_source=src, kv_cache_bf16=m) for m in {m for _, m in specs}}
+    ee_layer = min(w.ee_layer, shape.n_layers - 1) if ee else None
+    state = {}
+    for b, m in specs:
+        pos = int(si.ctx_len[b]) + orc.depths(si.parent)
+        state[(b, m)] = dict(x=oracles[m].embed(si.tokens[b], pos), pos=pos, k=[], v=[], x_ee=None)
+    for l in range(shape.n_layers):
+        for b in sorted({b for b, _ in specs}):
+            L = int(si.ctx_len[b])
+            ck = synth.host_ctx(shape, w.seed, l, "k", b, L) if L > 0 else None
+            cv = synth.host_ctx(shape, w.seed, l, "v", b, L) if L > 0 else None
+            for m in sorted({m for bb, m in specs if bb == b}):
+                st = state[(b, m)]
+                k, v = oracles[m].layer(l, st["x"], st["pos"], si.parent, ck, cv, L)
+                st["k"].append(k)
+                st["v"].append(v)
+                if ee_layer is not None and l + 1 == ee_layer:
+                    st["x_ee"] = st["x"].copy()
+    mode = mode or w.mode
+    out = {}
+    for (b, m), st in state.items():
+        o = oracles[m]
+        logits = o.head(st["x"])
+        ids = logp = marg = z_ee = None
+        if ee:
+            z_ee = o.head(st["x_ee"])
+            ids, logp, _ = orc.Oracle.topk(z_ee, w.kappa)
+            marg = margins(z_ee, w.kappa)
+        kw = {}
+        if mode != "greedy":
+            kw = dict(cand_ids=si.cand_ids[b], cand_q=si.cand_q[b], u_accept=si.u_accept[b],
+                      u_sample=si.u_sample[b])
+        A, nxt, path, td, tn = o.accept(si.parent, si.tokens[b], logits, mode, w.temperature,
+                                        tol_logit=TOL_LOGIT, return_tie=True, **kw)
+        out[(b, m)] = OracleSeq(logits, ids, logp, marg, st["k"], st["v"], A, nxt, path, td, tn, z_ee)
+    return out
