@@ -204,6 +204,25 @@ msd_status msd_verify_block(const msd_model* model, msd_kv_cache* kv, const msd_
                             float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * msd_verify_block without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same kernels and outputs, with the scratch in a
+ * static device array of the library, MSD_STATIC_SCRATCH_BYTES (64 MiB) per
+ * GPU, held from the first msd_model_create on that GPU until the process
+ * ends. The call allocates nothing. A block whose workspace
+ * (msd_workspace_bytes) exceeds that size returns MSD_ERR_WORKSPACE and
+ * enqueues nothing: the 14B-shaped chain and tree blocks and the 66B-shaped
+ * tree fit, long-context batches (batch 16 at 8K contexts) do not. Every call
+ * on one GPU shares its scratch, which keeps the last call's contents (the
+ * kernels clear what must start at zero): calls that overlap on one GPU,
+ * from different streams or threads, race and must be ordered by the caller.
+ */
+#define MSD_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+msd_status msd_verify_block_static(const msd_model* model, msd_kv_cache* kv, const msd_block* block,
+                                   const msd_ee_request* ee, float* logits, int32_t* argmax,
+                                   float* lse, hipStream_t stream);
+
+/*
  * Token channel of Sec. 3.1 from a residual: hidden is device fp32 [M][d_model]
  * (the residual stream after some layer); applies the final norm and the LM
  * head and writes the kappa best ids and log-probabilities per row.

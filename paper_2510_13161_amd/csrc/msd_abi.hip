@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -16,8 +17,16 @@ using namespace msd;
 static_assert(sizeof(msd_reuse_stats) == sizeof(ReuseStats), "reuse statistics layout");
 static_assert(MSD_MAX_TREE_NODES == kMaxTreeNodes, "hypothesis tree bound");
 
+// Scratch of msd_verify_block_static, for callers that cannot allocate: one
+// copy per GPU, held by the loaded code object until the process ends. Host
+// code never uses this name as an address (on the host it is a stand-in);
+// the device address comes from hipGetSymbolAddress, per device.
+constexpr size_t kStaticScratchBytes = MSD_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
 struct msd_model {
   msd_model_config cfg;
+  void* scratch = nullptr;         // this device's copy of `scratch` (msd_verify_block_static)
   std::vector<const uint16_t*> t;  // MSD_N_TENSORS(n_layers) entries
   float2* rope = nullptr;          // [max_positions][head_dim/2] (cos, sin)
   float* colsums = nullptr;        // LayerNorm column sums c = W g, e = W b (model create)
@@ -320,6 +329,33 @@ hipError_t prof_mark(const msd_model* m, int kclass, int layer, bool begin, hipS
   return ev ? hipEventRecord(ev, s) : hipSuccess;
 }
 
+// Device address of the current device's `scratch`, looked up once per
+// device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+msd_status static_scratch_address(void** out) {
+  int dev = -1;
+  MSD_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(MSD_ERR_UNSUPPORTED, "device index above 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    MSD_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(MSD_ERR_HIP, "hipGetSymbolAddress returned a null scratch address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MSD_OK;
+}
+
+msd_status verify_prepare(const msd_model* m, msd_kv_cache* kv, const msd_block* blk,
+                          const msd_ee_request* ee, const int32_t* argmax, Topo* topo, Layout* Lout);
+msd_status verify_launch(const msd_model* m, msd_kv_cache* kv, const msd_block* blk,
+                         const msd_ee_request* ee, float* logits, int32_t* argmax, float* lse,
+                         char* w, const Topo& topo, const Layout& L, hipStream_t stream);
+
 }  // namespace
 
 extern "C" {
@@ -523,6 +559,15 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
       return fail(MSD_ERR_HIP, std::string("rotary table: ") + hipGetErrorString(e));
     }
   }
+  // the static scratch of this device (msd_verify_block_static)
+  const msd_status sst = static_scratch_address(&m->scratch);
+  if (sst != MSD_OK) {
+    const std::string msg = g_err;
+    if (m->rope) (void)hipFree(m->rope);
+    if (m->colsums) (void)hipFree(m->colsums);
+    delete m;
+    return fail(sst, "static scratch: " + msg);
+  }
   *out = m;
   return MSD_OK;
 }
@@ -543,6 +588,39 @@ size_t msd_workspace_bytes(const msd_model* m, int32_t batch, int32_t n_slots, i
 msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_block* blk,
                             const msd_ee_request* ee, float* logits, int32_t* argmax, float* lse,
                             void* ws, size_t ws_bytes, hipStream_t stream) {
+  Topo topo;
+  Layout L;
+  msd_status st = verify_prepare(m, kv, blk, ee, argmax, &topo, &L);
+  if (st != MSD_OK) return st;
+  if (!ws || ws_bytes < L.total) return fail(MSD_ERR_WORKSPACE, "workspace too small");
+  return verify_launch(m, kv, blk, ee, logits, argmax, lse, static_cast<char*>(ws), topo, L, stream);
+}
+
+msd_status msd_verify_block_static(const msd_model* m, msd_kv_cache* kv, const msd_block* blk,
+                                   const msd_ee_request* ee, float* logits, int32_t* argmax,
+                                   float* lse, hipStream_t stream) {
+  Topo topo;
+  Layout L;
+  msd_status st = verify_prepare(m, kv, blk, ee, argmax, &topo, &L);
+  if (st != MSD_OK) return st;
+  if (L.total > kStaticScratchBytes)
+    return fail(MSD_ERR_WORKSPACE, "this block needs " + std::to_string(L.total) +
+                                       " bytes of scratch; the static scratch holds " +
+                                       std::to_string(kStaticScratchBytes) +
+                                       " (use msd_verify_block with a workspace)");
+  if (!m->scratch) return fail(MSD_ERR_HIP, "static scratch address unavailable");
+  return verify_launch(m, kv, blk, ee, logits, argmax, lse, static_cast<char*>(m->scratch), topo, L,
+                       stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Host checks of a verify call; fills the block topology and the workspace
+// layout. Enqueues nothing.
+msd_status verify_prepare(const msd_model* m, msd_kv_cache* kv, const msd_block* blk,
+                          const msd_ee_request* ee, const int32_t* argmax, Topo* topo, Layout* Lout) {
   msd_status st = check_block(m, blk);
   if (st != MSD_OK) return st;
   if (!kv || !kv->k || !kv->v || !kv->len || !kv->status) return fail(MSD_ERR_INVALID_ARG, "null kv cache field");
@@ -559,14 +637,21 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
     if (!ee->ids || !ee->logp) return fail(MSD_ERR_INVALID_ARG, "null early-exit outputs");
     kappa = ee->kappa;
   }
-  Topo topo;
-  st = make_topo(blk, &topo);
+  st = make_topo(blk, topo);
   if (st != MSD_OK) return st;
-  const Layout L = layout(m, blk->batch, blk->n_slots, kappa, kv->capacity);
-  if (!ws || ws_bytes < L.total) return fail(MSD_ERR_WORKSPACE, "workspace too small");
+  *Lout = layout(m, blk->batch, blk->n_slots, kappa, kv->capacity);
+  return MSD_OK;
+}
+
+// The verify pass proper: rows, N layers (early exit after layer l_e), final
+// head, all on `stream`, using the workspace at w laid out as L.
+msd_status verify_launch(const msd_model* m, msd_kv_cache* kv, const msd_block* blk,
+                         const msd_ee_request* ee, float* logits, int32_t* argmax, float* lse,
+                         char* w, const Topo& topo, const Layout& L, hipStream_t stream) {
+  msd_status st = MSD_OK;
+  const msd_model_config& c = m->cfg;
   const int M = blk->batch * blk->n_slots;
   const Shapes s = shapes(m, M);
-  char* w = static_cast<char*>(ws);
   const int d = c.d_model, qd = c.n_heads * c.head_dim;
   float* x = reinterpret_cast<float*>(w + L.x);
   float2* stats = reinterpret_cast<float2*>(w + L.stats);
@@ -713,6 +798,10 @@ msd_status msd_verify_block(const msd_model* m, msd_kv_cache* kv, const msd_bloc
   }
   return run_head(m, s, L, w, M, stats, 1, logits, nullptr, nullptr, argmax, lse, stream);
 }
+
+}  // namespace
+
+extern "C" {
 
 msd_status msd_early_exit_topk(const msd_model* m, const float* hidden, int32_t M, int32_t kappa,
                                int32_t* ids, float* logp, void* ws, size_t ws_bytes,

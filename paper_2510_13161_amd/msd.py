@@ -32,7 +32,8 @@ LAYER_SLOTS = ["attn_norm.g", "attn_norm.b", "wq", "wk", "wv", "bq", "bk", "bv",
 
 EXPORTED = ["msd_last_error", "msd_model_create", "msd_model_destroy", "msd_workspace_bytes",
             "msd_verify_block", "msd_early_exit_topk", "msd_accept", "msd_kv_commit",
-            "msd_reuse_select", "msd_set_profile"]
+            "msd_reuse_select", "msd_set_profile", "msd_verify_block_static"]
+MSD_STATIC_SCRATCH_BYTES = 64 << 20
 MSD_K_QKV, MSD_K_ATTN, MSD_K_OPROJ, MSD_K_FFN_UP, MSD_K_FFN_DOWN = 0, 1, 2, 3, 4
 MSD_NEXT_BRANCH, MSD_NEXT_CONTINUE, MSD_NEXT_FRESH = 0, 1, 2
 MSD_MAX_TREE_NODES = 256
@@ -105,12 +106,14 @@ def lib() -> ctypes.CDLL:
         L.msd_workspace_bytes.argtypes = [P, i32, i32, i32, i32]
         L.msd_workspace_bytes.restype = ctypes.c_size_t
         L.msd_verify_block.argtypes = [P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+        L.msd_verify_block_static.argtypes = [P, P, P, P, P, P, P, P]
         L.msd_early_exit_topk.argtypes = [P, P, i32, i32, P, P, P, ctypes.c_size_t, P]
         L.msd_accept.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.msd_kv_commit.argtypes = [P, P, P, P, P, P]
         L.msd_set_profile.argtypes = [P, i32, P, P, i32]
         L.msd_reuse_select.argtypes = [P, P, P, P, P, P, P, P, P, i32, P, P, P, P, P]
-        for f in ("msd_model_create", "msd_verify_block", "msd_early_exit_topk", "msd_accept",
+        for f in ("msd_model_create", "msd_verify_block", "msd_verify_block_static",
+                  "msd_early_exit_topk", "msd_accept",
                   "msd_kv_commit", "msd_reuse_select", "msd_set_profile"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
@@ -162,6 +165,14 @@ def verify_block(handle, kv: KVCache, block: Block, ee: Optional[EERequest], log
     _check(lib().msd_verify_block(handle, ctypes.byref(kv), ctypes.byref(block),
                                   ctypes.byref(ee) if ee is not None else None, _ptr(logits),
                                   _ptr(argmax), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def verify_block_static(handle, kv: KVCache, block: Block, ee: Optional[EERequest], logits, argmax,
+                        lse, stream=None) -> None:
+    """msd_verify_block with the library's static scratch (no workspace)."""
+    _check(lib().msd_verify_block_static(handle, ctypes.byref(kv), ctypes.byref(block),
+                                         ctypes.byref(ee) if ee is not None else None, _ptr(logits),
+                                         _ptr(argmax), _ptr(lse), _stream(stream)))
 
 
 def early_exit_topk(handle, hidden: torch.Tensor, kappa: int, ids, logp, ws: torch.Tensor,
