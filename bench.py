@@ -165,7 +165,7 @@ def copy_calibration(nbytes: int) -> None:
 
 def after_accept(msd, torch, np, model, blk, acc, nxt, path, logits, lse, ids, w, vocab, reps=50):
     """The step after acceptance (Sec. 3.1 reuse criterion and next-window
-    selection, App. C statistics) on the last timed step's outputs, timed on
+    selection, App. E statistics) on the last timed step's outputs, timed on
     its own: the hypothesis tree has kappa chains of gamma + 1 nodes (the
     window's depth; fewer if kappa chains would exceed the tree's node limit)
     rooted at each sequence's early-exit top-kappa (root row), continuation
@@ -359,7 +359,7 @@ def latency_law(args) -> dict:
     ee.ready = None
     delta = t_target - t_prefix
 
-    # Speculative Streaming draft (Sec. 3.3, timing only): one draft forward
+    # Speculative Streaming draft (Sec. 3.2, timing only): one draft forward
     # carries, for each of the kappa branches, the main stream (the branch
     # root) and gamma lookahead streams, stream j attending to the verified
     # prefix and to streams 1..j: a chain of gamma + 1 slots per branch, i.e.

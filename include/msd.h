@@ -19,7 +19,7 @@
  *   msd_kv_commit        Sec. 2: commit the accepted tokens (and the root) to
  *                        the KV cache; everything else rolls back.
  *   msd_reuse_select     Sec. 3.1 reuse criterion and next-window selection,
- *                        App. C fallback statistics.
+ *                        App. E fallback statistics.
  *
  * Conventions
  *  - Every pointer marked "device" is HIP device memory owned by the caller;
@@ -293,7 +293,7 @@ msd_status msd_kv_commit(const msd_model* model, msd_kv_cache* kv, const msd_blo
 /*
  * Reuse criterion and next-window selection (Sec. 3.1, "Verification vs.
  * reuse criterion" and "Operational selection of the next window") with the
- * fallback statistics of App. C.
+ * fallback statistics of App. E.
  *
  * The hypothesis tree T_t is what the draft built from the early-exit top-k
  * roots: node i at depth d_i (roots d = 1) holds the token for position
@@ -312,7 +312,7 @@ enum { MSD_NEXT_BRANCH = 0, MSD_NEXT_CONTINUE = 1, MSD_NEXT_FRESH = 2 };
 /* Running fallback statistics (device memory, zeroed once by the caller and
  * accumulated by every call; calls sharing one must be stream-ordered).
  * One trial = one sequence of one step. FF = fallbacks / trials; the mean
- * overlap mass is omega_sum / omega_trials (App. C: FF <= 1 - Omega). */
+ * overlap mass is omega_sum / omega_trials (App. E: FF <= 1 - Omega). */
 typedef struct {
   uint64_t trials;
   uint64_t fallbacks;        /* F_t = 1: fresh rollout                        */
@@ -334,7 +334,8 @@ typedef struct {
  *            several match), -1 on fallback.
  * Omega (optional, all of logits, lse, ee_ids non-NULL): the overlap mass at
  * the root row, Omega_k = sum over the early-exit top-k ids of
- * softmax(logits)[id] (App. C), fp64 accumulation, written to omega[b] if
+ * softmax(logits)[id] (Sec. 3.1, sampling width at early exit; App. E),
+ * fp64 accumulation, written to omega[b] if
  * omega is non-NULL; logits/lse/ee_ids are the verify call's outputs
  * ([M][vocab], [M], [M][kappa]). stats may be NULL.
  */

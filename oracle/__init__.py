@@ -6,7 +6,7 @@ benchmark's ``cpu_baseline`` leg use it; the product path never does.
 The functions here only marshal arrays into the C oracle and sequence its
 per-layer calls; every number of the verification pass comes from
 ``msdo.c``. The step after acceptance (the Sec. 3.1 reuse criterion over the
-draft's hypothesis tree, the App. C overlap mass) is written at the end of
+draft's hypothesis tree, the App. E overlap mass) is written at the end of
 this file in plain Python and NumPy fp64. The model description and weights
 come from the shared input generator (``synth``), which holds none of the
 method's arithmetic.
@@ -343,7 +343,7 @@ def depths(parent: np.ndarray) -> np.ndarray:
 
 # ---------------------------------------------------------------------------
 # After acceptance: reuse criterion and next-window selection (Sec. 3.1),
-# fallback statistics (App. C). Plain Python over the hypothesis tree (a few
+# fallback statistics (App. E). Plain Python over the hypothesis tree (a few
 # hundred nodes at most), NumPy fp64 for the overlap mass.
 # ---------------------------------------------------------------------------
 NEXT_BRANCH, NEXT_CONTINUE, NEXT_FRESH = 0, 1, 2
@@ -376,7 +376,8 @@ def reuse_select(parent: Sequence[int], tokens: Sequence[int], accepted: Sequenc
 
 
 def overlap_mass(logits_row: np.ndarray, ids: Sequence[int]) -> float:
-    """App. C: Omega_kappa = sum over the early-exit Top-kappa ids of
+    """Sec. 3.1 (sampling width at early exit), App. E: Omega_kappa = sum
+    over the early-exit Top-kappa ids of
     q(y) = Softmax(logits)(y), the final head's next-token law, in fp64."""
     z = np.asarray(logits_row, dtype=np.float64)
     mx = z.max()

@@ -1,5 +1,5 @@
 // Reuse criterion and next-window selection (Sec. 3.1) and the fallback
-// statistics of App. C, after acceptance.
+// statistics of App. E, after acceptance.
 //
 // Per sequence, the corrected prefix Pi+ = (accepted tokens, correction) is
 // looked up among the root-to-depth-tau paths of the hypothesis tree T_t

@@ -399,7 +399,7 @@ def test_early_exit_topk_entry_point(which, M, kappa):
 
 
 def test_tiny_reuse_selection_and_fallback_statistics():
-    """Sec. 3.1 reuse criterion and next-window selection with the App. C
+    """Sec. 3.1 reuse criterion and next-window selection with the App. E
     fallback statistics, through the C ABI, against the oracle. Accept
     outcomes are planted (A cycles through 0..gamma along the chain block,
     corrections drawn), the hypothesis tree (4 chains of gamma + 1 nodes,

@@ -535,6 +535,119 @@ def test_rejection_sampling_reproduces_the_target_law(n_children):
         assert abs(acc - closed) < 4 * np.sqrt(closed * (1 - closed) / N)
 
 
+def _threshold(decide, lo=0.0, hi=1.0, iters=32):
+    """The point t in [lo, hi] where a monotone yes-below / no-above decision
+    of the oracle flips (decide(u) is True for u < t). The uniforms are fp32
+    inputs, so t is resolved to their spacing (2^-24 near 1)."""
+    if not decide(lo):
+        return lo
+    if decide(hi):
+        return hi
+    for _ in range(iters):
+        mid = 0.5 * (lo + hi)
+        if decide(mid):
+            lo = mid
+        else:
+            hi = mid
+    return 0.5 * (lo + hi)
+
+
+def _bins(draw, V, lo=0.0, hi=1.0 - 2.0 ** -24, iters=32):
+    """Measure of {u in [0, 1): draw(u) = y} for every y, for a nondecreasing
+    step function draw (inverse-CDF sampling over ascending ids), by
+    bisection for its breakpoints."""
+    mass = np.zeros(V)
+
+    def rec(a, b, ya, yb):
+        if ya == yb:
+            mass[ya] += b - a
+            return
+        if b - a < 2.0 ** -iters:
+            mass[ya] += (b - a) / 2
+            mass[yb] += (b - a) / 2
+            return
+        m = 0.5 * (a + b)
+        ym = draw(m)
+        rec(a, m, ya, ym)
+        rec(m, b, ym, yb)
+
+    rec(lo, hi, draw(lo), draw(hi))
+    mass[draw(hi)] += 1.0 - hi
+    return mass
+
+
+@pytest.mark.parametrize("n_children", [1, 2, 3])
+def test_rejection_output_law_exact_enumeration(n_children):
+    """Losslessness of REJECTION by exact enumeration (Leviathan et al. 2023,
+    Thm. 1; several children drawn without replacement: recursive rejection,
+    Jeon et al. 2024), with the oracle as a black box: every ordered draw of
+    the children from q is enumerated with its probability; each accept
+    test's outcome is a threshold in its uniform, found by bisection on the
+    oracle's decision; the final draw's bins in u_sample likewise. The law of
+    the first committed token must equal p = Softmax(z) to 1e-6 (the
+    uniforms are fp32: each threshold is resolved to 2^-24)."""
+    import itertools
+    V = 10
+    g = np.random.default_rng(40 + n_children)
+    p = g.dirichlet(np.ones(V))
+    cands = np.array([1, 4, 5, 8])
+    q = synth.dirichlet_rows(g, 0.5, (len(cands),))
+    qd = q.astype(np.float64)
+    n = 1 + n_children
+    parent = np.array([-1] + [0] * n_children)
+    cand_ids = np.tile(cands, (n, 1)).astype(np.int32)
+    cand_q = np.tile(q, (n, 1)).astype(np.float32)
+    logits = np.tile(np.log(p), (n, 1))
+    law = np.zeros(V)
+    for order in itertools.permutations(range(len(cands)), n_children):
+        w, left = 1.0, 1.0
+        for j in order:
+            w *= qd[j] / left
+            left -= qd[j]
+        tok = np.concatenate([[0], cands[list(order)]]).astype(np.int32)
+        u_acc = np.full(n, 0.5, np.float32)
+
+        def run(ua, us0=0.5):
+            us = np.full(n, us0, np.float32)
+            return orc.Oracle.accept(parent, tok, logits, "rejection", 1.0, cand_ids, cand_q,
+                                     ua.astype(np.float32), us)
+
+        reach = w                                   # probability of testing child c
+        for c in range(1, n):
+            def accepted(u, c=c):
+                ua = u_acc.copy()
+                ua[c] = u
+                A, _, path = run(ua)
+                return A >= 1 and path[1] == c
+            alpha = _threshold(accepted)
+            law[tok[c]] += reach * alpha
+            reach *= 1.0 - alpha
+            u_acc[c] = np.float32(min(alpha + (1.0 - alpha) / 2, 1.0 - 2.0 ** -24))
+        if reach > 0:                               # every child rejected: the residual draw
+            law += reach * _bins(lambda u: run(u_acc, u)[1], V)
+    assert abs(law.sum() - 1.0) < 1e-6
+    assert np.max(np.abs(law - p)) < 1e-6, (law, p)
+
+
+def test_match_output_law_exact_enumeration():
+    """MATCH (the paper's sample-and-compare): the first committed token is
+    the draw y = Sample(p, u); its bins in u, found by bisection on the
+    oracle, have the masses p exactly."""
+    V = 10
+    p = np.random.default_rng(50).dirichlet(np.ones(V))
+    parent = np.array([-1, 0, 0])
+    tok = np.array([0, 3, 7], np.int32)
+    logits = np.tile(np.log(p), (3, 1))
+
+    def first(u):
+        A, nxt, path = orc.Oracle.accept(parent, tok, logits, "match", 1.0,
+                                         u_sample=np.array([u, 0.5, 0.5], np.float32))
+        return int(tok[path[1]]) if A >= 1 else nxt
+
+    law = _bins(first, V)
+    assert np.max(np.abs(law - p)) < 1e-6
+
+
 def test_match_rule_reproduces_the_target_law():
     """The paper's sample-and-compare operator: y ~ p, matched against the draft."""
     V = 10

@@ -1,5 +1,5 @@
 """Pins of the oracle's step after acceptance: the Sec. 3.1 reuse criterion /
-next-window selection and the App. C fallback statistics (CPU only)."""
+next-window selection and the App. E fallback statistics (CPU only)."""
 import itertools
 
 import numpy as np
@@ -82,7 +82,7 @@ def _tree_from_roots(roots, depth, vocab):
 
 
 def test_prop1_fallback_nonincreasing_in_kappa():
-    """App. C Prop. 1: with roots = Top-kappa of the early-exit law, every
+    """App. E Prop. 1: with roots = Top-kappa of the early-exit law, every
     event that reuses at kappa1 reuses at any kappa2 >= kappa1; at kappa = |V|
     no tau = 1 event falls back."""
     V, depth = 12, 3
@@ -106,7 +106,7 @@ def test_prop1_fallback_nonincreasing_in_kappa():
 
 @pytest.mark.parametrize("kappa", [1, 2, 4, 8])
 def test_tau1_fallback_probability_is_one_minus_omega(kappa):
-    """App. C: when the first draft token is rejected, reuse succeeds iff the
+    """App. E: when the first draft token is rejected, reuse succeeds iff the
     correction y ~ q lies in Top-kappa of the early-exit law, so
     P(F = 1 | A = 0) = 1 - Omega_kappa exactly (enumerated over y)."""
     V = 16
