@@ -134,8 +134,10 @@ typedef struct msd_model msd_model;
  * The tensors stay caller-owned and must outlive the model.
  * Weight layout: the call rearranges every projection matrix (q, k, v, o,
  * gate, up, down and the LM head; the embedding too when tied) IN PLACE into
- * the library's fragment-major layout (16-row groups stored as consecutive
- * 1 KB MFMA operands along K), so the verify pass reads HBM sequentially.
+ * the library's k-step-major layout (for each 32-column k-step, the 1 KB
+ * MFMA operands of all 16-row groups one after the other), so the
+ * workgroups of a projection, which advance through K together, read one
+ * contiguous window of HBM.
  * After the call those tensors are opaque to the caller, and one set of
  * tensors can back only one model. The call synchronises the device and
  * briefly allocates a temporary buffer the size of the largest matrix.

@@ -6,9 +6,10 @@
 // Mapping (gfx950, wave64, MFMA 16x16x32 bf16 -> fp32):
 //  * a workgroup of NW waves owns a 64-column output tile and one of
 //    `splits` contiguous slices of K; its waves cut the slice in NW k-ranges;
-//  * weights are stored fragment-major (1 KB MFMA operands one after the
-//    other along K, per 16-row group) and each wave keeps D k-steps of them
-//    in flight, straight from HBM into the MFMA;
+//  * weights are stored k-step-major (for each k-step, the 1 KB MFMA operands
+//    of all 16-row groups one after the other), so the workgroups working at
+//    the same k-step read one contiguous window of HBM; each wave keeps D
+//    k-steps in flight with non-temporal loads, straight into the MFMA;
 //  * the input is an activation image: X (times the pre-norm gain) already
 //    split into bf16 hi + lo parts in MFMA operand order by the kernel that
 //    produced it, so the loop is loads and MFMAs only (two MFMAs per weight
@@ -28,16 +29,15 @@
 namespace msd {
 namespace {
 
-// Weights live in the fragment-major layout (see repack_kernel): the 16-row
-// group G of a matrix is a contiguous run of K/32 fragments of 1 KB, fragment
-// ks holding rows 16G..16G+15 x columns 32ks..32ks+31 in MFMA operand order
-// (lane l: row 16G + l%16, columns 32ks + 8(l/16) .. +8).
+// Weights live in the k-step-major layout (see repack_kernel): fragment
+// (G, ks) of a matrix with NG = rows / 16 groups is the 1 KB block at element
+// (ks * NG + G) * 512, holding rows 16G..16G+15 x columns 32ks..32ks+31 in
+// MFMA operand order (lane l: row 16G + l%16, columns 32ks + 8(l/16) .. +8).
 // A tile is JT sub-tiles of 16 output columns (JT = 4: 64 columns; JT = 8:
-// 128 columns, for the SwiGLU FFN up projection with up to 3 row tiles).
-// Returns the lane's pointer into fragment 0 of the group feeding sub-tile j.
+// 128 columns). Returns the lane's pointer into fragment (group, 0) of the
+// group feeding sub-tile j.
 template <int JT>
 __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t, int j, int lane) {
-  const size_t run = (size_t)(a.K >> 5) * 512;  // elements per 16-row group
   const uint16_t* base;
   int grp;
   if (a.map == MAP_QKV) {  // JT = 4: a tile is 32 rotary pairs of one head
@@ -64,7 +64,23 @@ __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t,
     const int last = (a.N >> 4) - 1;  // padding columns re-read a valid group; output masked
     if (grp > last) grp = last;
   }
-  return base + (size_t)grp * run + lane * 8;
+  return base + (size_t)grp * 512 + lane * 8;
+}
+
+// Elements from one k-step of tile t's weights to the next: the group count
+// of its matrix times 512 (the same for every sub-tile of a tile: one
+// matrix, or the gate and up matrices of equal size).
+__device__ __forceinline__ uint32_t weight_kstride(const GemmArgs& a, int t) {
+  int rows;
+  if (a.map == MAP_QKV) {
+    const int hh = t / (a.head_dim >> 6);
+    rows = (hh < a.n_heads ? a.n_heads : a.n_kv_heads) * a.head_dim;
+  } else if (a.map == MAP_GATEUP) {
+    rows = a.N >> 1;
+  } else {
+    rows = a.N;
+  }
+  return (uint32_t)(rows >> 4) * 512u;
 }
 
 // Logical output column (index into biases and LayerNorm column sums) of
@@ -535,8 +551,9 @@ struct KStep {
 
 template <int MT, int NW, int EPI, int JT>
 __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
-  // k-steps in flight per wave
-  constexpr int D = MT == 1 ? (JT == 8 ? 7 : (NW == 8 ? 4 : 8)) : (MT <= 3 ? 4 : 2);
+  // k-steps in flight per wave (measured per shape with the k-step-major
+  // layout: the 2-wave 128-column FFN up tiles 5, 8-wave split-K tiles 6)
+  constexpr int D = MT == 1 ? (JT == 8 ? (NW == 2 ? 5 : 4) : (NW == 8 ? 4 : 8)) : (MT <= 3 ? 4 : 2);
   constexpr int RCH = MT < 3 ? MT : 3;  // row tiles per LDS reduction round
   constexpr int TF = MT * JT * 256;     // floats of one tile's partial
   __shared__ floatx4 red[NW][RCH * JT][kWave];
@@ -558,6 +575,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   const uint16_t* wp[JT];
 #pragma unroll
   for (int j = 0; j < JT; ++j) wp[j] = weight_frag<JT>(a, t, j, lane);
+  const size_t kstr = __builtin_amdgcn_readfirstlane(weight_kstride(a, t));
   const uint16_t* ap = a.a_img + lane * 8;
 
   // one row tile: the epilogue's inputs are loaded ahead (the sequence
@@ -585,7 +603,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   KStep<MT, JT> st[D];
   auto issue = [&](KStep<MT, JT>& x, int k) {
 #pragma unroll
-    for (int j = 0; j < JT; ++j) x.w[j] = load16(wp[j] + (size_t)k * 512);
+    for (int j = 0; j < JT; ++j) x.w[j] = load_nt(wp[j] + (size_t)k * kstr);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const uint16_t* p = ap + (size_t)(k * MT + mt) * 1024;
@@ -787,7 +805,8 @@ hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  if (a.jt == 8) {  // 128-column tiles: the SwiGLU FFN up projection, up to 3 row tiles
+  if (a.jt == 8) {  // 128-column tiles: the SwiGLU FFN up projection (up to 3
+                    // row tiles, 2 waves) and the LM head (one row tile, 4 waves)
     if constexpr (EPI == EPI_SWIGLU) {
       if (a.waves != 2) return hipErrorInvalidValue;
       switch (a.MT) {
@@ -796,6 +815,10 @@ hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
         case 3: return launch_cfg<3, 2, EPI, 8>(a, s);
         default: return hipErrorInvalidValue;
       }
+    }
+    if constexpr (EPI == EPI_HEAD) {
+      if (a.waves != 4 || a.MT != 1) return hipErrorInvalidValue;
+      return launch_cfg<1, 4, EPI, 8>(a, s);
     }
     return hipErrorInvalidValue;
   }
@@ -810,18 +833,19 @@ hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
   }
 }
 
-// Row-major [rows][K] -> fragment-major: fragment (G, ks) holds rows
-// 16G..16G+15, columns 32ks..32ks+31, lane l taking row 16G + l%16 and
-// columns 32ks + 8(l/16) .. +8 (16 bytes); dst is written sequentially.
+// Row-major [rows][K] -> k-step-major fragments: fragment (G, ks), G < NG =
+// rows / 16, at (ks * NG + G) * 512 elements holds rows 16G..16G+15, columns
+// 32ks..32ks+31, lane l taking row 16G + l%16 and columns 32ks + 8(l/16) .. +8
+// (16 bytes); dst is written sequentially.
 __global__ __launch_bounds__(256) void repack_kernel(const uint16_t* __restrict__ src,
                                                      uint16_t* __restrict__ dst, int64_t rows,
                                                      int32_t K) {
-  const int64_t KS = K >> 5;
-  const int64_t total = (rows >> 4) * KS * 64;  // 16-byte lane chunks
+  const int64_t NG = rows >> 4;
+  const int64_t total = NG * (K >> 5) * 64;  // 16-byte lane chunks
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * blockDim.x) {
     const int64_t lanes = i & 63, frag = i >> 6;
-    const int64_t G = frag / KS, ks = frag - G * KS;
+    const int64_t ks = frag / NG, G = frag - ks * NG;
     const int64_t row = 16 * G + (lanes & 15), col = 32 * ks + 8 * (lanes >> 4);
     *reinterpret_cast<u32x4*>(dst + i * 8) = *reinterpret_cast<const u32x4*>(src + row * K + col);
   }

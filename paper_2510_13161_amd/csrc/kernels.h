@@ -53,7 +53,8 @@ struct GemmArgs {
   int32_t M, MT, K, N;     // N = logical output columns (padding masked)
   int32_t n_tiles, splits, waves;
   int32_t jt;              // 16-column sub-tiles per tile: 4 (64 columns), or 8 (128
-                           // columns: EPI_SWIGLU with up to 3 row tiles and 2 waves)
+                           // columns: EPI_SWIGLU with up to 3 row tiles and 2 waves,
+                           // EPI_HEAD with one row tile and 4 waves)
   int32_t map;
   const uint16_t* w0;
   const uint16_t* w1;
@@ -93,7 +94,7 @@ struct GemmArgs {
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
-// row-major [rows][K] -> fragment-major weight layout (src and dst distinct)
+// row-major [rows][K] -> k-step-major weight fragments (src and dst distinct)
 hipError_t launch_repack(const uint16_t* src, uint16_t* dst, int64_t rows, int32_t K,
                          hipStream_t s);
 // c[n] = sum_k W[n][k] g[k] (and e with b) for a row-major bf16 matrix, fp64
@@ -110,7 +111,7 @@ struct RowsArgs {
   const int32_t* tokens;   // [M]
   const uint16_t* embed;   // [V][d]
   const uint16_t* pos_embed;
-  int32_t embed_frag;      // the table is stored fragment-major (tied LM head)
+  int32_t embed_frag;      // the table is stored as k-step-major fragments (tied LM head)
   const int32_t* len;
   int32_t M, MT, d, n_slots, max_positions, vocab;
   uint32_t* status;        // MSD_DEV_TOKEN on an id outside [0, vocab)

@@ -120,6 +120,11 @@ Shapes shapes(const msd_model* m, int M) {
     s.up.n_tiles = c.d_ffn / 64;
     s.up.waves = 2;
   }
+  if (one) {  // the LM head at one row tile: 128-column tiles of 4 waves
+    s.head.jt = 8;
+    s.head.n_tiles = (c.vocab + 2 * kTileN - 1) / (2 * kTileN);
+    s.head.waves = 4;
+  }
   for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head})
     g->splits = splits_for(m, g->n_tiles, g->K, g->waves);
   return s;
@@ -501,7 +506,7 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
     m->up_e.assign(c.n_layers, nullptr);
   }
 
-  // every projection matrix goes fragment-major, in place, through one
+  // every projection matrix goes k-step-major, in place, through one
   // temporary buffer as large as the largest matrix
   {
     struct Mat {

@@ -66,10 +66,11 @@ __global__ __launch_bounds__(256) void rows_kernel(RowsArgs a) {
     for (int c = 0; c < 8; ++c) {
       const int col = 64 * tt + 8 * c;
       if (a.embed_frag) {
-        // row tok of a fragment-major table: 8 consecutive columns per 16 bytes
-        const size_t run = (size_t)(a.d >> 5) * 512;
+        // row tok of a k-step-major fragment table (vocab / 16 groups per
+        // k-step): 8 consecutive columns per 16 bytes
+        const size_t ng = (size_t)(a.vocab >> 4);
         const int ks = col >> 5, lane = (tok & 15) + 16 * ((col >> 3) & 3);
-        w[c] = *reinterpret_cast<const u32x4*>(a.embed + (size_t)(tok >> 4) * run + (size_t)ks * 512 +
+        w[c] = *reinterpret_cast<const u32x4*>(a.embed + ((size_t)ks * ng + (size_t)(tok >> 4)) * 512 +
                                                lane * 8);
       } else {
         w[c] = *reinterpret_cast<const u32x4*>(a.embed + (size_t)tok * a.d + col);
