@@ -241,7 +241,8 @@ __device__ __forceinline__ floatx4 load_coherent4(__amdgpu_buffer_rsrc_t r, uint
   return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kCoherentPolicy);
 }
 
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+// z * sigmoid(z) with the hardware exponential and reciprocal
+__device__ __forceinline__ float silu(float z) { return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 // Activation image: the split-bf16 MFMA operand form of an activation matrix
 // [M][K] (M padded to 16 MT rows). Element order [K/32][MT][2][64][8]: k-step

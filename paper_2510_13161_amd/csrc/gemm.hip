@@ -122,8 +122,24 @@ struct EpiIn {
 };
 
 template <int EPI>
-__device__ __forceinline__ constexpr bool has_norm() {
+__host__ __device__ constexpr bool has_norm() {
   return EPI != EPI_RESID;
+}
+
+// One row tile with a pre-norm (the QKV and FFN up projections): one more
+// wave, beside the NW that stream the weights, loads the producer's row
+// summaries at the start of the kernel and leaves each row's (mu, r) in
+// LDS, so the epilogue after the k-loop has no summary loads or merge left.
+// Only for 2- and 8-wave workgroups: a fifth wave would cost the 4-wave ones
+// (the LM head, wide one-row-tile GEMMs) their second workgroup per compute
+// unit, or registers.
+template <int MT, int NW, int EPI>
+__host__ __device__ constexpr bool norm_helper() {
+  return MT == 1 && (NW == 2 || NW == 8) && has_norm<EPI>() && EPI != EPI_HEAD;
+}
+template <int MT, int NW, int EPI>
+__host__ __device__ constexpr int block_waves() {
+  return NW + (norm_helper<MT, NW, EPI>() ? 1 : 0);
 }
 
 // committed length of the sequence of row m (EPI_QKV)
@@ -131,12 +147,12 @@ __device__ __forceinline__ int row_len(const GemmArgs& a, int m) {
   return a.len[(m < a.M ? m : 0) / a.n_slots];
 }
 
-template <int EPI>
+template <int EPI, bool NORM = true>
 __device__ __forceinline__ void epi_load(const GemmArgs& a, int t, int mt, EpiIn& in) {
   const int lane = threadIdx.x & 63, q = lane >> 4, r16 = lane & 15;
   const int m = 16 * mt + r16;
   const int mm = m < a.M ? m : 0;
-  if constexpr (has_norm<EPI>()) {
+  if constexpr (has_norm<EPI>() && NORM) {
     if (a.norm.kind != 0) {
 #pragma unroll
       for (int i = 0; i < kMaxPer; ++i) {
@@ -492,7 +508,7 @@ __device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
 // when they were loaded ahead (one row tile), otherwise they are loaded here.
 template <int EPI, int JT, bool AHEAD>
 __device__ __forceinline__ void epilogue_tile(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[JT],
-                                              float* scr, const EpiIn& in1) {
+                                              float* scr, const EpiIn& in1, const float2* norm_sh = nullptr) {
   EpiIn inl;
   if constexpr (!AHEAD) {
     if constexpr (EPI == EPI_QKV) inl.L = row_len(a, 16 * mt + (threadIdx.x & 15));
@@ -500,7 +516,15 @@ __device__ __forceinline__ void epilogue_tile(const GemmArgs& a, int t, int mt, 
   }
   const EpiIn& in = AHEAD ? in1 : inl;
   float mu = 0.0f, rs = 1.0f;
-  if constexpr (has_norm<EPI>()) norm_finish(a, in, mu, rs);
+  if constexpr (has_norm<EPI>()) {
+    if (norm_sh) {  // the helper wave's (mu, r) of this lane's row
+      const float2 v = norm_sh[threadIdx.x & 15];
+      mu = v.x;
+      rs = v.y;
+    } else {
+      norm_finish(a, in, mu, rs);
+    }
+  }
   if constexpr (EPI == EPI_SWIGLU) epi_swiglu<JT>(a, t, mt, acc, scr, mu, rs);
   else if constexpr (EPI == EPI_HEAD) epi_head<JT>(a, t, mt, acc, mu, rs);
   else if constexpr (JT == 4) {  // the other epilogues run on 64-column tiles only
@@ -550,7 +574,7 @@ struct KStep {
 };
 
 template <int MT, int NW, int EPI, int JT>
-__global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
+__global__ __launch_bounds__((64 * block_waves<MT, NW, EPI>())) void gemm_kernel(GemmArgs a) {
   // k-steps in flight per wave (measured per shape with the k-step-major
   // layout: the 2-wave 128-column FFN up tiles 5, 8-wave split-K tiles 6)
   constexpr int D = MT == 1 ? (JT == 8 ? (NW == 2 ? 5 : 4) : (NW == 8 ? 4 : 8)) : (MT <= 3 ? 4 : 2);
@@ -561,11 +585,26 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   // tiles' epilogues
   __shared__ __attribute__((aligned(16))) float scr_all[(MT == 1 ? 1 : NW) * 16 * kScr];
   __shared__ int last_sh;
+  __shared__ float2 norm_sh[16];  // helper wave: (mu, r) per row of the tile
 
   const int lane = threadIdx.x & 63;
   // wave-uniform (scalar) so that the k-loop branches and waits are scalar
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int t = blockIdx.x / a.splits, s = blockIdx.x - t * a.splits;
+  if constexpr (norm_helper<MT, NW, EPI>()) {
+    if (wave == NW) {
+      // the row norm, while the other waves stream; then the reduction's two
+      // barriers, which order the LDS write before the epilogue reads it
+      EpiIn hin;
+      epi_load<EPI>(a, t, 0, hin);
+      float mu, rs;
+      norm_finish(a, hin, mu, rs);
+      if (lane < 16) norm_sh[lane] = make_float2(mu, rs);
+      __syncthreads();
+      __syncthreads();
+      return;
+    }
+  }
   const int KS = a.K >> 5;
   const int kb0 = (int)((int64_t)KS * s / a.splits), ke0 = (int)((int64_t)KS * (s + 1) / a.splits);
   const int nk = ke0 - kb0;
@@ -654,7 +693,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
   }
 
   if constexpr (MT == 1) {
-    if (wave == 0) epi_load<EPI>(a, t, 0, in1);
+    if (wave == 0) epi_load<EPI, !norm_helper<MT, NW, EPI>()>(a, t, 0, in1);
   }
 
   if constexpr (MT == 1) {
@@ -726,7 +765,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
       if (lane == 0) counter_reset(&a.counters[t]);
     }
 
-    epilogue_tile<EPI, JT, true>(a, t, 0, acc[0], scr_all, in1);
+    epilogue_tile<EPI, JT, true>(a, t, 0, acc[0], scr_all, in1,
+                                 norm_helper<MT, NW, EPI>() ? norm_sh : nullptr);
   } else {
     // Several row tiles: row tile mt belongs to wave mt % NW, which sums it
     // over the waves (in wave order, as above) and finishes it, so that the
@@ -799,7 +839,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(GemmArgs a) {
 
 template <int MT, int NW, int EPI, int JT>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_kernel<MT, NW, EPI, JT>), dim3(a.n_tiles * a.splits), dim3(64 * NW), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<MT, NW, EPI, JT>), dim3(a.n_tiles * a.splits),
+                     dim3(64 * block_waves<MT, NW, EPI>()), 0, s, a);
   return hipGetLastError();
 }
 
