@@ -147,20 +147,26 @@ __device__ __forceinline__ int row_len(const GemmArgs& a, int m) {
   return a.len[(m < a.M ? m : 0) / a.n_slots];
 }
 
+// the pre-norm summaries of the lane's row of row tile mt
+__device__ __forceinline__ void stats_load(const GemmArgs& a, int mt, EpiIn& in) {
+  const int lane = threadIdx.x & 63, q = lane >> 4, r16 = lane & 15;
+  const int m = 16 * mt + r16;
+  const int mm = m < a.M ? m : 0;
+  if (a.norm.kind != 0) {
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+      const int tt = q + 4 * i;
+      in.st[i] = a.norm.stats[(size_t)(tt < a.norm.tiles ? tt : 0) * a.M + mm];
+    }
+  }
+}
+
 template <int EPI, bool NORM = true>
 __device__ __forceinline__ void epi_load(const GemmArgs& a, int t, int mt, EpiIn& in) {
   const int lane = threadIdx.x & 63, q = lane >> 4, r16 = lane & 15;
   const int m = 16 * mt + r16;
   const int mm = m < a.M ? m : 0;
-  if constexpr (has_norm<EPI>() && NORM) {
-    if (a.norm.kind != 0) {
-#pragma unroll
-      for (int i = 0; i < kMaxPer; ++i) {
-        const int tt = q + 4 * i;
-        in.st[i] = a.norm.stats[(size_t)(tt < a.norm.tiles ? tt : 0) * a.M + mm];
-      }
-    }
-  }
+  if constexpr (has_norm<EPI>() && NORM) stats_load(a, mt, in);
   if constexpr (EPI == EPI_RESID) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -506,13 +512,15 @@ __device__ void epi_head(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
 
 // The epilogue of row tile mt of a finished tile; `in` holds its inputs
 // when they were loaded ahead (one row tile), otherwise they are loaded here.
-template <int EPI, int JT, bool AHEAD>
+// norm_sh: (mu, r) of the tile's 16 rows, already merged (then NLDS: the
+// summaries are not loaded)
+template <int EPI, int JT, bool AHEAD, bool NLDS = false>
 __device__ __forceinline__ void epilogue_tile(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[JT],
                                               float* scr, const EpiIn& in1, const float2* norm_sh = nullptr) {
   EpiIn inl;
   if constexpr (!AHEAD) {
     if constexpr (EPI == EPI_QKV) inl.L = row_len(a, 16 * mt + (threadIdx.x & 15));
-    epi_load<EPI>(a, t, mt, inl);
+    epi_load<EPI, !NLDS>(a, t, mt, inl);
   }
   const EpiIn& in = AHEAD ? in1 : inl;
   float mu = 0.0f, rs = 1.0f;
@@ -540,9 +548,10 @@ __device__ __forceinline__ void epilogue_tile(const GemmArgs& a, int t, int mt, 
 // little); each pass picks its row tile's accumulators by compile-time
 // index, so acc is never indexed at run time (that would put it in scratch
 // memory).
-template <int MT, int EPI, int JT>
+template <int MT, int EPI, int JT, bool NLDS = false>
 __device__ __forceinline__ void epilogue_rows(const GemmArgs& a, int t, const floatx4 (&acc)[MT][JT],
-                                              float* scr, int owner, int owners) {
+                                              float* scr, int owner, int owners,
+                                              const float2* norm_sh = nullptr) {
   if constexpr (MT <= 5) {
     // up to 5 row tiles: unrolled (the compact loop below costs these
     // variants their second wave per SIMD)
@@ -550,7 +559,7 @@ __device__ __forceinline__ void epilogue_rows(const GemmArgs& a, int t, const fl
     for (int mt = 0; mt < MT; ++mt) {
       if (mt % owners != owner) continue;
       EpiIn none;
-      epilogue_tile<EPI, JT, false>(a, t, mt, acc[mt], scr, none);
+      epilogue_tile<EPI, JT, false, NLDS>(a, t, mt, acc[mt], scr, none, NLDS ? norm_sh + 16 * mt : nullptr);
     }
     return;
   }
@@ -563,7 +572,7 @@ __device__ __forceinline__ void epilogue_rows(const GemmArgs& a, int t, const fl
 #pragma unroll
         for (int j = 0; j < JT; ++j) cur[j] = acc[mm][j];
     EpiIn none;
-    epilogue_tile<EPI, JT, false>(a, t, mt, cur, scr, none);
+    epilogue_tile<EPI, JT, false, NLDS>(a, t, mt, cur, scr, none, NLDS ? norm_sh + 16 * mt : nullptr);
   }
 }
 
@@ -837,6 +846,238 @@ __global__ __launch_bounds__((64 * block_waves<MT, NW, EPI>())) void gemm_kernel
   }
 }
 
+// ---------------------------------------------------------------------------
+// Many row tiles: the activation shared through LDS
+// ---------------------------------------------------------------------------
+// From about 5 row tiles on, a k-step of a 64-column tile is 2 MT JT MFMAs
+// against JT weight fragments and 2 MT activation fragments: the activation
+// bytes outnumber the weight bytes, and a wave that kept both in flight for
+// an HBM round trip would run out of registers. Here a workgroup owns NW
+// adjacent 64-column tiles, one per compute wave, and one split of K. One
+// more wave copies each k-step of the activation image (its 2 MT fragments
+// are contiguous) into a ring of R LDS slots with direct global-to-LDS
+// loads, P k-steps ahead of the compute waves, which read their operands
+// from there: the image crosses L2 once per NW tiles instead of once per
+// tile, and the compute waves keep only weights in flight (D k-steps). One
+// barrier per k-step passes the slots between the loader and the compute
+// waves. Split-K as above, per tile: the last split to arrive sums all
+// splits in split order.
+template <int MT>
+__host__ __device__ constexpr int rows_depth() {  // weight k-steps in flight per compute wave
+  return MT >= 9 ? 3 : 6;
+}
+// Activation k-steps in flight: the loader waits on its own load counter
+// (at most 63 loads outstanding) for the oldest, one 1 KB load per fragment.
+template <int MT>
+__host__ __device__ constexpr int rows_ahead() {
+  return 63 / (2 * MT) + 1 < 8 ? 63 / (2 * MT) + 1 : 8;
+}
+
+// s_waitcnt for at most n outstanding vector-memory loads (expcnt and
+// lgkmcnt not waited on)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt field is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int MT, int NW, int EPI>
+__global__ __launch_bounds__(64 * (NW + 1)) void gemm_rows_kernel(GemmArgs a) {
+  constexpr int JT = 4;
+  constexpr int D = rows_depth<MT>();
+  constexpr int P = rows_ahead<MT>();
+  constexpr int R = P + 1;    // LDS slots: a slot is refilled one barrier after its last read
+  constexpr int AF = 2 * MT;  // activation fragments of a k-step: hi and lo of each row tile
+  constexpr int TF = MT * JT * 256;
+  __shared__ __attribute__((aligned(16))) u32x4 act_sh[R][AF][kWave];
+  __shared__ __attribute__((aligned(16))) float scr_all[NW * 16 * kScr];
+  __shared__ float2 norm_sh[MT * 16];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tw = blockIdx.x / a.splits, s = blockIdx.x - tw * a.splits;
+  const int KS = a.K >> 5;
+  const int kb = (int)((int64_t)KS * s / a.splits), ke = (int)((int64_t)KS * (s + 1) / a.splits);
+  const int n = ke - kb;
+  // k-steps from a point rotated by the workgroup's tiles (fixed per tile:
+  // sums stay bit-reproducible), so that concurrent workgroups read different
+  // k-steps of the shared image
+  const int rot = n > 0 ? (int)((int64_t)n * (tw & 15) / 16) : 0;
+  auto kstep = [&](int i) {
+    const int x = i + rot;
+    return kb + (x >= n ? x - n : x);
+  };
+
+  if (wave == NW) {
+    // the loader: k-step i goes to slot i % R, issued after barrier i - P
+    // (which the compute waves pass only once done with step i - P - 1, the
+    // slot's previous content) and complete before barrier i
+    const uint16_t* src = a.a_img + lane * 8;
+    auto fetch = [&](int i, int slot) {
+      const uint16_t* p = src + (size_t)kstep(i) * AF * 512;
+#pragma unroll
+      for (int f = 0; f < AF; ++f)
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(p + f * 512),
+                                         (__attribute__((address_space(3))) void*)&act_sh[slot][f][0], 16, 0,
+                                         0);
+    };
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+      if (p < n) fetch(p, p);
+    int slot_in = P % R;
+    for (int i = 0; i < n; ++i) {
+      // steps i + 1 .. i + P - 1 may stay in flight
+      if (i + P <= n) wait_vmcnt<(P - 1) * AF>();
+      else wait_vmcnt<0>();
+      lds_barrier();
+      if (i + P < n) {
+        fetch(i + P, slot_in);
+        slot_in = slot_in + 1 == R ? 0 : slot_in + 1;
+      }
+    }
+    return;
+  }
+
+  // the pre-norm's (mu, r) of every row, merged once before the k-loop (the
+  // summaries' registers are free then) and left in LDS for the epilogues;
+  // barrier 0 below orders the writes before any read
+  if constexpr (has_norm<EPI>()) {
+    for (int mt = wave; mt < MT; mt += NW) {
+      EpiIn nin;
+      stats_load(a, mt, nin);
+      float mu, rs;
+      norm_finish(a, nin, mu, rs);
+      if (lane < 16) norm_sh[16 * mt + lane] = make_float2(mu, rs);
+    }
+  }
+
+  const int t = tw * NW + wave;
+  const int tc = t < a.n_tiles ? t : a.n_tiles - 1;  // a wave past the last tile streams a valid one
+  const uint16_t* wp[JT];
+#pragma unroll
+  for (int j = 0; j < JT; ++j) wp[j] = weight_frag<JT>(a, tc, j, lane);
+  const size_t kstr = __builtin_amdgcn_readfirstlane(weight_kstride(a, tc));
+
+  floatx4 acc[MT][JT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int j = 0; j < JT; ++j) acc[mt][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  bf16x8 w[D][JT];
+  auto issue = [&](bf16x8(&x)[JT], int i) {
+    const int k = kstep(i);
+#pragma unroll
+    for (int j = 0; j < JT; ++j) x[j] = load_nt(wp[j] + (size_t)k * kstr);
+  };
+  auto compute = [&](const bf16x8(&x)[JT], int slot) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const bf16x8 ah = __builtin_bit_cast(bf16x8, act_sh[slot][2 * mt][lane]);
+      const bf16x8 al = __builtin_bit_cast(bf16x8, act_sh[slot][2 * mt + 1][lane]);
+#pragma unroll
+      for (int j = 0; j < JT; ++j) {
+        acc[mt][j] = mfma16x16x32(x[j], ah, acc[mt][j]);
+        acc[mt][j] = mfma16x16x32(x[j], al, acc[mt][j]);
+      }
+    }
+  };
+  // D k-steps of weights in flight; as in gemm_kernel the steady-state loop
+  // runs only over batches whose D refills are all real (a branch in it
+  // would make every batch wait for all its loads). Each k-step starts at a
+  // barrier, after which its activation is in its slot.
+  int slot = 0;
+  auto step = [&](const bf16x8(&x)[JT]) {
+    lds_barrier();
+    compute(x, slot);
+    slot = slot + 1 == R ? 0 : slot + 1;
+  };
+  if (n >= D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) issue(w[d], d);
+    const int nfull = (n - D) / D;
+    for (int b = 0; b < nfull; ++b) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        step(w[d]);
+        issue(w[d], (b + 1) * D + d);
+      }
+    }
+    const int done = (nfull + 1) * D, r = n - done;  // 0 <= r < D
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      step(w[d]);
+      if (d < r) issue(w[d], done + d);
+    }
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+      if (d < r) step(w[d]);
+  } else {
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+      if (d < n) issue(w[d], d);
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+      if (d < n) step(w[d]);
+  }
+  if (t >= a.n_tiles) return;
+
+  if (a.splits > 1) {
+    const __amdgpu_buffer_rsrc_t part =
+        coherent_region(a.partial + (size_t)t * a.splits * TF, (uint32_t)(a.splits * TF * 4));
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < JT; ++j)
+        store_coherent4(part, (uint32_t)((s * TF + (mt * JT + j) * 256 + lane * 4) * 4), acc[mt][j]);
+    drain_stores();
+    int old = 0;
+    if (lane == 0) old = counter_add(&a.counters[t], 1);
+    old = __shfl(old, 0);
+    if (old != a.splits - 1) return;
+    // the sum in split order, this split's own tile from registers; the
+    // other splits' tiles of MC row tiles at a time in flight
+    constexpr int MC = 3;
+#pragma unroll
+    for (int m0 = 0; m0 < MT; m0 += MC) {
+      floatx4 sum[MC][JT];
+#pragma unroll
+      for (int c = 0; c < MC; ++c)
+#pragma unroll
+        for (int j = 0; j < JT; ++j) sum[c][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int sp = 0; sp < a.splits; ++sp) {
+        floatx4 pv[MC][JT];
+#pragma unroll
+        for (int c = 0; c < MC; ++c)
+#pragma unroll
+          for (int j = 0; j < JT; ++j) {
+            const int mt = m0 + c < MT ? m0 + c : m0;
+            pv[c][j] = sp == s ? acc[mt][j]
+                               : load_coherent4(part, (uint32_t)((sp * TF + (mt * JT + j) * 256 + lane * 4) * 4));
+          }
+#pragma unroll
+        for (int c = 0; c < MC; ++c)
+#pragma unroll
+          for (int j = 0; j < JT; ++j) sum[c][j] += pv[c][j];
+      }
+#pragma unroll
+      for (int c = 0; c < MC; ++c)
+        if (m0 + c < MT)
+#pragma unroll
+          for (int j = 0; j < JT; ++j) acc[m0 + c][j] = sum[c][j];
+    }
+    if (lane == 0) counter_reset(&a.counters[t]);
+  }
+  epilogue_rows<MT, EPI, JT, has_norm<EPI>()>(a, t, acc, scr_all + wave * 16 * kScr, 0, 1, norm_sh);
+}
+
+template <int MT, int NW, int EPI>
+hipError_t launch_rows(const GemmArgs& a, hipStream_t s) {
+  const int wgs = (a.n_tiles + NW - 1) / NW;
+  hipLaunchKernelGGL((gemm_rows_kernel<MT, NW, EPI>), dim3(wgs * a.splits), dim3(64 * (NW + 1)), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int MT, int NW, int EPI, int JT>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((gemm_kernel<MT, NW, EPI, JT>), dim3(a.n_tiles * a.splits),
@@ -864,6 +1105,14 @@ hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
   }
   if (a.jt != 4) return hipErrorInvalidValue;
+  if (a.wg_tiles > 1) {  // tiles per workgroup, the activation shared through LDS
+    if (a.wg_tiles != 4) return hipErrorInvalidValue;
+    switch (a.MT) {
+      case 5: return launch_rows<5, 4, EPI>(a, s);
+      case 9: return launch_rows<9, 4, EPI>(a, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (a.MT) {
     case 1: return a.waves == 8 ? launch_cfg<1, 8, EPI, 4>(a, s) : launch_cfg<1, 4, EPI, 4>(a, s);
     case 2: return launch_cfg<2, 4, EPI, 4>(a, s);

@@ -35,6 +35,8 @@ struct msd_model {
   const float* head_e = nullptr;
   int32_t target_wgs = 240;        // split-K sizing target (workgroups per GEMM)
   int32_t waves = 8;               // waves of a split-K workgroup for one row tile
+  int32_t rows_max_splits = 2;     // splits of K at most, 5 or more row tiles
+  int32_t rows_min_tiles = 256;    // 64-column tiles of a GEMM that takes the LDS-shared kernel
   int32_t attn_spans = 0;          // attention spans per chunk (0: chosen per call; 1: one-span kernel)
   int32_t prof_class = -1;         // instrumentation (msd_set_profile)
   std::vector<hipEvent_t> prof_begin, prof_end;
@@ -83,8 +85,25 @@ int splits_for(const msd_model* m, int n_tiles, int K, int waves) {
   return want < max_s ? want : max_s;
 }
 
+// Many row tiles, wide GEMMs (the FFN up projection, the LM head): 4 tiles a
+// workgroup sharing the activation through LDS, splits of K so that about
+// kRowsWaves compute waves (one per 64-column tile and split) share the chip,
+// at most m->rows_max_splits (each split adds an fp32 partial of the whole
+// [M][64] tile to write and read back) and at least 8 k-steps a split.
+// Narrower GEMMs would need many splits for as many waves; they keep the
+// split-K kernel.
+constexpr int kRowsMinMT = 5;
+constexpr int kRowsWaves = 1024;
+int rows_splits(const msd_model* m, int n_tiles, int K) {
+  int want = (kRowsWaves + n_tiles / 2) / n_tiles;
+  want = std::min(want, m->rows_max_splits);
+  want = std::min(want, (K / 32) / 8);
+  return want < 1 ? 1 : want;
+}
+
 struct GemmShape {
   int n_tiles, K, splits, waves, jt;
+  int wg_tiles = 1;
 };
 
 struct Shapes {
@@ -125,8 +144,16 @@ Shapes shapes(const msd_model* m, int M) {
     s.head.n_tiles = (c.vocab + 2 * kTileN - 1) / (2 * kTileN);
     s.head.waves = 4;
   }
-  for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head})
-    g->splits = splits_for(m, g->n_tiles, g->K, g->waves);
+  for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
+    if (row_tiles(M) >= kRowsMinMT && g->n_tiles >= m->rows_min_tiles) {
+      // 4 tiles a workgroup, the activation shared in LDS
+      g->wg_tiles = 4;
+      g->waves = 4;
+      g->splits = rows_splits(m, g->n_tiles, g->K);
+    } else {
+      g->splits = splits_for(m, g->n_tiles, g->K, g->waves);
+    }
+  }
   return s;
 }
 
@@ -276,6 +303,7 @@ GemmArgs gemm_base(const msd_model* m, const Layout& L, char* ws, int M, const G
   g.splits = sh.splits;
   g.waves = sh.waves;
   g.jt = sh.jt;
+  g.wg_tiles = sh.wg_tiles;
   g.partial = reinterpret_cast<float*>(ws + L.partial);
   g.counters = reinterpret_cast<int32_t*>(ws + L.counters);
   g.n_heads = m->cfg.n_heads;
@@ -444,6 +472,14 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
   if (const char* e = getenv("MSD_GEMM_WAVES")) {
     const int v = atoi(e);
     if (v == 4 || v == 8) m->waves = v;
+  }
+  if (const char* e = getenv("MSD_ROWS_MIN_TILES")) {
+    const int v = atoi(e);
+    if (v >= 1) m->rows_min_tiles = v;
+  }
+  if (const char* e = getenv("MSD_ROWS_MAX_SPLITS")) {
+    const int v = atoi(e);
+    if (v >= 1 && v <= 64) m->rows_max_splits = v;
   }
   if (const char* e = getenv("MSD_ATTN_SPANS")) {
     const int v = atoi(e);

@@ -600,6 +600,33 @@ def test_attention_streaming_ragged_batch(monkeypatch, spans):
     print("streaming ragged:", _compare(case, gr, seqs))
 
 
+# widths whose tile counts are not multiples of 4: 15 q/k/v tiles, 5 output
+# and down tiles, 34 SwiGLU up tiles, 63 LM-head tiles (the last half padding)
+ROWS_RAGGED = synth.ModelShape("rows_ragged", 2, 320, 5, 5, 64, 1088, 4000, rope_theta=1.0e4)
+
+
+@pytest.mark.parametrize("shape,batch,splits", [("tiny", 16, 1), ("tiny", 16, 4), ("tiny", 6, 2),
+                                                ("ragged", 16, 2)])
+def test_rows_kernel_every_gemm(monkeypatch, shape, batch, splits):
+    """The GEMM kernel that shares the activation through LDS (4 tiles a
+    workgroup, a loader wave) forced on every GEMM: nine row tiles (batch 16
+    x 9 slots) and five (batch 6: 54 rows, padding rows in the last tile),
+    whole-K and split-K (the FFN down projection, 32 k-steps, takes the
+    splits); and widths whose last workgroup has waves past the matrix."""
+    _torch()
+    monkeypatch.setenv("MSD_ROWS_MIN_TILES", "1")
+    monkeypatch.setenv("MSD_ROWS_MAX_SPLITS", str(splits))
+    model = synth.TINY if shape == "tiny" else ROWS_RAGGED
+    w = synth.WORKLOADS["14b_batch16"].with_model(model, batch=batch, ctx=(1, 600), ee_layer=1, kappa=4,
+                                                  seed=31 + batch + splits)
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run(ee=True)
+    weights = synth.host_weights(case.shape, w.seed)
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b, weights=weights) for b in range(w.batch)}
+    print("rows kernel", shape, batch, splits, _compare(case, gr, seqs))
+
+
 def test_attention_streaming_max_tree(monkeypatch):
     """Streaming kernel forced on the 64-slot tree (4 query tiles: a group of
     3 and a group of 1) after a 700-key context: the tree rows straddle two
