@@ -132,15 +132,57 @@ def cpu_baseline(shape, w, reps: int = 3) -> dict:
         o.accept(si.parent, si.tokens[0], z)
     timed += time.perf_counter() - t0
     timed /= reps
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    threads = orc.omp_threads()
     per_seq_tokens = w.n_slots - 1
+    single = tiny_single_thread(orc, synth)
     return {"value": round(per_seq_tokens / timed, 4), "unit": "verified tokens/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu": cpu_model(), "host_cpus": os.cpu_count(),
+            "tiny_single_thread": single,
             "sample": (f"one whole step of sequence 0 of {w.name} ({per_seq_tokens} draft tokens): "
                        f"embed, {shape.n_layers} decoder layers, early-exit and final heads, "
-                       f"top-{w.kappa}, acceptance; fp64 C oracle, OpenMP; each call run {reps} "
-                       f"times, {timed * reps:.1f} s of oracle time in all, {timed:.2f} s per step "
-                       "(weight generation untimed)")}
+                       f"top-{w.kappa}, acceptance; fp64 C oracle, OpenMP over {threads} threads; "
+                       f"each call run {reps} times, {timed * reps:.1f} s of oracle time in all, "
+                       f"{timed:.2f} s per step (weight generation untimed)")}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def tiny_single_thread(orc, synth, seconds: float = 1.0) -> dict:
+    """The oracle on one thread over whole steps of the tiny chain workload
+    (2 layers, d 256, 4 drafts), repeated for about `seconds`."""
+    w = synth.WORKLOADS["tiny_chain"]
+    shape = w.model
+    si = synth.step_inputs(w)
+    L = int(si.ctx_len[0])
+    o = orc.Oracle(shape, synth.host_weights(shape, w.seed))
+    cc = {l: (synth.host_ctx(shape, w.seed, l, "k", 0, L), synth.host_ctx(shape, w.seed, l, "v", 0, L))
+          for l in range(shape.n_layers)}
+    pos = L + orc.depths(si.parent)
+    before = orc.omp_threads()
+    orc.set_omp_threads(1)
+    try:
+        n, t0 = 0, time.perf_counter()
+        while True:
+            r = o.forward(si.tokens[0], pos, si.parent, lambda l: cc[l], L, ee_layer=w.ee_layer)
+            orc.Oracle.topk(o.head(r.x_ee), w.kappa)
+            o.accept(si.parent, si.tokens[0], r.logits)
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                break
+    finally:
+        orc.set_omp_threads(before)
+    return {"value": round((w.n_slots - 1) * n / el, 2), "unit": "verified tokens/s", "cores": 1,
+            "steps": n, "workload": w.name}
 
 
 def copy_calibration(nbytes: int) -> None:

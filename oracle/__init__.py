@@ -84,6 +84,23 @@ def lib():
     return _lib
 
 
+def _gomp():
+    lib()  # the oracle's OpenMP runtime is the one it was linked with
+    g = ctypes.CDLL("libgomp.so.1")
+    g.omp_get_max_threads.restype = ctypes.c_int
+    g.omp_set_num_threads.argtypes = [ctypes.c_int]
+    return g
+
+
+def omp_threads() -> int:
+    """Threads the oracle's parallel loops use."""
+    return int(_gomp().omp_get_max_threads())
+
+
+def set_omp_threads(n: int) -> None:
+    _gomp().omp_set_num_threads(int(n))
+
+
 def _p(a: Optional[np.ndarray]):
     return None if a is None else a.ctypes.data
 
