@@ -143,7 +143,8 @@ typedef struct msd_model msd_model;
  * briefly allocates a temporary buffer the size of the largest matrix.
  * Launch-shape overrides, read from the environment here (tuning and tests;
  * results differ only by floating-point summation order): MSD_GEMM_TARGET_WGS
- * (split-K sizing, workgroups per GEMM), MSD_GEMM_WAVES (4 or 8) and
+ * (split-K sized for about this many workgroups per GEMM; unset, for the
+ * best balance over the device's compute units), MSD_GEMM_WAVES (4 or 8) and
  * MSD_ATTN_SPANS (256-key spans per attention workgroup: 1 forces the
  * one-span kernel, 2 or more the streaming one; unset, chosen per call),
  * MSD_ROWS_MIN_TILES (from 5 row tiles on, GEMMs with at least this many

@@ -33,7 +33,8 @@ struct msd_model {
   std::vector<const float*> qkv_c, qkv_e, up_c, up_e;
   const float* head_c = nullptr;
   const float* head_e = nullptr;
-  int32_t target_wgs = 240;        // split-K sizing target (workgroups per GEMM)
+  int32_t n_cus = 256;             // compute units of the model's device
+  int32_t target_wgs = 0;          // > 0: split-K sized for about this many workgroups
   int32_t waves = 8;               // waves of a split-K workgroup for one row tile
   int32_t rows_max_splits = 2;     // splits of K at most, 5 or more row tiles
   int32_t rows_min_tiles = 256;    // 64-column tiles of a GEMM that takes the LDS-shared kernel
@@ -74,15 +75,37 @@ inline int row_tiles(int M) {
   return mt <= 3 ? mt : (mt <= 5 ? 5 : kMaxMT);
 }
 
-// Split-K factor: about target_wgs workgroups per GEMM, each wave keeping at
-// least 2 k-steps.
-int splits_for(const msd_model* m, int n_tiles, int K, int waves) {
+// Split-K factor. A workgroup streams its 1/s of a tile at about one
+// compute unit's rate, so a GEMM lasts as long as its busiest unit: W =
+// n_tiles * s workgroups over C units put ceil(W / C) of them on one unit.
+// s maximises the balance W / (C ceil(W / C)) (the smallest s on a tie),
+// with W <= per_cu * C (more would wait for a second dispatch round; per_cu
+// is how many of these workgroups a unit holds) unless s = 1, and at least
+// 2 k-steps per wave. Measured: 66B tree, O and down projections (144
+// tiles, 4-wave workgroups, two a unit) 2 -> 3 splits: 59.4 -> 46.4 us and
+// 207.6 -> 154.2 us. m->target_wgs > 0 instead asks for about that many
+// workgroups (tuning).
+int splits_for(const msd_model* m, int n_tiles, int K, int waves, int per_cu) {
   const int ks = K / 32;
   int max_s = ks / (2 * waves);
   if (max_s < 1) max_s = 1;
-  int want = (m->target_wgs + n_tiles / 2) / n_tiles;
-  if (want < 1) want = 1;
-  return want < max_s ? want : max_s;
+  if (m->target_wgs > 0) {
+    const int want = std::max(1, (m->target_wgs + n_tiles / 2) / n_tiles);
+    return want < max_s ? want : max_s;
+  }
+  const int64_t C = m->n_cus;
+  int best = 1;
+  double best_bal = 0.0;
+  for (int s = 1; s <= max_s; ++s) {
+    const int64_t W = (int64_t)n_tiles * s;
+    if (s > 1 && W > (int64_t)per_cu * C) break;
+    const double bal = (double)W / (double)(C * ((W + C - 1) / C));
+    if (bal > best_bal + 1e-9) {
+      best = s;
+      best_bal = bal;
+    }
+  }
+  return best;
 }
 
 // Many row tiles, wide GEMMs (the FFN up projection, the LM head): 4 tiles a
@@ -132,7 +155,7 @@ Shapes shapes(const msd_model* m, int M) {
   s.head.K = c.d_model;
   for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
     g->jt = 4;
-    g->waves = one && g->n_tiles < m->target_wgs ? m->waves : 4;
+    g->waves = one && g->n_tiles < m->n_cus ? m->waves : 4;
   }
   if (row_tiles(M) <= 3 && c.act == MSD_ACT_SWIGLU && c.d_ffn % 64 == 0) {
     s.up.jt = 8;
@@ -151,7 +174,7 @@ Shapes shapes(const msd_model* m, int M) {
       g->waves = 4;
       g->splits = rows_splits(m, g->n_tiles, g->K);
     } else {
-      g->splits = splits_for(m, g->n_tiles, g->K, g->waves);
+      g->splits = splits_for(m, g->n_tiles, g->K, g->waves, g->waves >= 8 ? 1 : 2);
     }
   }
   return s;
@@ -465,6 +488,12 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
       for (int s : {MSD_L_BQ, MSD_L_BK, MSD_L_BV, MSD_L_BO, MSD_L_B_UP, MSD_L_B_DOWN})
         m->t[MSD_TENSOR_INDEX(l, s)] = nullptr;
   if (c.pos != MSD_POS_LEARNED) m->t[MSD_T_POS_EMBED] = nullptr;
+  {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+      m->n_cus = cus;
+  }
   if (const char* e = getenv("MSD_GEMM_TARGET_WGS")) {
     const int v = atoi(e);
     if (v > 0) m->target_wgs = v;
