@@ -147,9 +147,11 @@ typedef struct msd_model msd_model;
  * best balance over the device's compute units), MSD_GEMM_WAVES (4 or 8) and
  * MSD_ATTN_SPANS (256-key spans per attention workgroup: 1 forces the
  * one-span kernel, 2 or more the streaming one; unset, chosen per call),
- * MSD_ROWS_MIN_TILES (from 5 row tiles on, GEMMs with at least this many
- * 64-column tiles, 256 unset, run the kernel that shares the activation
- * through LDS) and MSD_ROWS_MAX_SPLITS (its splits of K at most, 2 unset). */
+ * MSD_ROWS_MIN_MT (row tiles from which GEMMs with 256 or more 64-column
+ * tiles may run the kernel that shares the activation through LDS: 3 unset;
+ * it runs where its workgroups balance the compute units),
+ * MSD_ROWS_MIN_TILES (forces that kernel on GEMMs with at least this many
+ * tiles) and MSD_ROWS_MAX_SPLITS (its splits of K at most, 2 unset). */
 msd_status msd_model_create(const msd_model_config* cfg, const void* const* tensors,
                             int32_t n_tensors, msd_model** out);
 void msd_model_destroy(msd_model* model);

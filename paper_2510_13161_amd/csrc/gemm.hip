@@ -849,10 +849,10 @@ __global__ __launch_bounds__((64 * block_waves<MT, NW, EPI>())) void gemm_kernel
 // ---------------------------------------------------------------------------
 // Many row tiles: the activation shared through LDS
 // ---------------------------------------------------------------------------
-// From about 5 row tiles on, a k-step of a 64-column tile is 2 MT JT MFMAs
-// against JT weight fragments and 2 MT activation fragments: the activation
-// bytes outnumber the weight bytes, and a wave that kept both in flight for
-// an HBM round trip would run out of registers. Here a workgroup owns NW
+// With several row tiles a k-step of a 64-column tile is 2 MT JT MFMAs
+// against JT weight fragments and 2 MT activation fragments: from 3 row
+// tiles on the activation bytes outnumber the weight bytes, and a wave that
+// kept both in flight for an HBM round trip would run out of registers. Here a workgroup owns NW
 // adjacent 64-column tiles, one per compute wave, and one split of K. One
 // more wave copies each k-step of the activation image (its 2 MT fragments
 // are contiguous) into a ring of R LDS slots with direct global-to-LDS
@@ -1108,6 +1108,8 @@ hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
   if (a.wg_tiles > 1) {  // tiles per workgroup, the activation shared through LDS
     if (a.wg_tiles != 4) return hipErrorInvalidValue;
     switch (a.MT) {
+      case 2: return launch_rows<2, 4, EPI>(a, s);
+      case 3: return launch_rows<3, 4, EPI>(a, s);
       case 5: return launch_rows<5, 4, EPI>(a, s);
       case 9: return launch_rows<9, 4, EPI>(a, s);
       default: return hipErrorInvalidValue;

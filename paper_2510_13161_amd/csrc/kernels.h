@@ -55,7 +55,7 @@ struct GemmArgs {
   int32_t jt;              // 16-column sub-tiles per tile: 4 (64 columns), or 8 (128
                            // columns: EPI_SWIGLU with up to 3 row tiles and 2 waves,
                            // EPI_HEAD with one row tile and 4 waves)
-  int32_t wg_tiles;        // 64-column tiles per workgroup: 1, or 4 (5 or 9 row tiles:
+  int32_t wg_tiles;        // 64-column tiles per workgroup: 1, or 4 (2 to 9 row tiles:
                            // one compute wave a tile and a wave that stages the
                            // activation through LDS; then waves = 4)
   int32_t map;

@@ -38,6 +38,8 @@ struct msd_model {
   int32_t waves = 8;               // waves of a split-K workgroup for one row tile
   int32_t rows_max_splits = 2;     // splits of K at most, 5 or more row tiles
   int32_t rows_min_tiles = 256;    // 64-column tiles of a GEMM that takes the LDS-shared kernel
+  int32_t rows_min_mt = 3;         // row tiles from which it does
+  bool rows_forced = false;        // MSD_ROWS_MIN_TILES set: no balance check
   int32_t attn_spans = 0;          // attention spans per chunk (0: chosen per call; 1: one-span kernel)
   int32_t prof_class = -1;         // instrumentation (msd_set_profile)
   std::vector<hipEvent_t> prof_begin, prof_end;
@@ -108,20 +110,35 @@ int splits_for(const msd_model* m, int n_tiles, int K, int waves, int per_cu) {
   return best;
 }
 
-// Many row tiles, wide GEMMs (the FFN up projection, the LM head): 4 tiles a
-// workgroup sharing the activation through LDS, splits of K so that about
-// kRowsWaves compute waves (one per 64-column tile and split) share the chip,
-// at most m->rows_max_splits (each split adds an fp32 partial of the whole
-// [M][64] tile to write and read back) and at least 8 k-steps a split.
-// Narrower GEMMs would need many splits for as many waves; they keep the
-// split-K kernel.
-constexpr int kRowsMinMT = 5;
-constexpr int kRowsWaves = 1024;
+// Several row tiles, wide GEMMs (256 or more 64-column tiles): 4 tiles a
+// workgroup sharing the activation through LDS (one workgroup per compute
+// unit: its LDS ring and registers). Splits of K as for split-K above, for
+// the best balance of ceil(n_tiles / 4) * s workgroups over the units within
+// one dispatch round, at most m->rows_max_splits (each split adds an fp32
+// partial of the whole [M][64] tile to write and read back) and at least 8
+// k-steps a split. Returns 0 where no split count balances at least 3/4 of
+// the units (then the split-K kernel runs), unless the kernel is forced.
+// Measured: 14B batch 16, FFN up (108 workgroup tiles, 2 splits) and LM head
+// (594, whole K): 136.8 -> 97.0 us and 740 -> 522 us; 66B tree (3 row
+// tiles): QKV (108, 2 splits) 118.3 -> 97.2 us, LM head (197) 224.8 -> 166.5
+// us, but its FFN up (144 workgroup tiles: 0.56 at best) 168.8 -> 177.7 us.
 int rows_splits(const msd_model* m, int n_tiles, int K) {
-  int want = (kRowsWaves + n_tiles / 2) / n_tiles;
-  want = std::min(want, m->rows_max_splits);
-  want = std::min(want, (K / 32) / 8);
-  return want < 1 ? 1 : want;
+  const int64_t C = m->n_cus;
+  const int64_t wg = (n_tiles + 3) / 4;
+  const int max_s = std::max(1, std::min(m->rows_max_splits, (K / 32) / 8));
+  int best = 1;
+  double best_bal = 0.0;
+  for (int s = 1; s <= max_s; ++s) {
+    const int64_t W = wg * s;
+    if (s > 1 && W > C) break;
+    const double bal = (double)W / (double)(C * ((W + C - 1) / C));
+    if (bal > best_bal + 1e-9) {
+      best = s;
+      best_bal = bal;
+    }
+  }
+  if (m->rows_forced) return best;
+  return best_bal >= 0.75 ? best : 0;
 }
 
 struct GemmShape {
@@ -168,11 +185,13 @@ Shapes shapes(const msd_model* m, int M) {
     s.head.waves = 4;
   }
   for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
-    if (row_tiles(M) >= kRowsMinMT && g->n_tiles >= m->rows_min_tiles) {
-      // 4 tiles a workgroup, the activation shared in LDS
+    const int rs = row_tiles(M) >= m->rows_min_mt && g->n_tiles >= m->rows_min_tiles && g->jt == 4
+                       ? rows_splits(m, g->n_tiles, g->K)
+                       : 0;
+    if (rs > 0) {  // 4 tiles a workgroup, the activation shared in LDS
       g->wg_tiles = 4;
       g->waves = 4;
-      g->splits = rows_splits(m, g->n_tiles, g->K);
+      g->splits = rs;
     } else {
       g->splits = splits_for(m, g->n_tiles, g->K, g->waves, g->waves >= 8 ? 1 : 2);
     }
@@ -502,9 +521,16 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
     const int v = atoi(e);
     if (v == 4 || v == 8) m->waves = v;
   }
+  if (const char* e = getenv("MSD_ROWS_MIN_MT")) {
+    const int v = atoi(e);
+    if (v >= 2 && v <= kMaxMT) m->rows_min_mt = v;
+  }
   if (const char* e = getenv("MSD_ROWS_MIN_TILES")) {
     const int v = atoi(e);
-    if (v >= 1) m->rows_min_tiles = v;
+    if (v >= 1) {
+      m->rows_min_tiles = v;
+      m->rows_forced = true;
+    }
   }
   if (const char* e = getenv("MSD_ROWS_MAX_SPLITS")) {
     const int v = atoi(e);

@@ -606,14 +606,17 @@ ROWS_RAGGED = synth.ModelShape("rows_ragged", 2, 320, 5, 5, 64, 1088, 4000, rope
 
 
 @pytest.mark.parametrize("shape,batch,splits", [("tiny", 16, 1), ("tiny", 16, 4), ("tiny", 6, 2),
-                                                ("ragged", 16, 2)])
+                                                ("ragged", 16, 2), ("tiny", 4, 2), ("ragged", 2, 4)])
 def test_rows_kernel_every_gemm(monkeypatch, shape, batch, splits):
     """The GEMM kernel that shares the activation through LDS (4 tiles a
-    workgroup, a loader wave) forced on every GEMM: nine row tiles (batch 16
-    x 9 slots) and five (batch 6: 54 rows, padding rows in the last tile),
-    whole-K and split-K (the FFN down projection, 32 k-steps, takes the
-    splits); and widths whose last workgroup has waves past the matrix."""
+    workgroup, a loader wave) forced on every GEMM of 64-column tiles: nine
+    row tiles (batch 16 x 9 slots), five (batch 6: 54 rows, padding rows in
+    the last tile), three (batch 4) and two (batch 2; the SwiGLU up
+    projection keeps its 128-column tiles below four row tiles), whole-K and
+    split-K (the FFN down projection, 32 k-steps, takes the splits); and
+    widths whose last workgroup has waves past the matrix."""
     _torch()
+    monkeypatch.setenv("MSD_ROWS_MIN_MT", "2")
     monkeypatch.setenv("MSD_ROWS_MIN_TILES", "1")
     monkeypatch.setenv("MSD_ROWS_MAX_SPLITS", str(splits))
     model = synth.TINY if shape == "tiny" else ROWS_RAGGED
