@@ -864,7 +864,13 @@ __global__ __launch_bounds__((64 * block_waves<MT, NW, EPI>())) void gemm_kernel
 // splits in split order.
 template <int MT>
 __host__ __device__ constexpr int rows_depth() {  // weight k-steps in flight per compute wave
-  return MT >= 9 ? 3 : 6;
+  return MT >= 9 ? 3 : (MT >= 5 ? 6 : 4);
+}
+// Up to 3 row tiles two workgroups share a compute unit (their LDS rings fit
+// together): 10 waves, so up to 3 on a SIMD, 168 VGPRs each at most.
+template <int MT>
+__host__ __device__ constexpr int rows_waves_per_simd() {
+  return MT <= 3 ? 3 : 1;
 }
 // Activation k-steps in flight: the loader waits on its own load counter
 // (at most 63 loads outstanding) for the oldest, one 1 KB load per fragment.
@@ -882,7 +888,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 template <int MT, int NW, int EPI>
-__global__ __launch_bounds__(64 * (NW + 1)) void gemm_rows_kernel(GemmArgs a) {
+__global__ __launch_bounds__(64 * (NW + 1), rows_waves_per_simd<MT>()) void gemm_rows_kernel(GemmArgs a) {
   constexpr int JT = 4;
   constexpr int D = rows_depth<MT>();
   constexpr int P = rows_ahead<MT>();

@@ -36,7 +36,7 @@ struct msd_model {
   int32_t n_cus = 256;             // compute units of the model's device
   int32_t target_wgs = 0;          // > 0: split-K sized for about this many workgroups
   int32_t waves = 8;               // waves of a split-K workgroup for one row tile
-  int32_t rows_max_splits = 2;     // splits of K at most, 5 or more row tiles
+  int32_t rows_max_splits = 4;     // its splits of K at most
   int32_t rows_min_tiles = 256;    // 64-column tiles of a GEMM that takes the LDS-shared kernel
   int32_t rows_min_mt = 3;         // row tiles from which it does
   bool rows_forced = false;        // MSD_ROWS_MIN_TILES set: no balance check
@@ -112,17 +112,19 @@ int splits_for(const msd_model* m, int n_tiles, int K, int waves, int per_cu) {
 
 // Several row tiles, wide GEMMs (256 or more 64-column tiles): 4 tiles a
 // workgroup sharing the activation through LDS (one workgroup per compute
-// unit: its LDS ring and registers). Splits of K as for split-K above, for
-// the best balance of ceil(n_tiles / 4) * s workgroups over the units within
-// one dispatch round, at most m->rows_max_splits (each split adds an fp32
-// partial of the whole [M][64] tile to write and read back) and at least 8
-// k-steps a split. Returns 0 where no split count balances at least 3/4 of
-// the units (then the split-K kernel runs), unless the kernel is forced.
-// Measured: 14B batch 16, FFN up (108 workgroup tiles, 2 splits) and LM head
-// (594, whole K): 136.8 -> 97.0 us and 740 -> 522 us; 66B tree (3 row
-// tiles): QKV (108, 2 splits) 118.3 -> 97.2 us, LM head (197) 224.8 -> 166.5
-// us, but its FFN up (144 workgroup tiles: 0.56 at best) 168.8 -> 177.7 us.
-int rows_splits(const msd_model* m, int n_tiles, int K) {
+// unit from 5 row tiles on, by its LDS ring and registers; two up to 3).
+// Splits of K as for split-K above, for the best balance of
+// ceil(n_tiles / 4) * s workgroups over the units within one dispatch
+// round, at most m->rows_max_splits (each split adds an fp32 partial of the
+// whole [M][64] tile to write and read back) and at least 8 k-steps a
+// split. Returns 0 where no split count balances at least 3/4 of the units
+// (then the split-K kernel runs), unless the kernel is forced. Measured:
+// 14B batch 16, FFN up (108 workgroup tiles, 2 splits) and LM head (594,
+// whole K): 136.8 -> 97.0 us and 740 -> 522 us; 66B tree (3 row tiles, one
+// workgroup a unit then): QKV (108, 2 splits) 118.3 -> 97.2 us, LM head
+// (197) 224.8 -> 166.5 us, its FFN up (144 workgroup tiles: 0.56 at best)
+// 168.8 -> 177.7 us.
+int rows_splits(const msd_model* m, int n_tiles, int K, int per_cu) {
   const int64_t C = m->n_cus;
   const int64_t wg = (n_tiles + 3) / 4;
   const int max_s = std::max(1, std::min(m->rows_max_splits, (K / 32) / 8));
@@ -130,7 +132,7 @@ int rows_splits(const msd_model* m, int n_tiles, int K) {
   double best_bal = 0.0;
   for (int s = 1; s <= max_s; ++s) {
     const int64_t W = wg * s;
-    if (s > 1 && W > C) break;
+    if (s > 1 && W > per_cu * C) break;
     const double bal = (double)W / (double)(C * ((W + C - 1) / C));
     if (bal > best_bal + 1e-9) {
       best = s;
@@ -186,7 +188,7 @@ Shapes shapes(const msd_model* m, int M) {
   }
   for (GemmShape* g : {&s.qkv, &s.o, &s.up, &s.down, &s.head}) {
     const int rs = row_tiles(M) >= m->rows_min_mt && g->n_tiles >= m->rows_min_tiles && g->jt == 4
-                       ? rows_splits(m, g->n_tiles, g->K)
+                       ? rows_splits(m, g->n_tiles, g->K, row_tiles(M) <= 3 ? 2 : 1)
                        : 0;
     if (rs > 0) {  // 4 tiles a workgroup, the activation shared in LDS
       g->wg_tiles = 4;
