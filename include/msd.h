@@ -147,6 +147,8 @@ typedef struct msd_model msd_model;
  * best balance over the device's compute units), MSD_GEMM_WAVES (4 or 8) and
  * MSD_ATTN_SPANS (256-key spans per attention workgroup: 1 forces the
  * one-span kernel, 2 or more the streaming one; unset, chosen per call),
+ * MSD_ATTN_DEFER (the attention's chunk merge in a kernel of its own: 1
+ * always, 0 never; unset, from 6 chunks on),
  * MSD_ROWS_MIN_MT (row tiles from which GEMMs with 256 or more 64-column
  * tiles may run the kernel that shares the activation through LDS: 3 unset;
  * it runs where its workgroups balance the compute units),

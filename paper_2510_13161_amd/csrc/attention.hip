@@ -439,7 +439,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
     publish_tile<HD>(region_all, ml_sh, o, mx, ls);
     merge_waves<HD>(a, region_all, ml_sh, b, kvh, qt, Qn, nch, c, pbase, pco);
   }
-  if (nch == 1) return;
+  if (nch == 1 || a.defer) return;
   merge_chunks<HD>(a, &last, a.counters + ((size_t)b * a.n_kv_heads + kvh) * QG + qgi, b, kvh, qt0, qt1, Qn,
                    nch, pbase, pco);
 }
@@ -681,9 +681,59 @@ __global__ __launch_bounds__(256, 1) void attn_stream_kernel(AttnArgs a) {
     publish_tile<HD>(region_all, ml_sh, o[t], mrun[t], lrun[t]);
     merge_waves<HD>(a, region_all, ml_sh, b, kvh, qt0 + t, Qn, nch, c, pbase, pco);
   }
-  if (nch == 1) return;
+  if (nch == 1 || a.defer) return;
   merge_chunks<HD>(a, &last, a.counters + ((size_t)b * a.n_kv_heads + kvh) * QG + qgi, b, kvh, qt0,
                    qt0 + ntile, Qn, nch, pbase, pco);
+}
+
+// The chunk merge as a kernel of its own (AttnArgs::defer): one thread per
+// (sequence, kv head, query, 4 output dims) of every sequence with more than
+// one chunk, the running merge of merge_chunks in chunk order (the same
+// arithmetic, so the same bits), output written into the image. The kernel
+// boundary orders the chunks' partials before these loads, so the chunk
+// workgroups need no drain, counter or last-arrival pass.
+template <int HD>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+  constexpr int C4 = HD / 4;
+  constexpr int MB = 8;
+  const int G = a.n_heads / a.n_kv_heads, ns = a.n_slots, Qn = G * ns;
+  const int b = blockIdx.z, kvh = blockIdx.y;
+  const int x = blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= Qn * C4) return;
+  const int T = a.len[b] + ns;
+  if (T > a.capacity) return;  // flagged by the attention kernel
+  const int nch = (T + a.nb * kAttnChunk - 1) / (a.nb * kAttnChunk);
+  if (nch <= 1) return;        // written by its only chunk
+  const int qg = x / C4, c4 = x - qg * C4;
+  const size_t pbase = ((size_t)b * a.n_kv_heads + kvh) * a.max_chunks;
+  float M = -INFINITY, S = 0.0f, o4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int c0 = 0; c0 < nch; c0 += MB) {
+    float2 ml[MB];
+    floatx4 v[MB];
+#pragma unroll
+    for (int u = 0; u < MB; ++u) {
+      const int cc = c0 + u < nch ? c0 + u : c0;
+      const size_t pidx = (pbase + cc) * Qn + qg;
+      ml[u] = *reinterpret_cast<const float2*>(a.part_ml + 2 * pidx);
+      v[u] = *reinterpret_cast<const floatx4*>(a.part_o + pidx * HD + 4 * c4);
+    }
+#pragma unroll
+    for (int u = 0; u < MB; ++u) {
+      if (c0 + u >= nch || ml[u].x == -INFINITY) continue;
+      const float Mn = fmaxf(M, ml[u].x);
+      const float fa = M == -INFINITY ? 0.0f : exp2_hw(M - Mn);
+      const float fb = exp2_hw(ml[u].x - Mn);
+      S = S * fa + ml[u].y * fb;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o4[e] = o4[e] * fa + v[u][e] * fb;
+      M = Mn;
+    }
+  }
+  const float inv = S > 0.0f ? 1.0f / S : 0.0f;
+  float out[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) out[e] = o4[e] * inv;
+  write_out4<HD>(a, b, kvh, qg, c4, out);
 }
 
 }  // namespace
@@ -720,6 +770,15 @@ hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s) {
     if (multi) hipLaunchKernelGGL((attn_kernel<64, true>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((attn_kernel<64, false>), grid, dim3(256), 0, s, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_merge(int head_dim, const AttnArgs& a, hipStream_t s) {
+  const int qn = a.n_heads / a.n_kv_heads * a.n_slots;
+  const dim3 grid((qn * (head_dim / 4) + 255) / 256, a.n_kv_heads, a.batch);
+  if (head_dim == 128) hipLaunchKernelGGL((attn_merge_kernel<128>), grid, dim3(256), 0, s, a);
+  else if (head_dim == 64) hipLaunchKernelGGL((attn_merge_kernel<64>), grid, dim3(256), 0, s, a);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -154,9 +154,13 @@ struct AttnArgs {
   int32_t nb;               // 256-key spans per workgroup chunk: 1, or more for the
                             // streaming kernel (then q_per_wg <= 3)
   float scale;
+  int32_t defer;            // 1: chunks only publish their partials; a second
+                            // kernel merges them (no in-kernel hand-off)
   Topo topo;
 };
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s);
+// the deferred chunk merge (after launch_attention with a.defer = 1, same args)
+hipError_t launch_attention_merge(int head_dim, const AttnArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // head merge (per row): top-kappa, argmax, logsumexp

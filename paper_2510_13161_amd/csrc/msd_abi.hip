@@ -41,6 +41,7 @@ struct msd_model {
   int32_t rows_min_mt = 3;         // row tiles from which it does
   bool rows_forced = false;        // MSD_ROWS_MIN_TILES set: no balance check
   int32_t attn_spans = 0;          // attention spans per chunk (0: chosen per call; 1: one-span kernel)
+  int32_t attn_defer = -1;         // chunk merge in its own kernel: -1 by chunk count, 0 never, 1 always
   int32_t prof_class = -1;         // instrumentation (msd_set_profile)
   std::vector<hipEvent_t> prof_begin, prof_end;
 };
@@ -337,6 +338,19 @@ AttnShape attn_shape(const msd_model* m, int max_chunks, int n_kv_heads, int bat
   return {attn_q_per_wg(max_chunks, n_kv_heads, batch, q_tiles), 1};
 }
 
+// Chunk merge in a kernel of its own (instead of the last chunk to arrive)
+// from kAttnDeferChunks chunks of the cache's capacity on (m->attn_defer: -1
+// that rule, 0 never, 1 always). Measured: the 14B tree (9 chunks of 2
+// spans) 8.62 -> 8.30 ms per step; where the last-arrival merge is short
+// (the chain's 5 one-span chunks, 2 or 3 chunks at batch 16 and the 66B
+// tree) the extra launch does not pay.
+constexpr int kAttnDeferChunks = 6;
+bool attn_defer(const msd_model* m, int max_chunks, int nb) {
+  const int chunks = (max_chunks + nb - 1) / nb;
+  if (chunks <= 1 || m->attn_defer == 0) return false;
+  return m->attn_defer == 1 || chunks >= kAttnDeferChunks;
+}
+
 GemmArgs gemm_base(const msd_model* m, const Layout& L, char* ws, int M, const GemmShape& sh, int N) {
   GemmArgs g{};
   g.M = M;
@@ -537,6 +551,10 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
   if (const char* e = getenv("MSD_ROWS_MAX_SPLITS")) {
     const int v = atoi(e);
     if (v >= 1 && v <= 64) m->rows_max_splits = v;
+  }
+  if (const char* e = getenv("MSD_ATTN_DEFER")) {
+    const int v = atoi(e);
+    if (v >= -1 && v <= 1) m->attn_defer = v;
   }
   if (const char* e = getenv("MSD_ATTN_SPANS")) {
     const int v = atoi(e);
@@ -839,8 +857,10 @@ msd_status verify_launch(const msd_model* m, msd_kv_cache* kv, const msd_block* 
     aa.nb = ash.nb;
     aa.scale = 1.0f / std::sqrt((float)c.head_dim);
     aa.topo = topo;
+    aa.defer = attn_defer(m, L.max_chunks, ash.nb) ? 1 : 0;
     MSD_HIP(prof_mark(m, MSD_K_ATTN, l, true, stream));
     MSD_HIP(launch_attention(c.head_dim, aa, stream));
+    if (aa.defer) MSD_HIP(launch_attention_merge(c.head_dim, aa, stream));
     MSD_HIP(prof_mark(m, MSD_K_ATTN, l, false, stream));
 
     g = gemm_base(m, L, w, M, s.o, d);

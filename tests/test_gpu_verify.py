@@ -630,6 +630,27 @@ def test_rows_kernel_every_gemm(monkeypatch, shape, batch, splits):
     print("rows kernel", shape, batch, splits, _compare(case, gr, seqs))
 
 
+@pytest.mark.parametrize("spans", [1, 2])
+def test_attention_deferred_merge(monkeypatch, spans):
+    """The attention's chunk merge in a kernel of its own, forced, under both
+    attention kernels (one-span and streaming): a ragged batch (contexts 1
+    to 1000) where some sequences fit one chunk (written by it, skipped by
+    the merge kernel) and others merge up to 4."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_DEFER", "1")
+    monkeypatch.setenv("MSD_ATTN_SPANS", str(spans))
+    w = synth.WORKLOADS["14b_batch16"].with_model(synth.TINY, batch=6, ctx=(1, 1000), ee_layer=1, kappa=4,
+                                                  seed=20)
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run()
+    weights = synth.host_weights(case.shape, w.seed)
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b, weights=weights) for b in range(w.batch)}
+    lens = case.si.ctx_len + w.n_slots
+    assert lens.min() <= 256 * spans < lens.max()
+    print("deferred merge:", _compare(case, gr, seqs))
+
+
 def test_attention_streaming_max_tree(monkeypatch):
     """Streaming kernel forced on the 64-slot tree (4 query tiles: a group of
     3 and a group of 1) after a 700-key context: the tree rows straddle two
