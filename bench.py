@@ -27,6 +27,7 @@ import sys
 import time
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PROFILE_STRIDE = 6     # layers between timed FFN up-projection launches
 METRIC = "verified tokens/sec per verify step + % HBM roofline, 14B-shaped γ=8"
 
@@ -61,6 +62,18 @@ def step_bytes(shape, w, ctx_mean: float) -> dict:
     logits = M * shape.vocab * 4
     return {"weights": layer_w, "heads": 2 * head, "kv": kv_read + kv_write, "logits": logits,
             "total": layer_w + 2 * head + kv_read + kv_write + logits}
+
+
+def step_gemm_flops(shape, w) -> float:
+    """Algorithmic GEMM flops of one step: 2·M per weight of every
+    projection matrix, the LM head twice (attention's score and value
+    products, a few per cent at these shapes, are not counted)."""
+    import re
+    import numpy as np
+    from paper_2510_13161_amd import synth
+    mats = sum(int(np.prod(s.shape)) for s in synth.tensor_specs(shape)
+               if re.match(r"l\d+\.", s.name) and len(s.shape) == 2)
+    return 2.0 * w.rows * (mats + 2 * shape.vocab * shape.d_model)
 
 
 def ffn_up_bytes(shape, M: int) -> int:
@@ -608,6 +621,7 @@ def main():
 
     ctx_mean = float(si.ctx_len.mean()) + (args.warmup + args.steps)  # len grows by 1 per step
     sb = step_bytes(shape, w, ctx_mean)
+    fl = step_gemm_flops(shape, w)
     step_gbs = sb["total"] / (ms * 1e-3) / 1e9
     value = w.draft_tokens / (ms * 1e-3)
     out = {
@@ -624,6 +638,12 @@ def main():
         "step_bytes": sb["total"], "step_hbm_gbs": round(step_gbs, 1),
         "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
         "roofline": roof,
+        # MFMA work: each GEMM runs two bf16 products per weight (the
+        # activation's hi and lo parts), so the issued work is twice the
+        # algorithmic flops; against the dense bf16 MFMA peak
+        "mfma": {"gemm_tflop_per_step": round(fl / 1e12, 4), "issued_tflop_per_step": round(2 * fl / 1e12, 4),
+                 "achieved_tflops": round(2 * fl / (ms * 1e-3) / 1e12, 1), "peak_tflops": MFMA_PEAK_TFLOPS,
+                 "frac": round(2 * fl / (ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS, 4)},
         "ms_to_early_exit": None if t_ee is None else round(t_ee, 4),
         "after_accept": post,
         "setup_s": round(t_setup, 2),

@@ -33,3 +33,14 @@ def test_step_bytes_14b_chain_closed_form():
 
 def test_ffn_up_bytes_14b():
     assert bench.ffn_up_bytes(synth.QWEN14B, 9) == 2 * 13824 * 5120 * 2 + 9 * 5120 * 2 + 9 * 13824 * 2
+
+
+def test_step_gemm_flops_closed_forms():
+    """2·M flops per projection weight, the LM head twice: 14B batch 16
+    (M = 144) and the 66B tree (M = 33, ReLU FFN, no gate)."""
+    d, hq, hk, hd, f, v, n = 5120, 40, 8, 128, 13824, 152064, 48
+    mats = n * (d * hq * hd + 2 * hk * hd * d + hq * hd * d + 3 * f * d) + 2 * v * d
+    assert bench.step_gemm_flops(synth.QWEN14B, synth.WORKLOADS["14b_batch16"]) == 2.0 * 144 * mats
+    d, h, f, v, n = 9216, 72, 36864, 50272, 64
+    mats = n * (4 * d * h * 128 + 2 * f * d) + 2 * v * d
+    assert bench.step_gemm_flops(synth.OPT66B, synth.WORKLOADS["66b_tree"]) == 2.0 * 33 * mats
