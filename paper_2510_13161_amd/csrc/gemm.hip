@@ -1036,6 +1036,7 @@ __global__ __launch_bounds__(64 * (NW + 1), rows_waves_per_simd<MT>()) void gemm
 #pragma unroll
       for (int j = 0; j < JT; ++j)
         store_coherent4(part, (uint32_t)((s * TF + (mt * JT + j) * 256 + lane * 4) * 4), acc[mt][j]);
+    if (a.defer_epi) return;  // gemm_epi_kernel sums the splits and finishes
     drain_stores();
     int old = 0;
     if (lane == 0) old = counter_add(&a.counters[t], 1);
@@ -1077,10 +1078,55 @@ __global__ __launch_bounds__(64 * (NW + 1), rows_waves_per_simd<MT>()) void gemm
   epilogue_rows<MT, EPI, JT, has_norm<EPI>()>(a, t, acc, scr_all + wave * 16 * kScr, 0, 1, norm_sh);
 }
 
+// The split sum and epilogue of gemm_rows_kernel as a kernel of their own
+// (GemmArgs::defer_epi, with splits > 1): one wave per (64-column tile, row
+// tile) sums that row tile's partials in split order and runs its epilogue,
+// so that narrow GEMMs can take many splits of K (enough waves for the MFMA
+// work of 144 rows) without one wave summing and finishing all row tiles of
+// its tile in series.
+template <int MT, int EPI>
+__global__ __launch_bounds__(256) void gemm_epi_kernel(GemmArgs a) {
+  constexpr int JT = 4;
+  constexpr int TF = MT * JT * 256;
+  __shared__ __attribute__((aligned(16))) float scr_all[4 * 16 * kScr];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int u = blockIdx.x * 4 + wave;
+  const int t = u / MT, mt = u - t * MT;
+  if (t >= a.n_tiles) return;
+  const float* part = a.partial + (size_t)t * a.splits * TF + (mt * JT) * 256 + lane * 4;
+  floatx4 acc[JT];
+#pragma unroll
+  for (int j = 0; j < JT; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  constexpr int SB = 4;  // splits' partials in flight
+  for (int sp0 = 0; sp0 < a.splits; sp0 += SB) {
+    floatx4 pv[SB][JT];
+#pragma unroll
+    for (int q = 0; q < SB; ++q) {
+      const int sp = sp0 + q < a.splits ? sp0 + q : sp0;
+#pragma unroll
+      for (int j = 0; j < JT; ++j)
+        pv[q][j] = *reinterpret_cast<const floatx4*>(part + (size_t)sp * TF + j * 256);
+    }
+#pragma unroll
+    for (int q = 0; q < SB; ++q)
+      if (sp0 + q < a.splits)
+#pragma unroll
+        for (int j = 0; j < JT; ++j) acc[j] += pv[q][j];
+  }
+  EpiIn none;
+  epilogue_tile<EPI, JT, false>(a, t, mt, acc, scr_all + wave * 16 * kScr, none);
+}
+
 template <int MT, int NW, int EPI>
 hipError_t launch_rows(const GemmArgs& a, hipStream_t s) {
   const int wgs = (a.n_tiles + NW - 1) / NW;
   hipLaunchKernelGGL((gemm_rows_kernel<MT, NW, EPI>), dim3(wgs * a.splits), dim3(64 * (NW + 1)), 0, s, a);
+  if (a.defer_epi && a.splits > 1) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm_epi_kernel<MT, EPI>), dim3((a.n_tiles * MT + 3) / 4), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -58,6 +58,8 @@ struct GemmArgs {
   int32_t wg_tiles;        // 64-column tiles per workgroup: 1, or 4 (2 to 9 row tiles:
                            // one compute wave a tile and a wave that stages the
                            // activation through LDS; then waves = 4)
+  int32_t defer_epi;       // wg_tiles 4 with splits > 1: partials only; a second kernel
+                           // sums them and runs the epilogue, one wave a row tile
   int32_t map;
   const uint16_t* w0;
   const uint16_t* w1;

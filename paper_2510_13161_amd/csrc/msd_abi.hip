@@ -40,6 +40,8 @@ struct msd_model {
   int32_t rows_min_tiles = 256;    // 64-column tiles of a GEMM that takes the LDS-shared kernel
   int32_t rows_min_mt = 3;         // row tiles from which it does
   bool rows_forced = false;        // MSD_ROWS_MIN_TILES set: no balance check
+  int32_t rows_narrow = 1;         // narrow GEMMs from 5 row tiles on: many splits, deferred epilogue
+                                   // (0 off, 1 large matrices, 2 any)
   int32_t attn_spans = 0;          // attention spans per chunk (0: chosen per call; 1: one-span kernel)
   int32_t attn_defer = -1;         // chunk merge in its own kernel: -1 by chunk count, 0 never, 1 always
   int32_t prof_class = -1;         // instrumentation (msd_set_profile)
@@ -144,9 +146,41 @@ int rows_splits(const msd_model* m, int n_tiles, int K, int per_cu) {
   return best_bal >= 0.75 ? best : 0;
 }
 
+// Narrow GEMMs (fewer tiles than m->rows_min_tiles) from 5 row tiles on:
+// the same kernel with many splits of K, so that the 144-row MFMA work
+// spreads over the chip, and the split sum plus epilogue in a kernel of its
+// own (one wave per row tile) instead of in the last split to arrive; the
+// split count as above, at most kRowsNarrowSplits, for matrices of at least
+// kRowsNarrowMinWeights weights (each split writes and the epilogue kernel
+// reads an fp32 partial of all M rows: 35 MB at 12 splits of a 5120-column
+// output). m->rows_narrow: 0 off, 1 that rule, 2 any size (tests). Measured at 14B batch 16 (µs, GEMM +
+// epilogue kernel against the split-K kernel): QKV 32.6 + 13.6 against
+// 51.7, FFN down 43.8 + 10.2 against 66.4, but the O projection (26M
+// weights, 13 k-steps a split) 34.0 + 10.5 against 36.3.
+constexpr int kRowsNarrowSplits = 16;
+constexpr int64_t kRowsNarrowMinWeights = 32ll << 20;
+int rows_narrow_splits(const msd_model* m, int n_tiles, int K) {
+  const int64_t C = m->n_cus;
+  const int64_t wg = (n_tiles + 3) / 4;
+  const int max_s = std::max(1, std::min(kRowsNarrowSplits, (K / 32) / 8));
+  int best = 1;
+  double best_bal = 0.0;
+  for (int s = 1; s <= max_s; ++s) {
+    const int64_t W = wg * s;
+    if (s > 1 && W > C) break;
+    const double bal = (double)W / (double)(C * ((W + C - 1) / C));
+    if (bal > best_bal + 1e-9) {
+      best = s;
+      best_bal = bal;
+    }
+  }
+  return best;
+}
+
 struct GemmShape {
   int n_tiles, K, splits, waves, jt;
   int wg_tiles = 1;
+  int defer_epi = 0;
 };
 
 struct Shapes {
@@ -195,6 +229,12 @@ Shapes shapes(const msd_model* m, int M) {
       g->wg_tiles = 4;
       g->waves = 4;
       g->splits = rs;
+    } else if (m->rows_narrow && row_tiles(M) >= 5 && g->jt == 4 && g->n_tiles < m->rows_min_tiles &&
+               (m->rows_narrow == 2 || (int64_t)g->n_tiles * kTileN * g->K >= kRowsNarrowMinWeights)) {
+      g->wg_tiles = 4;
+      g->waves = 4;
+      g->splits = rows_narrow_splits(m, g->n_tiles, g->K);
+      g->defer_epi = g->splits > 1;
     } else {
       g->splits = splits_for(m, g->n_tiles, g->K, g->waves, g->waves >= 8 ? 1 : 2);
     }
@@ -362,6 +402,7 @@ GemmArgs gemm_base(const msd_model* m, const Layout& L, char* ws, int M, const G
   g.waves = sh.waves;
   g.jt = sh.jt;
   g.wg_tiles = sh.wg_tiles;
+  g.defer_epi = sh.defer_epi;
   g.partial = reinterpret_cast<float*>(ws + L.partial);
   g.counters = reinterpret_cast<int32_t*>(ws + L.counters);
   g.n_heads = m->cfg.n_heads;
@@ -536,6 +577,10 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
   if (const char* e = getenv("MSD_GEMM_WAVES")) {
     const int v = atoi(e);
     if (v == 4 || v == 8) m->waves = v;
+  }
+  if (const char* e = getenv("MSD_ROWS_NARROW")) {
+    const int v = atoi(e);
+    if (v >= 0 && v <= 2) m->rows_narrow = v;
   }
   if (const char* e = getenv("MSD_ROWS_MIN_MT")) {
     const int v = atoi(e);

@@ -630,6 +630,25 @@ def test_rows_kernel_every_gemm(monkeypatch, shape, batch, splits):
     print("rows kernel", shape, batch, splits, _compare(case, gr, seqs))
 
 
+@pytest.mark.parametrize("shape,batch", [("tiny", 16), ("tiny", 6), ("ragged", 16)])
+def test_rows_narrow_deferred_epilogue(monkeypatch, shape, batch):
+    """Narrow GEMMs at 5 and 9 row tiles in the LDS-shared kernel with their
+    split sum and epilogue in a kernel of their own (MSD_ROWS_NARROW): the
+    FFN down projection (32 k-steps) takes 4 splits, summed and finished one
+    wave per row tile; widths of 5 and 15 tiles leave idle waves."""
+    _torch()
+    monkeypatch.setenv("MSD_ROWS_NARROW", "2")
+    model = synth.TINY if shape == "tiny" else ROWS_RAGGED
+    w = synth.WORKLOADS["14b_batch16"].with_model(model, batch=batch, ctx=(1, 600), ee_layer=1, kappa=4,
+                                                  seed=41 + batch)
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run(ee=True)
+    weights = synth.host_weights(case.shape, w.seed)
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b, weights=weights) for b in range(w.batch)}
+    print("narrow deferred", shape, batch, _compare(case, gr, seqs))
+
+
 @pytest.mark.parametrize("spans", [1, 2])
 def test_attention_deferred_merge(monkeypatch, spans):
     """The attention's chunk merge in a kernel of its own, forced, under both
