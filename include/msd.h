@@ -154,7 +154,7 @@ typedef struct msd_model msd_model;
  * it runs where its workgroups balance the compute units),
  * MSD_ROWS_MIN_TILES (forces that kernel on GEMMs with at least this many
  * tiles), MSD_ROWS_MAX_SPLITS (its splits of K at most, 4 unset) and
- * MSD_ROWS_NARROW (narrower GEMMs of 5 or more row tiles in that kernel
+ * MSD_ROWS_NARROW (narrower GEMMs of 3 or more row tiles in that kernel
  * with many splits and their split sum and epilogue in a second kernel: 0
  * never, 2 at any size; unset, for matrices of 32M weights or more). */
 msd_status msd_model_create(const msd_model_config* cfg, const void* const* tensors,

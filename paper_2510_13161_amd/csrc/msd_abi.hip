@@ -42,6 +42,7 @@ struct msd_model {
   bool rows_forced = false;        // MSD_ROWS_MIN_TILES set: no balance check
   int32_t rows_narrow = 1;         // narrow GEMMs from 5 row tiles on: many splits, deferred epilogue
                                    // (0 off, 1 large matrices, 2 any)
+  int32_t rows_narrow_mt = 3;      // row tiles from which it does
   int32_t attn_spans = 0;          // attention spans per chunk (0: chosen per call; 1: one-span kernel)
   int32_t attn_defer = -1;         // chunk merge in its own kernel: -1 by chunk count, 0 never, 1 always
   int32_t prof_class = -1;         // instrumentation (msd_set_profile)
@@ -146,7 +147,7 @@ int rows_splits(const msd_model* m, int n_tiles, int K, int per_cu) {
   return best_bal >= 0.75 ? best : 0;
 }
 
-// Narrow GEMMs (fewer tiles than m->rows_min_tiles) from 5 row tiles on:
+// Narrow GEMMs (fewer tiles than m->rows_min_tiles) from 3 row tiles on:
 // the same kernel with many splits of K, so that the 144-row MFMA work
 // spreads over the chip, and the split sum plus epilogue in a kernel of its
 // own (one wave per row tile) instead of in the last split to arrive; the
@@ -156,10 +157,13 @@ int rows_splits(const msd_model* m, int n_tiles, int K, int per_cu) {
 // output). m->rows_narrow: 0 off, 1 that rule, 2 any size (tests). Measured at 14B batch 16 (µs, GEMM +
 // epilogue kernel against the split-K kernel): QKV 32.6 + 13.6 against
 // 51.7, FFN down 43.8 + 10.2 against 66.4, but the O projection (26M
-// weights, 13 k-steps a split) 34.0 + 10.5 against 36.3.
+// weights, 13 k-steps a split) 34.0 + 10.5 against 36.3; 66B tree (3 row
+// tiles, two workgroups a unit, 7 splits, 12 MB of partials): O 46.4 ->
+// 31.5 + 7.3, down 154.2 -> 116.9 + 7.3, 30.0 -> 28.1 ms per step; at 2
+// row tiles (14B tree) slower, 8.41 -> 8.78 ms.
 constexpr int kRowsNarrowSplits = 16;
 constexpr int64_t kRowsNarrowMinWeights = 32ll << 20;
-int rows_narrow_splits(const msd_model* m, int n_tiles, int K) {
+int rows_narrow_splits(const msd_model* m, int n_tiles, int K, int per_cu) {
   const int64_t C = m->n_cus;
   const int64_t wg = (n_tiles + 3) / 4;
   const int max_s = std::max(1, std::min(kRowsNarrowSplits, (K / 32) / 8));
@@ -167,7 +171,7 @@ int rows_narrow_splits(const msd_model* m, int n_tiles, int K) {
   double best_bal = 0.0;
   for (int s = 1; s <= max_s; ++s) {
     const int64_t W = wg * s;
-    if (s > 1 && W > C) break;
+    if (s > 1 && W > per_cu * C) break;
     const double bal = (double)W / (double)(C * ((W + C - 1) / C));
     if (bal > best_bal + 1e-9) {
       best = s;
@@ -229,11 +233,11 @@ Shapes shapes(const msd_model* m, int M) {
       g->wg_tiles = 4;
       g->waves = 4;
       g->splits = rs;
-    } else if (m->rows_narrow && row_tiles(M) >= 5 && g->jt == 4 && g->n_tiles < m->rows_min_tiles &&
+    } else if (m->rows_narrow && row_tiles(M) >= m->rows_narrow_mt && g->jt == 4 && g->n_tiles < m->rows_min_tiles &&
                (m->rows_narrow == 2 || (int64_t)g->n_tiles * kTileN * g->K >= kRowsNarrowMinWeights)) {
       g->wg_tiles = 4;
       g->waves = 4;
-      g->splits = rows_narrow_splits(m, g->n_tiles, g->K);
+      g->splits = rows_narrow_splits(m, g->n_tiles, g->K, row_tiles(M) <= 3 ? 2 : 1);
       g->defer_epi = g->splits > 1;
     } else {
       g->splits = splits_for(m, g->n_tiles, g->K, g->waves, g->waves >= 8 ? 1 : 2);
@@ -581,6 +585,10 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
   if (const char* e = getenv("MSD_ROWS_NARROW")) {
     const int v = atoi(e);
     if (v >= 0 && v <= 2) m->rows_narrow = v;
+  }
+  if (const char* e = getenv("MSD_ROWS_NARROW_MT")) {
+    const int v = atoi(e);
+    if (v >= 2 && v <= kMaxMT) m->rows_narrow_mt = v;
   }
   if (const char* e = getenv("MSD_ROWS_MIN_MT")) {
     const int v = atoi(e);

@@ -630,9 +630,9 @@ def test_rows_kernel_every_gemm(monkeypatch, shape, batch, splits):
     print("rows kernel", shape, batch, splits, _compare(case, gr, seqs))
 
 
-@pytest.mark.parametrize("shape,batch", [("tiny", 16), ("tiny", 6), ("ragged", 16)])
+@pytest.mark.parametrize("shape,batch", [("tiny", 16), ("tiny", 6), ("ragged", 16), ("tiny", 4)])
 def test_rows_narrow_deferred_epilogue(monkeypatch, shape, batch):
-    """Narrow GEMMs at 5 and 9 row tiles in the LDS-shared kernel with their
+    """Narrow GEMMs at 3, 5 and 9 row tiles in the LDS-shared kernel with their
     split sum and epilogue in a kernel of their own (MSD_ROWS_NARROW): the
     FFN down projection (32 k-steps) takes 4 splits, summed and finished one
     wave per row tile; widths of 5 and 15 tiles leave idle waves."""
