@@ -860,8 +860,8 @@ __global__ __launch_bounds__((64 * block_waves<MT, NW, EPI>())) void gemm_kernel
 // from there: the image crosses L2 once per NW tiles instead of once per
 // tile, and the compute waves keep only weights in flight (D k-steps). One
 // barrier per k-step passes the slots between the loader and the compute
-// waves. Split-K as above, per tile: the last split to arrive sums all
-// splits in split order.
+// waves. With splits of K each split writes its partial of the tile and
+// gemm_epi_kernel sums them and runs the epilogues.
 template <int MT>
 __host__ __device__ constexpr int rows_depth() {  // weight k-steps in flight per compute wave
   return MT >= 9 ? 3 : (MT >= 5 ? 6 : 4);
@@ -1029,61 +1029,23 @@ __global__ __launch_bounds__(64 * (NW + 1), rows_waves_per_simd<MT>()) void gemm
   if (t >= a.n_tiles) return;
 
   if (a.splits > 1) {
-    const __amdgpu_buffer_rsrc_t part =
-        coherent_region(a.partial + (size_t)t * a.splits * TF, (uint32_t)(a.splits * TF * 4));
+    // this split's partial of the tile (all row tiles); gemm_epi_kernel sums
+    // the splits in split order and runs the epilogue
+    float* part = a.partial + ((size_t)t * a.splits + s) * TF + lane * 4;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int j = 0; j < JT; ++j)
-        store_coherent4(part, (uint32_t)((s * TF + (mt * JT + j) * 256 + lane * 4) * 4), acc[mt][j]);
-    if (a.defer_epi) return;  // gemm_epi_kernel sums the splits and finishes
-    drain_stores();
-    int old = 0;
-    if (lane == 0) old = counter_add(&a.counters[t], 1);
-    old = __shfl(old, 0);
-    if (old != a.splits - 1) return;
-    // the sum in split order, this split's own tile from registers; the
-    // other splits' tiles of MC row tiles at a time in flight
-    constexpr int MC = 3;
-#pragma unroll
-    for (int m0 = 0; m0 < MT; m0 += MC) {
-      floatx4 sum[MC][JT];
-#pragma unroll
-      for (int c = 0; c < MC; ++c)
-#pragma unroll
-        for (int j = 0; j < JT; ++j) sum[c][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-      for (int sp = 0; sp < a.splits; ++sp) {
-        floatx4 pv[MC][JT];
-#pragma unroll
-        for (int c = 0; c < MC; ++c)
-#pragma unroll
-          for (int j = 0; j < JT; ++j) {
-            const int mt = m0 + c < MT ? m0 + c : m0;
-            pv[c][j] = sp == s ? acc[mt][j]
-                               : load_coherent4(part, (uint32_t)((sp * TF + (mt * JT + j) * 256 + lane * 4) * 4));
-          }
-#pragma unroll
-        for (int c = 0; c < MC; ++c)
-#pragma unroll
-          for (int j = 0; j < JT; ++j) sum[c][j] += pv[c][j];
-      }
-#pragma unroll
-      for (int c = 0; c < MC; ++c)
-        if (m0 + c < MT)
-#pragma unroll
-          for (int j = 0; j < JT; ++j) acc[m0 + c][j] = sum[c][j];
-    }
-    if (lane == 0) counter_reset(&a.counters[t]);
+      for (int j = 0; j < JT; ++j) *reinterpret_cast<floatx4*>(part + (mt * JT + j) * 256) = acc[mt][j];
+    return;
   }
   epilogue_rows<MT, EPI, JT, has_norm<EPI>()>(a, t, acc, scr_all + wave * 16 * kScr, 0, 1, norm_sh);
 }
 
-// The split sum and epilogue of gemm_rows_kernel as a kernel of their own
-// (GemmArgs::defer_epi, with splits > 1): one wave per (64-column tile, row
-// tile) sums that row tile's partials in split order and runs its epilogue,
-// so that narrow GEMMs can take many splits of K (enough waves for the MFMA
-// work of 144 rows) without one wave summing and finishing all row tiles of
-// its tile in series.
+// The split sum and epilogue of gemm_rows_kernel with splits > 1, a kernel
+// of their own: one wave per (64-column tile, row tile) sums that row
+// tile's partials in split order and runs its epilogue, so that no wave sums
+// and finishes all row tiles of its tile in series, and narrow GEMMs can
+// take many splits of K (enough waves for the MFMA work of 144 rows).
 template <int MT, int EPI>
 __global__ __launch_bounds__(256) void gemm_epi_kernel(GemmArgs a) {
   constexpr int JT = 4;
@@ -1122,7 +1084,7 @@ template <int MT, int NW, int EPI>
 hipError_t launch_rows(const GemmArgs& a, hipStream_t s) {
   const int wgs = (a.n_tiles + NW - 1) / NW;
   hipLaunchKernelGGL((gemm_rows_kernel<MT, NW, EPI>), dim3(wgs * a.splits), dim3(64 * (NW + 1)), 0, s, a);
-  if (a.defer_epi && a.splits > 1) {
+  if (a.splits > 1) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((gemm_epi_kernel<MT, EPI>), dim3((a.n_tiles * MT + 3) / 4), dim3(256), 0, s, a);

@@ -57,9 +57,9 @@ struct GemmArgs {
                            // EPI_HEAD with one row tile and 4 waves)
   int32_t wg_tiles;        // 64-column tiles per workgroup: 1, or 4 (2 to 9 row tiles:
                            // one compute wave a tile and a wave that stages the
-                           // activation through LDS; then waves = 4)
-  int32_t defer_epi;       // wg_tiles 4 with splits > 1: partials only; a second kernel
-                           // sums them and runs the epilogue, one wave a row tile
+                           // activation through LDS; then waves = 4, and with
+                           // splits > 1 a second kernel sums the splits and runs
+                           // the epilogue)
   int32_t map;
   const uint16_t* w0;
   const uint16_t* w1;

@@ -184,7 +184,6 @@ int rows_narrow_splits(const msd_model* m, int n_tiles, int K, int per_cu) {
 struct GemmShape {
   int n_tiles, K, splits, waves, jt;
   int wg_tiles = 1;
-  int defer_epi = 0;
 };
 
 struct Shapes {
@@ -238,7 +237,6 @@ Shapes shapes(const msd_model* m, int M) {
       g->wg_tiles = 4;
       g->waves = 4;
       g->splits = rows_narrow_splits(m, g->n_tiles, g->K, row_tiles(M) <= 3 ? 2 : 1);
-      g->defer_epi = g->splits > 1;
     } else {
       g->splits = splits_for(m, g->n_tiles, g->K, g->waves, g->waves >= 8 ? 1 : 2);
     }
@@ -406,7 +404,6 @@ GemmArgs gemm_base(const msd_model* m, const Layout& L, char* ws, int M, const G
   g.waves = sh.waves;
   g.jt = sh.jt;
   g.wg_tiles = sh.wg_tiles;
-  g.defer_epi = sh.defer_epi;
   g.partial = reinterpret_cast<float*>(ws + L.partial);
   g.counters = reinterpret_cast<int32_t*>(ws + L.counters);
   g.n_heads = m->cfg.n_heads;
