@@ -255,6 +255,26 @@ __device__ __forceinline__ void merge_chunks(const AttnArgs& a, int* last, int32
   if (tid == 0) counter_reset(ctr);
 }
 
+// Workgroup coordinates from a one-dimensional grid ordered kv head first:
+// the hardware hands consecutive workgroups to the 8 XCDs in turn, so with
+// a kv-head count that is a multiple of 8 every workgroup of one kv head
+// (its chunks, query-tile groups and sequences) runs on the same XCD and its
+// repeated reads of that head's K and V are served by one L2.
+struct AttnWg {
+  int b, kvh, qgi, c;
+};
+__device__ __forceinline__ AttnWg attn_wg(const AttnArgs& a, int chunks, int QG) {
+  int id = blockIdx.x;
+  AttnWg w;
+  w.kvh = id % a.n_kv_heads;
+  id /= a.n_kv_heads;
+  w.c = id % chunks;
+  id /= chunks;
+  w.qgi = id % QG;
+  w.b = id / QG;
+  return w;
+}
+
 // MULTI: the workgroup takes several query tiles in turn (K and V operands
 // stay in registers across them); otherwise exactly one.
 template <int HD, bool MULTI>
@@ -275,12 +295,13 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(AttnArgs a) {
   const int Qn = G * ns;
   const int QT = (Qn + 15) >> 4;
   const int QG = (QT + a.q_per_wg - 1) / a.q_per_wg;  // query-tile groups per kv head
-  const int b = blockIdx.z, kvh = blockIdx.y / QG, qgi = blockIdx.y - kvh * QG, c = blockIdx.x;
+  const AttnWg wg = attn_wg(a, a.max_chunks, QG);
+  const int b = wg.b, kvh = wg.kvh, qgi = wg.qgi, c = wg.c;
   const int qt0 = qgi * a.q_per_wg, qt1 = MULTI ? min(QT, qt0 + a.q_per_wg) : qt0 + 1;
   const int L = a.len[b];
   const int T = L + ns;
   if (T > a.capacity) {
-    if (c == 0 && blockIdx.y == 0 && tid == 0) atomicOr(a.status, 1u);
+    if (c == 0 && kvh == 0 && qgi == 0 && tid == 0) atomicOr(a.status, 1u);
     return;
   }
   const int nch = (T + kAttnChunk - 1) / kAttnChunk;
@@ -471,12 +492,13 @@ __global__ __launch_bounds__(256, 1) void attn_stream_kernel(AttnArgs a) {
   const int Qn = G * ns;
   const int QT = (Qn + 15) >> 4;
   const int QG = (QT + QPW - 1) / QPW;
-  const int b = blockIdx.z, kvh = blockIdx.y / QG, qgi = blockIdx.y - kvh * QG, c = blockIdx.x;
+  const AttnWg wg = attn_wg(a, (a.max_chunks + a.nb - 1) / a.nb, QG);
+  const int b = wg.b, kvh = wg.kvh, qgi = wg.qgi, c = wg.c;
   const int qt0 = qgi * QPW, ntile = min(QPW, QT - qt0);
   const int L = a.len[b];
   const int T = L + ns;
   if (T > a.capacity) {
-    if (c == 0 && blockIdx.y == 0 && tid == 0) atomicOr(a.status, 1u);
+    if (c == 0 && kvh == 0 && qgi == 0 && tid == 0) atomicOr(a.status, 1u);
     return;
   }
   const int nch = (T + a.nb * kAttnChunk - 1) / (a.nb * kAttnChunk);
@@ -748,7 +770,7 @@ hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s) {
   if (a.nb > 1) {
     // the streaming kernel: up to 3 query tiles a workgroup, chunks of nb spans
     if (a.q_per_wg > 3) return hipErrorInvalidValue;
-    const dim3 grid((a.max_chunks + a.nb - 1) / a.nb, a.n_kv_heads * qg, a.batch);
+    const dim3 grid((unsigned)((a.max_chunks + a.nb - 1) / a.nb) * a.n_kv_heads * qg * a.batch);
     const int qpw = a.q_per_wg;
     if (head_dim == 128) {
       if (qpw == 1) hipLaunchKernelGGL((attn_stream_kernel<128, 1>), grid, dim3(256), 0, s, a);
@@ -761,7 +783,7 @@ hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s) {
     }
     return hipGetLastError();
   }
-  const dim3 grid(a.max_chunks, a.n_kv_heads * qg, a.batch);
+  const dim3 grid((unsigned)a.max_chunks * a.n_kv_heads * qg * a.batch);
   const bool multi = a.q_per_wg > 1 && qt > 1;
   if (head_dim == 128) {
     if (multi) hipLaunchKernelGGL((attn_kernel<128, true>), grid, dim3(256), 0, s, a);

@@ -542,6 +542,25 @@ def test_depth_reduced_14b_chain():
     print("14b L2 chain:", rep)
 
 
+@pytest.mark.parametrize("gamma", [0, 8])
+def test_draft_shape(gamma):
+    """The 0.6B-shaped draft decoder that the latency-law measurement runs (d
+    1024, GQA 16/8 x 128, SwiGLU 3072, tied head over the target's 152064
+    vocabulary), 4 layers, kappa = 8 sequences after a 1024-key context: one
+    slot each (one greedy draft decode step of the kappa branches, 8 rows)
+    and gamma + 1 = 9 slots each (the Speculative Streaming pass: per branch
+    the main stream and gamma lookahead streams form a chain; 72 rows, five
+    row tiles)."""
+    _torch()
+    w = synth.Workload("draft_shape", synth.DRAFT06B, 8, (1024, 1024), "chain", gamma, ee_layer=2,
+                       kappa=4, seed=5)
+    case = H.GpuCase(w, n_layers=4)
+    gr = case.run()
+    weights = synth.host_weights(case.shape, w.seed)
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b, weights=weights) for b in (0, 3, 7)}
+    print("draft shape, gamma", gamma, _compare(case, gr, seqs))
+
+
 def _gqa64_tree():
     shape = synth.ModelShape("gqa64", 2, 1024, 16, 4, 64, 2048, 4096, rope_theta=1.0e4)
     return synth.Workload("gqa64_tree", shape, 4, (4600, 4800), "tree", 6, branches=4, ee_layer=1,
