@@ -33,6 +33,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
@@ -708,6 +709,265 @@ __global__ __launch_bounds__(256, 1) void attn_stream_kernel(AttnArgs a) {
                    qt0 + ntile, Qn, nch, pbase, pco);
 }
 
+// Long contexts, fed through an LDS ring (head dim 128): a workgroup owns
+// a chunk of nb consecutive 256-key spans of one (sequence, kv head) and a
+// group of up to 4 query tiles, one compute wave per tile. Two loader waves
+// copy the chunk's 64-key blocks of K and of V straight from HBM into a ring
+// of R LDS slots with global-to-LDS loads, P blocks ahead of the compute
+// waves, each waiting on its own load counter; one barrier per block passes
+// the slots on (the protocol of the LDS-shared GEMM kernel). Every compute
+// wave then reads the block's K operands and transposed V operands from LDS
+// and keeps its tile's running (max, sum, output) in registers with the
+// online softmax of attn_stream_kernel, so a compute unit keeps P blocks
+// (96 KB) in flight without registers for them and no wave waits for its
+// own loads. Rows are stored XOR-swizzled by 16-byte unit (K: unit ^ key%16;
+// V: unit ^ 2 (key%8)) so that the K operand reads (16 keys, one unit each)
+// and the transposing V reads (8 keys, two half-units each per 32 lanes)
+// touch every LDS bank once. The chunk's partials are merged as in the
+// kernels above (last arrival or the merge kernel).
+template <int NQ>
+__global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
+  constexpr int HD = 128;
+  constexpr int KSTEPS = HD / 32;
+  constexpr int DSUB = HD / 16;
+  constexpr int C4 = HD / 4;
+  constexpr int UNITS = HD / 8;             // 16-byte units of a key row
+  constexpr int LOADS = 64 * UNITS / 64;    // 1 KB global-to-LDS loads per block of K (or V)
+  constexpr int P = 3;                      // blocks in flight ahead of the one computed
+  constexpr int R = P + 1;                  // ring slots: refilled one barrier after their last read
+  constexpr int ORS = HD + 4;               // floats per row of a wave's output staging
+  static_assert((P - 1) * LOADS <= 63, "a loader waits on at most 63 outstanding loads");
+  static_assert(R * 2 * 64 * HD * 2 >= NQ * 16 * ORS * 4, "the output staging reuses the ring");
+  __shared__ __attribute__((aligned(16))) uint16_t ring[R][2][64 * HD];
+  __shared__ float2 ml_sh[NQ][16];
+  __shared__ int last;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int G = a.n_heads / a.n_kv_heads;
+  const int ns = a.n_slots;
+  const int Qn = G * ns;
+  const int QT = (Qn + 15) >> 4;
+  const int QG = (QT + NQ - 1) / NQ;
+  const AttnWg wg = attn_wg(a, (a.max_chunks + a.nb - 1) / a.nb, QG);
+  const int b = wg.b, kvh = wg.kvh, qgi = wg.qgi, c = wg.c;
+  const int qt0 = qgi * NQ, ntile = min(NQ, QT - qt0);
+  const int L = a.len[b];
+  const int T = L + ns;
+  if (T > a.capacity) {
+    if (c == 0 && kvh == 0 && qgi == 0 && tid == 0) atomicOr(a.status, 1u);
+    return;
+  }
+  const int ck = a.nb * kAttnChunk;  // keys per chunk
+  const int nch = (T + ck - 1) / ck;
+  if (c >= nch) return;
+  const int kbeg = c * ck;
+  const int nblk = (min(T, kbeg + ck) - kbeg + 63) >> 6;
+  const size_t row0 = ((size_t)b * a.n_kv_heads + kvh) * a.capacity;
+
+  floatx4 o[DSUB];
+  float mrun = -INFINITY, lrun = 0.0f;
+#pragma unroll
+  for (int ds = 0; ds < DSUB; ++ds) o[ds] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  if (wave >= NQ) {
+    // the loaders: wave NQ the K blocks, wave NQ + 1 the V blocks; block i
+    // goes to slot i % R, issued after barrier i - P (which the compute waves
+    // pass only once done with block i - P - 1, the slot's previous content)
+    // and complete before barrier i
+    const int isv = wave - NQ;
+    const uint16_t* src = (isv ? a.v_cache : a.k_cache) + row0 * HD;
+    auto fetch = [&](int i, int slot) {
+      const int k0 = kbeg + 64 * i;
+#pragma unroll
+      for (int x = 0; x < LOADS; ++x) {
+        const int U = x * 64 + lane;  // 16-byte unit of the slot
+        const int key = U / UNITS, p = U - key * UNITS;
+        const int u = isv ? p ^ ((key & 7) << 1) : p ^ (key & 15);
+        const int pos = min(k0 + key, T - 1);  // rows past the last key: a valid row, masked
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(src + (size_t)pos * HD + u * 8),
+                                         (__attribute__((address_space(3))) void*)&ring[slot][isv][x * 512], 16, 0,
+                                         0);
+      }
+    };
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+      if (p < nblk) fetch(p, p);
+    int slot_in = P % R;
+    for (int i = 0; i < nblk; ++i) {
+      if (i + P <= nblk) wait_vmcnt<(P - 1) * LOADS>();
+      else wait_vmcnt<0>();
+      lds_barrier();
+      if (i + P < nblk) {
+        fetch(i + P, slot_in);
+        slot_in = slot_in + 1 == R ? 0 : slot_in + 1;
+      }
+    }
+  } else {
+    const int qt = qt0 + wave;
+    const bool has = wave < ntile;  // a wave past the group's last tile only passes the barriers
+    const int qv = qt * 16 + r16;
+    const uint64_t anc = has && qv < Qn ? a.topo.anc[qv % ns] : 0ull;
+    bf16x8 qh[KSTEPS], ql[KSTEPS];
+    {
+      const uint16_t* qtile =
+          a.q_img + (((size_t)b * a.n_kv_heads + kvh) * QT + (has ? qt : 0)) * (size_t)KSTEPS * 1024 + lane * 8;
+      const bool qok = has && qv < Qn;
+#pragma unroll
+      for (int kk = 0; kk < KSTEPS; ++kk) {
+        u32x4 h = *reinterpret_cast<const u32x4*>(qtile + (size_t)kk * 1024);
+        u32x4 l = *reinterpret_cast<const u32x4*>(qtile + (size_t)kk * 1024 + 512);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          h[x] = qok ? h[x] : 0u;
+          l[x] = qok ? l[x] : 0u;
+        }
+        qh[kk] = __builtin_bit_cast(bf16x8, h);
+        ql[kk] = __builtin_bit_cast(bf16x8, l);
+      }
+    }
+    const float scale2 = a.scale * kLog2e;
+    int slot = 0;
+    for (int i = 0; i < nblk; ++i) {
+      lds_barrier();
+      if (has) {
+        const uint16_t* ks = ring[slot][0];
+        const uint16_t* vsl = ring[slot][1];
+        const int k0 = kbeg + 64 * i;
+        const int key_hi = min(T, k0 + 64);
+        // S^T[key][query] = K Q^T: lane holds key 16 j + 4 g + r, query r16
+        floatx4 sc[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          sc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int kk = 0; kk < KSTEPS; ++kk) {
+            const bf16x8 kf =
+                *reinterpret_cast<const bf16x8*>(ks + (16 * j + r16) * HD + (((4 * kk + g) ^ r16) << 3));
+            sc[j] = mfma16x16x32(kf, qh[kk], sc[j]);
+            sc[j] = mfma16x16x32(kf, ql[kk], sc[j]);
+          }
+        }
+        float mx = -INFINITY;
+        if (k0 + 64 <= L) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              sc[j][r] *= scale2;
+              mx = fmaxf(mx, sc[j][r]);
+            }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int pos = k0 + 16 * j + 4 * g + r;
+              const bool anc_bit = (anc >> ((pos - L) & 63)) & 1ull;
+              const bool vis = (pos < key_hi) & ((pos < L) | anc_bit);
+              sc[j][r] = vis ? sc[j][r] * scale2 : -INFINITY;
+              mx = fmaxf(mx, sc[j][r]);
+            }
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        // the reference of the running sums moves up only when a block max
+        // exceeds it by more than 2^8 (as in attn_stream_kernel)
+        if (__builtin_amdgcn_read_exec() & __ballot(mx > mrun + 8.0f)) {
+          const float mnew = fmaxf(mrun, mx);
+          const float alpha = mrun == -INFINITY ? 0.0f : exp2_hw(mrun - mnew);
+          lrun *= alpha;
+          mrun = mnew;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float ar = __shfl(alpha, 4 * g + r);
+#pragma unroll
+            for (int ds = 0; ds < DSUB; ++ds) o[ds][r] *= ar;
+          }
+        }
+        const float mref = mrun == -INFINITY ? 0.0f : mrun;
+        float ls = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            sc[j][r] = exp2_hw(sc[j][r] - mref);
+            ls += sc[j][r];
+          }
+        ls += __shfl_xor(ls, 16);
+        ls += __shfl_xor(ls, 32);
+        lrun += ls;
+        // O += P V, P as bf16 hi + lo in the k order of the V operand (keys
+        // 4 g + r of the two 16-key tiles); V by the transposing LDS read:
+        // lane r16 of group g addresses key 32 kb + 4 g + r16 / 4 (and + 16),
+        // dims 16 ds + 4 (r16 % 4) .. + 4
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          u32x4 ph, pl;
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            const float p0 = sc[2 * kb + (x >> 1)][2 * (x & 1)];
+            const float p1 = sc[2 * kb + (x >> 1)][2 * (x & 1) + 1];
+            ph[x] = pack_bf16x2(p0, p1);
+            pl[x] = pack_bf16x2(p0 - bf_lo(ph[x]), p1 - bf_hi(ph[x]));
+          }
+          const bf16x8 pah = __builtin_bit_cast(bf16x8, ph);
+          const bf16x8 pal = __builtin_bit_cast(bf16x8, pl);
+          const int kr = 32 * kb + 4 * g + (r16 >> 2);
+#pragma unroll
+          for (int ds = 0; ds < DSUB; ++ds) {
+            const int u = 2 * ds + ((r16 & 3) >> 1);
+            const uint16_t* p0 = vsl + kr * HD + ((u ^ ((kr & 7) << 1)) << 3) + 4 * (r16 & 1);
+            const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p0);
+            const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0 + 16 * HD));
+            const bf16x8 vb = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            o[ds] = mfma16x16x32(pah, vb, o[ds]);
+            o[ds] = mfma16x16x32(pal, vb, o[ds]);
+          }
+        }
+      }
+      slot = slot + 1 == R ? 0 : slot + 1;
+    }
+  }
+
+  // every wave is past its last ring access: the ring becomes the output
+  // staging; each compute wave writes its tile's output or partial
+  __syncthreads();
+  const size_t pbase = ((size_t)b * a.n_kv_heads + kvh) * a.max_chunks;
+  const __amdgpu_buffer_rsrc_t pco =
+      coherent_region(a.part_o + pbase * Qn * HD, (uint32_t)((size_t)a.max_chunks * Qn * HD * 4));
+  if (wave < ntile) {
+    float* os = reinterpret_cast<float*>(&ring[0][0][0]) + wave * 16 * ORS;
+#pragma unroll
+    for (int ds = 0; ds < DSUB; ++ds)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) os[(4 * g + r) * ORS + ds * 16 + r16] = o[ds][r];
+    if (g == 0) ml_sh[wave][r16] = make_float2(mrun, lrun);
+    wave_lds_sync();
+    const int qt = qt0 + wave;
+    for (int x = lane; x < 16 * C4; x += 64) {
+      const int qloc = x / C4, c4 = x - qloc * C4;
+      const int qg = qt * 16 + qloc;
+      if (qg >= Qn) continue;
+      const float4 v = *reinterpret_cast<const float4*>(os + qloc * ORS + 4 * c4);
+      const float2 ml = ml_sh[wave][qloc];
+      if (nch == 1) {
+        const float inv = ml.y > 0.0f ? 1.0f / ml.y : 0.0f;
+        const float out[4] = {v.x * inv, v.y * inv, v.z * inv, v.w * inv};
+        write_out4<HD>(a, b, kvh, qg, c4, out);
+      } else {
+        store_coherent4(pco, (uint32_t)((((size_t)c * Qn + qg) * HD + 4 * c4) * 4),
+                        floatx4{v.x, v.y, v.z, v.w});
+        if (c4 == 0) store_coherent2(a.part_ml + 2 * ((pbase + c) * Qn + qg), ml.x, ml.y);
+      }
+    }
+  }
+  if (nch == 1 || a.defer) return;
+  merge_chunks<HD>(a, &last, a.counters + ((size_t)b * a.n_kv_heads + kvh) * QG + qgi, b, kvh, qt0,
+                   qt0 + ntile, Qn, nch, pbase, pco);
+}
+
 // The chunk merge as a kernel of its own (AttnArgs::defer): one thread per
 // (sequence, kv head, query, 4 output dims) of every sequence with more than
 // one chunk, the running merge of merge_chunks in chunk order (the same
@@ -767,6 +1027,18 @@ hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s) {
   const int qt = (a.n_heads / a.n_kv_heads * a.n_slots + 15) / 16;
   if (a.q_per_wg < 1 || a.nb < 1) return hipErrorInvalidValue;
   const int qg = (qt + a.q_per_wg - 1) / a.q_per_wg;
+  if (a.ring) {
+    // the ring-fed kernel: head dim 128, up to 4 query tiles a workgroup
+    if (head_dim != 128 || a.q_per_wg > 4) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((a.max_chunks + a.nb - 1) / a.nb) * a.n_kv_heads * qg * a.batch);
+    switch (a.q_per_wg) {
+      case 1: hipLaunchKernelGGL((attn_ring_kernel<1>), grid, dim3(64 * 3), 0, s, a); break;
+      case 2: hipLaunchKernelGGL((attn_ring_kernel<2>), grid, dim3(64 * 4), 0, s, a); break;
+      case 3: hipLaunchKernelGGL((attn_ring_kernel<3>), grid, dim3(64 * 5), 0, s, a); break;
+      default: hipLaunchKernelGGL((attn_ring_kernel<4>), grid, dim3(64 * 6), 0, s, a); break;
+    }
+    return hipGetLastError();
+  }
   if (a.nb > 1) {
     // the streaming kernel: up to 3 query tiles a workgroup, chunks of nb spans
     if (a.q_per_wg > 3) return hipErrorInvalidValue;

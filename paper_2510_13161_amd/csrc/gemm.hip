@@ -879,13 +879,6 @@ __host__ __device__ constexpr int rows_ahead() {
   return 63 / (2 * MT) + 1 < 8 ? 63 / (2 * MT) + 1 : 8;
 }
 
-// s_waitcnt for at most n outstanding vector-memory loads (expcnt and
-// lgkmcnt not waited on)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt field is 6 bits");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
 
 template <int MT, int NW, int EPI>
 __global__ __launch_bounds__(64 * (NW + 1), rows_waves_per_simd<MT>()) void gemm_rows_kernel(GemmArgs a) {

@@ -158,6 +158,8 @@ struct AttnArgs {
   float scale;
   int32_t defer;            // 1: chunks only publish their partials; a second
                             // kernel merges them (no in-kernel hand-off)
+  int32_t ring;             // 1: attn_ring_kernel (head dim 128, chunks of nb spans,
+                            // q_per_wg <= 4 tiles a workgroup)
   Topo topo;
 };
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s);

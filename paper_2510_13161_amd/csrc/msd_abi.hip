@@ -45,6 +45,7 @@ struct msd_model {
   int32_t rows_narrow_mt = 3;      // row tiles from which it does
   int32_t attn_spans = 0;          // attention spans per chunk (0: chosen per call; 1: one-span kernel)
   int32_t attn_defer = -1;         // chunk merge in its own kernel: -1 by chunk count, 0 never, 1 always
+  int32_t attn_ring = 1;           // chunks of several spans at head dim 128: the ring-fed kernel (0: streaming)
   int32_t prof_class = -1;         // instrumentation (msd_set_profile)
   std::vector<hipEvent_t> prof_begin, prof_end;
 };
@@ -370,14 +371,20 @@ int attn_q_per_wg(int max_chunks, int n_kv_heads, int batch, int q_tiles) {
 constexpr int64_t kAttnStreamWgs = 256;
 struct AttnShape {
   int q_per_wg, nb;
+  bool ring;
 };
-AttnShape attn_shape(const msd_model* m, int max_chunks, int n_kv_heads, int batch, int q_tiles) {
-  const int qs = std::min(3, q_tiles);
+// Chunks of several spans take attn_ring_kernel at head dim 128 (up to 4
+// query tiles a workgroup, K and V fed through an LDS ring; m->attn_ring 0
+// keeps attn_stream_kernel, up to 3 tiles).
+AttnShape attn_shape(const msd_model* m, int max_chunks, int n_kv_heads, int batch, int q_tiles,
+                     int head_dim) {
+  const bool ring = m->attn_ring != 0 && head_dim == 128;
+  const int qs = std::min(ring ? 4 : 3, q_tiles);
   const int64_t grid1 = (int64_t)max_chunks * n_kv_heads * batch * ((q_tiles + qs - 1) / qs);
   int64_t nb = m->attn_spans > 0 ? m->attn_spans : (grid1 + kAttnStreamWgs - 1) / kAttnStreamWgs;
   nb = std::min<int64_t>(nb, max_chunks);
-  if (nb >= 2) return {qs, (int)nb};
-  return {attn_q_per_wg(max_chunks, n_kv_heads, batch, q_tiles), 1};
+  if (nb >= 2) return {qs, (int)nb, ring};
+  return {attn_q_per_wg(max_chunks, n_kv_heads, batch, q_tiles), 1, false};
 }
 
 // Chunk merge in a kernel of its own (instead of the last chunk to arrive)
@@ -605,6 +612,10 @@ msd_status msd_model_create(const msd_model_config* cfg, const void* const* tens
   if (const char* e = getenv("MSD_ATTN_DEFER")) {
     const int v = atoi(e);
     if (v >= -1 && v <= 1) m->attn_defer = v;
+  }
+  if (const char* e = getenv("MSD_ATTN_RING")) {
+    const int v = atoi(e);
+    if (v == 0 || v == 1) m->attn_ring = v;
   }
   if (const char* e = getenv("MSD_ATTN_SPANS")) {
     const int v = atoi(e);
@@ -902,9 +913,10 @@ msd_status verify_launch(const msd_model* m, msd_kv_cache* kv, const msd_block* 
     aa.capacity = kv->capacity;
     aa.n_slots = blk->n_slots;
     aa.max_chunks = L.max_chunks;
-    const AttnShape ash = attn_shape(m, L.max_chunks, c.n_kv_heads, blk->batch, q_tiles);
+    const AttnShape ash = attn_shape(m, L.max_chunks, c.n_kv_heads, blk->batch, q_tiles, c.head_dim);
     aa.q_per_wg = ash.q_per_wg;
     aa.nb = ash.nb;
+    aa.ring = ash.ring ? 1 : 0;
     aa.scale = 1.0f / std::sqrt((float)c.head_dim);
     aa.topo = topo;
     aa.defer = attn_defer(m, L.max_chunks, ash.nb) ? 1 : 0;

@@ -726,11 +726,50 @@ def test_attention_streaming_14b_widths(monkeypatch):
     tiles in one group), 2 layers, a 1024-key context in 3 chunks of 2 spans."""
     _torch()
     monkeypatch.setenv("MSD_ATTN_SPANS", "2")
+    monkeypatch.setenv("MSD_ATTN_RING", "0")
     w = synth.WORKLOADS["14b_chain"].with_model(synth.QWEN14B)
     case = H.GpuCase(w, n_layers=2)
     gr = case.run()
     o = H.oracle_sequence(case.shape, w, case.si, 0)
     print("streaming 14b L2 chain:", _compare(case, gr, {0: o}))
+
+
+def test_attention_ring_14b_widths(monkeypatch):
+    """Ring-fed kernel (K and V blocks copied into an LDS ring by two loader
+    waves, one compute wave per query tile) at 14B widths, 2 layers: a
+    1033-key context in 3 chunks of 2 spans, the 3 query tiles of a kv head
+    in one workgroup, chunks merged by the last to arrive."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_SPANS", "2")
+    w = synth.WORKLOADS["14b_chain"].with_model(synth.QWEN14B)
+    case = H.GpuCase(w, n_layers=2)
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    print("ring 14b L2 chain:", _compare(case, gr, {0: o}))
+
+
+@pytest.mark.parametrize("heads,defer", [(8, 0), (8, 1), (16, 0)])
+def test_attention_ring_ragged_batch(monkeypatch, heads, defer):
+    """Ring-fed kernel on a ragged batch (head dim 128, 2 kv heads, contexts
+    1 to 1000, chunks of 2 spans): sequences of at most 512 keys are written
+    by their only chunk, longer ones merge two (by the last to arrive, or by
+    the merge kernel); blocks past a sequence's last key are masked. With 8
+    query heads a kv head has 3 query tiles (one workgroup); with 16 it has 5
+    (a group of 4 and a group of 1 whose other compute waves hold no tile)."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_SPANS", "2")
+    monkeypatch.setenv("MSD_ATTN_DEFER", str(defer))
+    shape = synth.ModelShape(f"h128x{heads}", 2, 512, heads, 2, 128, 1024, 4096, rope_theta=1.0e4)
+    w = synth.WORKLOADS["14b_batch16"].with_model(shape, batch=6, ctx=(1, 1000), ee_layer=1, kappa=4,
+                                                  seed=32 + heads)
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run()
+    weights = synth.host_weights(case.shape, w.seed)
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b, weights=weights) for b in range(w.batch)}
+    lens = case.si.ctx_len + w.n_slots
+    assert lens.min() <= 512 < lens.max()
+    print("ring ragged", heads, defer, _compare(case, gr, seqs))
 
 
 def test_streaming_attention_is_deterministic(monkeypatch):
