@@ -711,22 +711,23 @@ __global__ __launch_bounds__(256, 1) void attn_stream_kernel(AttnArgs a) {
 
 // Long contexts, fed through an LDS ring (head dim 128): a workgroup owns
 // a chunk of nb consecutive 256-key spans of one (sequence, kv head) and a
-// group of up to 4 query tiles, one compute wave per tile. Two loader waves
+// group of up to 4 query tiles, two compute waves per tile (one per 32-key
+// half of every block, so that each SIMD holds two and one's softmax overlaps
+// the other's MFMAs; the two halves are merged once at the end). Two loader waves
 // copy the chunk's 64-key blocks of K and of V straight from HBM into a ring
 // of R LDS slots with global-to-LDS loads, P blocks ahead of the compute
 // waves, each waiting on its own load counter; one barrier per block passes
 // the slots on (the protocol of the LDS-shared GEMM kernel). Every compute
-// wave then reads the block's K operands and transposed V operands from LDS
-// and keeps its tile's running (max, sum, output) in registers with the
-// online softmax of attn_stream_kernel, so a compute unit keeps P blocks
-// (96 KB) in flight without registers for them and no wave waits for its
-// own loads. Rows are stored XOR-swizzled by 16-byte unit (K: unit ^ key%16;
+// wave then reads its half-block's K operands and transposed V operands from
+// LDS and keeps its running (max, sum, output) in registers with the online
+// softmax of attn_stream_kernel, so a compute unit keeps P blocks (96 KB) in
+// flight without registers for them and no wave waits for its own loads. Rows are stored XOR-swizzled by 16-byte unit (K: unit ^ key%16;
 // V: unit ^ 2 (key%8)) so that the K operand reads (16 keys, one unit each)
 // and the transposing V reads (8 keys, two half-units each per 32 lanes)
 // touch every LDS bank once. The chunk's partials are merged as in the
 // kernels above (last arrival or the merge kernel).
 template <int NQ>
-__global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64 * (2 * NQ + 2)) void attn_ring_kernel(AttnArgs a) {
   constexpr int HD = 128;
   constexpr int KSTEPS = HD / 32;
   constexpr int DSUB = HD / 16;
@@ -737,9 +738,9 @@ __global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
   constexpr int R = P + 1;                  // ring slots: refilled one barrier after their last read
   constexpr int ORS = HD + 4;               // floats per row of a wave's output staging
   static_assert((P - 1) * LOADS <= 63, "a loader waits on at most 63 outstanding loads");
-  static_assert(R * 2 * 64 * HD * 2 >= NQ * 16 * ORS * 4, "the output staging reuses the ring");
+  static_assert(R * 2 * 64 * HD * 2 >= 2 * NQ * 16 * ORS * 4, "the output staging reuses the ring");
   __shared__ __attribute__((aligned(16))) uint16_t ring[R][2][64 * HD];
-  __shared__ float2 ml_sh[NQ][16];
+  __shared__ float2 ml_sh[NQ][2][16];
   __shared__ int last;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -771,12 +772,12 @@ __global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
 #pragma unroll
   for (int ds = 0; ds < DSUB; ++ds) o[ds] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  if (wave >= NQ) {
-    // the loaders: wave NQ the K blocks, wave NQ + 1 the V blocks; block i
+  if (wave >= 2 * NQ) {
+    // the loaders: wave 2 NQ the K blocks, wave 2 NQ + 1 the V blocks; block i
     // goes to slot i % R, issued after barrier i - P (which the compute waves
     // pass only once done with block i - P - 1, the slot's previous content)
     // and complete before barrier i
-    const int isv = wave - NQ;
+    const int isv = wave - 2 * NQ;
     const uint16_t* src = (isv ? a.v_cache : a.k_cache) + row0 * HD;
     auto fetch = [&](int i, int slot) {
       const int k0 = kbeg + 64 * i;
@@ -805,8 +806,9 @@ __global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
       }
     }
   } else {
-    const int qt = qt0 + wave;
-    const bool has = wave < ntile;  // a wave past the group's last tile only passes the barriers
+    const int hk = wave & 1;  // keys 32 hk .. 32 hk + 31 of every block
+    const int qt = qt0 + (wave >> 1);
+    const bool has = (wave >> 1) < ntile;  // a wave past the group's last tile only passes the barriers
     const int qv = qt * 16 + r16;
     const uint64_t anc = has && qv < Qn ? a.topo.anc[qv % ns] : 0ull;
     bf16x8 qh[KSTEPS], ql[KSTEPS];
@@ -836,15 +838,16 @@ __global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
         const uint16_t* vsl = ring[slot][1];
         const int k0 = kbeg + 64 * i;
         const int key_hi = min(T, k0 + 64);
-        // S^T[key][query] = K Q^T: lane holds key 16 j + 4 g + r, query r16
-        floatx4 sc[4];
+        // S^T[key][query] = K Q^T over the wave's half: lane holds key
+        // 16 (2 hk + j) + 4 g + r, query r16
+        floatx4 sc[2];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < 2; ++j) {
           sc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int kk = 0; kk < KSTEPS; ++kk) {
-            const bf16x8 kf =
-                *reinterpret_cast<const bf16x8*>(ks + (16 * j + r16) * HD + (((4 * kk + g) ^ r16) << 3));
+            const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + (16 * (2 * hk + j) + r16) * HD +
+                                                               (((4 * kk + g) ^ r16) << 3));
             sc[j] = mfma16x16x32(kf, qh[kk], sc[j]);
             sc[j] = mfma16x16x32(kf, ql[kk], sc[j]);
           }
@@ -852,7 +855,7 @@ __global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
         float mx = -INFINITY;
         if (k0 + 64 <= L) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
+          for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               sc[j][r] *= scale2;
@@ -860,10 +863,10 @@ __global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
             }
         } else {
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
+          for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-              const int pos = k0 + 16 * j + 4 * g + r;
+              const int pos = k0 + 16 * (2 * hk + j) + 4 * g + r;
               const bool anc_bit = (anc >> ((pos - L) & 63)) & 1ull;
               const bool vis = (pos < key_hi) & ((pos < L) | anc_bit);
               sc[j][r] = vis ? sc[j][r] * scale2 : -INFINITY;
@@ -889,7 +892,7 @@ __global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
         const float mref = mrun == -INFINITY ? 0.0f : mrun;
         float ls = 0.0f;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             sc[j][r] = exp2_hw(sc[j][r] - mref);
@@ -899,22 +902,21 @@ __global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
         ls += __shfl_xor(ls, 32);
         lrun += ls;
         // O += P V, P as bf16 hi + lo in the k order of the V operand (keys
-        // 4 g + r of the two 16-key tiles); V by the transposing LDS read:
-        // lane r16 of group g addresses key 32 kb + 4 g + r16 / 4 (and + 16),
-        // dims 16 ds + 4 (r16 % 4) .. + 4
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
+        // 4 g + r of the half's two 16-key tiles); V by the transposing LDS
+        // read: lane r16 of group g addresses key 32 hk + 4 g + r16 / 4 (and
+        // + 16), dims 16 ds + 4 (r16 % 4) .. + 4
+        {
           u32x4 ph, pl;
 #pragma unroll
           for (int x = 0; x < 4; ++x) {
-            const float p0 = sc[2 * kb + (x >> 1)][2 * (x & 1)];
-            const float p1 = sc[2 * kb + (x >> 1)][2 * (x & 1) + 1];
+            const float p0 = sc[x >> 1][2 * (x & 1)];
+            const float p1 = sc[x >> 1][2 * (x & 1) + 1];
             ph[x] = pack_bf16x2(p0, p1);
             pl[x] = pack_bf16x2(p0 - bf_lo(ph[x]), p1 - bf_hi(ph[x]));
           }
           const bf16x8 pah = __builtin_bit_cast(bf16x8, ph);
           const bf16x8 pal = __builtin_bit_cast(bf16x8, pl);
-          const int kr = 32 * kb + 4 * g + (r16 >> 2);
+          const int kr = 32 * hk + 4 * g + (r16 >> 2);
 #pragma unroll
           for (int ds = 0; ds < DSUB; ++ds) {
             const int u = 2 * ds + ((r16 & 3) >> 1);
@@ -932,26 +934,41 @@ __global__ __launch_bounds__(64 * (NQ + 2)) void attn_ring_kernel(AttnArgs a) {
   }
 
   // every wave is past its last ring access: the ring becomes the output
-  // staging; each compute wave writes its tile's output or partial
+  // staging. Each compute wave stages its half's (max, sum, output); then the
+  // two waves of a tile merge the halves (each half of the tile's items) and
+  // write the tile's output or partial.
   __syncthreads();
   const size_t pbase = ((size_t)b * a.n_kv_heads + kvh) * a.max_chunks;
   const __amdgpu_buffer_rsrc_t pco =
       coherent_region(a.part_o + pbase * Qn * HD, (uint32_t)((size_t)a.max_chunks * Qn * HD * 4));
-  if (wave < ntile) {
-    float* os = reinterpret_cast<float*>(&ring[0][0][0]) + wave * 16 * ORS;
+  float* stage = reinterpret_cast<float*>(&ring[0][0][0]);
+  const int tl = wave >> 1, hk = wave & 1;
+  if (wave < 2 * ntile) {
+    float* os = stage + wave * 16 * ORS;
 #pragma unroll
     for (int ds = 0; ds < DSUB; ++ds)
 #pragma unroll
       for (int r = 0; r < 4; ++r) os[(4 * g + r) * ORS + ds * 16 + r16] = o[ds][r];
-    if (g == 0) ml_sh[wave][r16] = make_float2(mrun, lrun);
-    wave_lds_sync();
-    const int qt = qt0 + wave;
-    for (int x = lane; x < 16 * C4; x += 64) {
+    if (g == 0) ml_sh[tl][hk][r16] = make_float2(mrun, lrun);
+  }
+  __syncthreads();
+  if (wave < 2 * ntile) {
+    const float* o0 = stage + 2 * tl * 16 * ORS;
+    const float* o1 = o0 + 16 * ORS;
+    const int qt = qt0 + tl;
+    for (int x = hk * 8 * C4 + lane; x < (hk + 1) * 8 * C4; x += 64) {
       const int qloc = x / C4, c4 = x - qloc * C4;
       const int qg = qt * 16 + qloc;
       if (qg >= Qn) continue;
-      const float4 v = *reinterpret_cast<const float4*>(os + qloc * ORS + 4 * c4);
-      const float2 ml = ml_sh[wave][qloc];
+      const float2 m0 = ml_sh[tl][0][qloc], m1 = ml_sh[tl][1][qloc];
+      const float M = fmaxf(m0.x, m1.x);
+      const float f0 = m0.x == -INFINITY ? 0.0f : exp2_hw(m0.x - M);
+      const float f1 = m1.x == -INFINITY ? 0.0f : exp2_hw(m1.x - M);
+      const float4 v0 = *reinterpret_cast<const float4*>(o0 + qloc * ORS + 4 * c4);
+      const float4 v1 = *reinterpret_cast<const float4*>(o1 + qloc * ORS + 4 * c4);
+      const float4 v = make_float4(v0.x * f0 + v1.x * f1, v0.y * f0 + v1.y * f1, v0.z * f0 + v1.z * f1,
+                                   v0.w * f0 + v1.w * f1);
+      const float2 ml = make_float2(M, m0.y * f0 + m1.y * f1);
       if (nch == 1) {
         const float inv = ml.y > 0.0f ? 1.0f / ml.y : 0.0f;
         const float out[4] = {v.x * inv, v.y * inv, v.z * inv, v.w * inv};
@@ -1032,10 +1049,10 @@ hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t s) {
     if (head_dim != 128 || a.q_per_wg > 4) return hipErrorInvalidValue;
     const dim3 grid((unsigned)((a.max_chunks + a.nb - 1) / a.nb) * a.n_kv_heads * qg * a.batch);
     switch (a.q_per_wg) {
-      case 1: hipLaunchKernelGGL((attn_ring_kernel<1>), grid, dim3(64 * 3), 0, s, a); break;
-      case 2: hipLaunchKernelGGL((attn_ring_kernel<2>), grid, dim3(64 * 4), 0, s, a); break;
-      case 3: hipLaunchKernelGGL((attn_ring_kernel<3>), grid, dim3(64 * 5), 0, s, a); break;
-      default: hipLaunchKernelGGL((attn_ring_kernel<4>), grid, dim3(64 * 6), 0, s, a); break;
+      case 1: hipLaunchKernelGGL((attn_ring_kernel<1>), grid, dim3(64 * 4), 0, s, a); break;
+      case 2: hipLaunchKernelGGL((attn_ring_kernel<2>), grid, dim3(64 * 6), 0, s, a); break;
+      case 3: hipLaunchKernelGGL((attn_ring_kernel<3>), grid, dim3(64 * 8), 0, s, a); break;
+      default: hipLaunchKernelGGL((attn_ring_kernel<4>), grid, dim3(64 * 10), 0, s, a); break;
     }
     return hipGetLastError();
   }
