@@ -545,8 +545,9 @@ def main():
     logp = torch.empty((M, w.kappa), dtype=torch.float32, device=dev)
     ee_ready = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ee = msd.EERequest(w.ee_layer, w.kappa, ids.data_ptr(), logp.data_ptr(), None)
-    ws = torch.empty(msd.workspace_bytes(model.handle, B, n, w.kappa, capacity), dtype=torch.uint8,
-                     device=dev)
+    # one workspace for the verify pass and then the acceptance's vocabulary statistics
+    ws = torch.empty(max(msd.workspace_bytes(model.handle, B, n, w.kappa, capacity),
+                         M * msd.MSD_ACCEPT_WS_PER_ROW), dtype=torch.uint8, device=dev)
     acc = torch.empty(B, dtype=torch.int32, device=dev)
     nxt = torch.empty(B, dtype=torch.int32, device=dev)
     path = torch.empty((B, n), dtype=torch.int32, device=dev)
@@ -560,7 +561,7 @@ def main():
 
     def step():
         msd.verify_block(model.handle, cache.c, blk, ee, logits, argmax, lse, ws)
-        msd.accept(model.handle, blk, logits, argmax, smp, acc, nxt, path, cache.status)
+        msd.accept(model.handle, blk, logits, argmax, smp, acc, nxt, path, cache.status, ws=ws)
         msd.kv_commit(model.handle, cache.c, blk, acc, path)
 
     for _ in range(args.warmup):

@@ -288,8 +288,16 @@ typedef struct {
  * GREEDY reads argmax only (children tried in slot order); the stochastic
  * modes read logits (fp32 [M][vocab]). sampling may be NULL for GREEDY.
  * status: device word for MSD_DEV_CANDIDATE, may be NULL for GREEDY and MATCH.
- * ws / ws_bytes are unused (NULL / 0 allowed).
+ * ws / ws_bytes: optional device scratch, 16-byte aligned. For REJECTION and
+ * MATCH with ws_bytes >= batch * n_slots * MSD_ACCEPT_WS_PER_ROW, per-row
+ * vocabulary statistics (64 chunks of fp64 max and sum) are computed there by
+ * a kernel spread over the device, and the walk reads the logsumexp and the
+ * inverse-CDF chunk masses from them (scanning only the drawn chunk);
+ * otherwise (NULL, or smaller) one workgroup per sequence makes the
+ * vocabulary passes itself. The decisions are the same either way up to
+ * fp64 summation order (inside the near-tie bands). GREEDY ignores ws.
  */
+#define MSD_ACCEPT_WS_PER_ROW 1024
 msd_status msd_accept(const msd_model* model, const msd_block* block, const float* logits,
                       const int32_t* argmax, const msd_sampling* sampling, int32_t* acc_len,
                       int32_t* next_tok, int32_t* path, uint8_t* near_tie, uint32_t* status,

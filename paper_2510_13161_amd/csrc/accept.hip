@@ -10,6 +10,12 @@
 // sparse draft law q lives on <= 64 candidate ids, so the rejection residual
 // r = normalise((r - q)^+) differs from a multiple f * p only on those ids:
 // the kernel keeps f and the candidate values, never a dense vocab vector.
+// With a workspace (AcceptArgs::stats) the vocabulary passes leave the walk:
+// row_stats_kernel, a workgroup per (row, 1/kStatChunks of the vocabulary)
+// over the whole device, stores each chunk's max of z / T and sum of
+// exp(z / T - max) in fp64; the walk then takes the logsumexp from the
+// chunk statistics, and an inverse-CDF draw picks its chunk from the chunk
+// masses (corrected on the candidate ids) and scans that chunk only.
 //
 // Near-tie flags (optional): a decision that a logit error of tol_logit could
 // flip marks the sequence. Bands: an argmax whose top-1 minus top-2 logit is
@@ -24,6 +30,7 @@ namespace {
 
 constexpr int kMaxCand = 64;
 constexpr int kThreads = 1024;  // 16 waves: the fp64 vocabulary passes are latency-bound
+constexpr int kStatChunks = kAcceptStatChunks;  // vocabulary chunks of the per-row statistics (one wave)
 
 struct Shared {
   double red[kThreads];
@@ -33,6 +40,11 @@ struct Shared {
   int cid[kMaxCand];       // candidate ids sorted ascending
   double rc[kMaxCand];     // residual mass at each sorted candidate
   double qc[kMaxCand];     // draft mass at each sorted candidate
+  double pcand[kMaxCand];  // target probability p at each sorted candidate
+  int tmp_id[kMaxCand];    // the node's candidate ids as given
+  int tok[kMaxSlots];      // the sequence's block tokens
+  float ua[kMaxSlots], us[kMaxSlots];  // its uniforms
+  double wtot[kThreads / 64];  // per-wave totals of a block scan
   int n_c;
   int found;
   int result;
@@ -184,13 +196,190 @@ __device__ int row_sample(const float* z, int V, double invT, double lse, double
   return r;
 }
 
+// Per row and vocabulary chunk c (ids [c ck, (c + 1) ck), ck = ceil(V /
+// kStatChunks)): the chunk's max m of z / T and sum of exp(z / T - m), fp64,
+// in a fixed order (thread-strided partials, then a tree over the threads).
+// An empty chunk stores (-inf, 0).
+__global__ __launch_bounds__(256) void row_stats_kernel(AcceptArgs a) {
+  __shared__ double red[256];
+  const int c = blockIdx.x, row = blockIdx.y, t = threadIdx.x;
+  const int V = a.vocab, ck = (V + kStatChunks - 1) / kStatChunks;
+  const int y0 = min(V, c * ck), y1 = min(V, y0 + ck);
+  const float* z = a.logits + (size_t)row * V;
+  const double invT = 1.0 / (double)a.temperature;
+  double m = -INFINITY;
+  for (int y = y0 + t; y < y1; y += 256) m = fmax(m, (double)z[y] * invT);
+  red[t] = m;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) red[t] = fmax(red[t], red[t + o]);
+    __syncthreads();
+  }
+  m = red[0];
+  __syncthreads();
+  double sum = 0.0;
+  if (m != -INFINITY)
+    for (int y = y0 + t; y < y1; y += 256) sum += exp((double)z[y] * invT - m);
+  red[t] = sum;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) red[t] += red[t + o];
+    __syncthreads();
+  }
+  if (t == 0) a.stats[(size_t)row * kStatChunks + c] = make_double2(m, red[0]);
+}
+
+// log sum_y exp(z_y / T) of a row from its chunk statistics (wave 0, lane c
+// holding chunk c; every thread returns it).
+__device__ double row_lse_stats(const double2* st, Shared& sh) {
+  const int t = threadIdx.x;
+  if (t < 64) {
+    const double2 v = st[t];
+    double M = v.x;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) M = fmax(M, __shfl_xor(M, o));
+    double S = v.x == -INFINITY ? 0.0 : v.y * exp(v.x - M);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o);
+    if (t == 0) sh.red[0] = M + log(S);
+  }
+  __syncthreads();
+  const double r = sh.red[0];
+  __syncthreads();
+  return r;
+}
+
+// Exclusive prefix of v over the workgroup in thread order (wave scans, then
+// the wave totals); every thread also gets the total.
+__device__ double block_scan(double v, double& total, Shared& sh) {
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  double x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh.wtot[wave] = x;
+  __syncthreads();
+  double before = 0.0, all = 0.0;
+  for (int w = 0; w < kThreads / 64; ++w) {
+    if (w < wave) before += sh.wtot[w];
+    all += sh.wtot[w];
+  }
+  __syncthreads();
+  total = all;
+  return before + x - v;
+}
+
+// row_sample with the chunk statistics st of the row: the chunks' masses of
+// w(y) = f p(y) off the candidates and sh.rc on them, the chunk holding the
+// target u * total, then the smallest id of that chunk whose cumulative mass
+// exceeds it (a thread per 1/kThreads of the chunk). sh.c_lo / sh.c_hi get
+// the cumulative fractions at the edges of the drawn id's bin.
+__device__ int row_sample_stats(const float* z, int V, double invT, double lse, double f, double u,
+                                const double2* st, Shared& sh) {
+  const int t = threadIdx.x;
+  const int ck = (V + kStatChunks - 1) / kStatChunks;
+  if (t < 64) {
+    const double2 v = st[t];
+    double off = v.x == -INFINITY ? 0.0 : v.y * exp(v.x - lse);  // sum of p over the chunk
+    double cand = 0.0;
+    const int c0 = t * ck, c1 = c0 + ck;
+    for (int j = 0; j < sh.n_c; ++j)
+      if (sh.cid[j] >= c0 && sh.cid[j] < c1) {
+        off -= sh.pcand[j];
+        cand += sh.rc[j];
+      }
+    double w = f * (off > 0.0 ? off : 0.0) + cand;
+    double x = w;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const double y = __shfl_up(x, o);
+      if (t >= o) x += y;
+    }
+    const double total = __shfl(x, 63);
+    const double target = u * total;
+    const double lo = x - w;
+    // the first chunk whose span holds the target (the last chunk with mass
+    // when rounding leaves the target at the total)
+    const unsigned long long hit = __ballot(w > 0.0 && lo <= target && target < x);
+    const unsigned long long any = __ballot(w > 0.0);
+    const int pick = hit ? __ffsll((long long)hit) - 1 : (any ? 63 - __clzll((long long)any) : 0);
+    const double lo_pick = __shfl(lo, pick);
+    if (t == 0) {
+      sh.result = pick;
+      sh.pre[0] = lo_pick;
+      sh.pre[1] = total;
+      sh.c_lo = target;  // the target, for the scan below
+    }
+  }
+  __syncthreads();
+  const int c = sh.result;
+  const double base = sh.pre[0], total = sh.pre[1], target = sh.c_lo;
+  const int y0 = min(V, c * ck), y1 = min(V, y0 + ck);
+  const int per = (y1 - y0 + kThreads - 1) / kThreads;
+  const int a0 = min(y1, y0 + t * per), a1 = min(y1, a0 + per);
+  auto weight = [&](int y) {
+    for (int j = 0; j < sh.n_c; ++j)
+      if (sh.cid[j] == y) return sh.rc[j];
+    return f * exp((double)z[y] * invT - lse);
+  };
+  double s = 0.0;
+  for (int y = a0; y < a1; ++y) s += weight(y);
+  double tot_c;
+  const double pre = base + block_scan(s, tot_c, sh);
+  __syncthreads();
+  if (t == 0) sh.found = 0;
+  __syncthreads();
+  if (pre <= target && target < pre + s) {
+    double cum = pre;
+    for (int y = a0; y < a1; ++y) {
+      const double w = weight(y);
+      if (w <= 0.0) continue;
+      const double before = cum;
+      cum += w;
+      if (cum > target) {
+        sh.result = y;
+        sh.c_lo = before / total;
+        sh.c_hi = cum / total;
+        sh.found = 1;
+        break;
+      }
+    }
+  }
+  __syncthreads();
+  if (!sh.found && t == 0) {
+    // rounding left the target past the chunk's recomputed mass: its last id
+    // with mass, drawn at a rounding edge (inside every band)
+    int r = -1;  // no mass anywhere: no token, as in row_sample
+    for (int y = y1 - 1; y >= y0; --y)
+      if (weight(y) > 0.0) {
+        r = y;
+        break;
+      }
+    sh.result = r;
+    sh.c_lo = sh.c_hi = u;
+  }
+  __syncthreads();
+  const int r = sh.result;
+  __syncthreads();
+  return r;
+}
+
 __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
   __shared__ Shared sh;
   const int b = blockIdx.x, t = threadIdx.x;
   const int ns = a.n_slots;
   int32_t* path = a.path + (size_t)b * ns;
-  const int32_t* tok = a.tokens + (size_t)b * ns;
-  for (int i = t; i < ns; i += kThreads) path[i] = i == 0 ? 0 : -1;
+  // the sequence's block tokens and uniforms, staged once (the walk reads
+  // them one node at a time)
+  for (int i = t; i < ns; i += kThreads) {
+    path[i] = i == 0 ? 0 : -1;
+    sh.tok[i] = a.tokens[(size_t)b * ns + i];
+    sh.ua[i] = a.u_accept ? a.u_accept[(size_t)b * ns + i] : 0.0f;
+    sh.us[i] = a.u_sample ? a.u_sample[(size_t)b * ns + i] : 0.0f;
+  }
+  const int32_t* tok = sh.tok;
   __syncthreads();
 
   const double tol = (double)a.tol_logit;
@@ -251,13 +440,15 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
   bool tie = false;
   for (;;) {
     const float* z = a.logits + ((size_t)b * ns + cur) * a.vocab;
-    const double lse = row_lse(z, a.vocab, invT, sh);
+    const double2* st = a.stats ? a.stats + ((size_t)b * ns + cur) * kStatChunks : nullptr;
+    const double lse = st ? row_lse_stats(st, sh) : row_lse(z, a.vocab, invT, sh);
     int next_child = -1, out_tok = -1;
     if (a.mode == 2) {  // MATCH: y ~ p, descend to the child carrying y
       if (t == 0) sh.n_c = 0;
       __syncthreads();
-      const double u = (double)a.u_sample[(size_t)b * ns + cur];
-      const int y = row_sample(z, a.vocab, invT, lse, 1.0, u, sh);
+      const double u = (double)sh.us[cur];
+      const int y = st ? row_sample_stats(z, a.vocab, invT, lse, 1.0, u, st, sh)
+                       : row_sample(z, a.vocab, invT, lse, 1.0, u, sh);
       tie |= icdf_near_tie(u, sh.c_lo, sh.c_hi, tol);
       for (int ch = cur + 1; ch < ns; ++ch)
         if (a.topo.parent[ch] == cur && tok[ch] == y) {
@@ -269,13 +460,16 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
       const int C = a.n_cand;
       const int* cid = a.cand_ids + ((size_t)b * ns + cur) * C;
       const float* cq = a.cand_q + ((size_t)b * ns + cur) * C;
+      if (t < C) sh.tmp_id[t] = cid[t];
+      __syncthreads();
       if (t < C) {  // rank-sort the (distinct) candidate ids
-        const int my = cid[t];
+        const int my = sh.tmp_id[t];
         int rank = 0;
-        for (int i = 0; i < C; ++i) rank += cid[i] < my;
+        for (int i = 0; i < C; ++i) rank += sh.tmp_id[i] < my;
         sh.cid[rank] = my;
         sh.qc[rank] = (double)cq[t];
         sh.rc[rank] = exp((double)z[my] * invT - lse);
+        sh.pcand[rank] = sh.rc[rank];
       }
       if (t == 0) sh.n_c = C;
       __syncthreads();
@@ -294,7 +488,7 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
         }
         const double ratio = sh.rc[jx] / sh.qc[jx];
         const double alpha = ratio < 1.0 ? ratio : 1.0;
-        const double u = (double)a.u_accept[(size_t)b * ns + ch];
+        const double u = (double)sh.ua[ch];
         tie |= fabs(u - alpha) < 2.0 * tol * alpha * invT;
         if (u < alpha) {
           next_child = ch;
@@ -302,13 +496,11 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
         }
         // rejected: r <- normalise((r - q)^+), q <- q without x, renormalised
         double pc = 0.0, rnew = 0.0;
-        for (int i = 0; i < C; ++i) pc += exp((double)z[sh.cid[i]] * invT - lse);
+        for (int i = 0; i < C; ++i) pc += sh.pcand[i];
         __syncthreads();
-        if (t == 0) {
-          for (int i = 0; i < C; ++i) {
-            const double d = sh.rc[i] - sh.qc[i];
-            sh.rc[i] = d > 0.0 ? d : 0.0;
-          }
+        if (t < C) {
+          const double d = sh.rc[t] - sh.qc[t];
+          sh.rc[t] = d > 0.0 ? d : 0.0;
         }
         __syncthreads();
         for (int i = 0; i < C; ++i) rnew += sh.rc[i];
@@ -316,15 +508,14 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
         __syncthreads();
         if (zr > 0.0) {
           f /= zr;
-          if (t == 0)
-            for (int i = 0; i < C; ++i) sh.rc[i] /= zr;
+          if (t < C) sh.rc[t] /= zr;
         }
         const double qx = sh.qc[jx];
         __syncthreads();
-        if (t == 0) {
-          sh.qc[jx] = 0.0;
-          if (qx < 1.0)
-            for (int i = 0; i < C; ++i) sh.qc[i] /= (1.0 - qx);
+        if (t < C) {
+          double qv = t == jx ? 0.0 : sh.qc[t];
+          if (qx < 1.0) qv /= (1.0 - qx);
+          sh.qc[t] = qv;
         }
         __syncthreads();
       }
@@ -337,8 +528,9 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptArgs a) {
         return;
       }
       if (next_child < 0) {
-        const double u = (double)a.u_sample[(size_t)b * ns + cur];
-        out_tok = row_sample(z, a.vocab, invT, lse, f, u, sh);
+        const double u = (double)sh.us[cur];
+        out_tok = st ? row_sample_stats(z, a.vocab, invT, lse, f, u, st, sh)
+                     : row_sample(z, a.vocab, invT, lse, f, u, sh);
         tie |= icdf_near_tie(u, sh.c_lo, sh.c_hi, tol);
       }
     }
@@ -397,6 +589,11 @@ __global__ void commit_len_kernel(CommitArgs a) {
 }  // namespace
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
+  if (a.stats) {
+    hipLaunchKernelGGL(row_stats_kernel, dim3(kStatChunks, a.batch * a.n_slots), dim3(256), 0, s, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(accept_kernel, dim3(a.batch), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }

@@ -203,8 +203,11 @@ struct AcceptArgs {
   uint8_t* near_tie;         // [batch] or null
   float tol_logit;           // half-width scale of the near-tie bands
   uint32_t* status;
+  double2* stats;            // [M][kAcceptStatChunks] (max of z / T, sum exp(z / T - max))
+                             // per vocabulary chunk, or null (the walk's own passes)
   Topo topo;
 };
+constexpr int kAcceptStatChunks = 64;
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 
 struct CommitArgs {

@@ -1017,8 +1017,6 @@ msd_status msd_accept(const msd_model* m, const msd_block* blk, const float* log
                       const int32_t* argmax, const msd_sampling* smp, int32_t* acc_len,
                       int32_t* next_tok, int32_t* path, uint8_t* near_tie, uint32_t* status,
                       void* ws, size_t ws_bytes, hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   msd_status st = check_block(m, blk, false);
   if (st != MSD_OK) return st;
   if (!acc_len || !next_tok || !path) return fail(MSD_ERR_INVALID_ARG, "null output");
@@ -1064,6 +1062,11 @@ msd_status msd_accept(const msd_model* m, const msd_block* blk, const float* log
   a.status = status;
   a.topo = topo;
   if (a.mode == MSD_REJECTION && !status) return fail(MSD_ERR_INVALID_ARG, "REJECTION needs a status word");
+  // the stochastic modes' vocabulary statistics in the caller's workspace
+  // when it holds them (16-byte aligned); otherwise the walk's own passes
+  const size_t stat_bytes = (size_t)blk->batch * blk->n_slots * kAcceptStatChunks * sizeof(double2);
+  if (a.mode != MSD_GREEDY && ws && ws_bytes >= stat_bytes && ((uintptr_t)ws & 15) == 0)
+    a.stats = reinterpret_cast<double2*>(ws);
   MSD_HIP(launch_accept(a, stream));
   return MSD_OK;
 }

@@ -34,6 +34,7 @@ EXPORTED = ["msd_last_error", "msd_model_create", "msd_model_destroy", "msd_work
             "msd_verify_block", "msd_early_exit_topk", "msd_accept", "msd_kv_commit",
             "msd_reuse_select", "msd_set_profile", "msd_verify_block_static"]
 MSD_STATIC_SCRATCH_BYTES = 64 << 20
+MSD_ACCEPT_WS_PER_ROW = 1024  # bytes a row of the acceptance workspace (msd.h)
 MSD_K_QKV, MSD_K_ATTN, MSD_K_OPROJ, MSD_K_FFN_UP, MSD_K_FFN_DOWN = 0, 1, 2, 3, 4
 MSD_NEXT_BRANCH, MSD_NEXT_CONTINUE, MSD_NEXT_FRESH = 0, 1, 2
 MSD_MAX_TREE_NODES = 256

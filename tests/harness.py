@@ -107,7 +107,9 @@ class GpuCase:
             req = msd.EERequest(min(w.ee_layer, self.shape.n_layers - 1), w.kappa, ids.data_ptr(),
                                 logp.data_ptr(), None)
         nb = msd.workspace_bytes(self.model.handle, B, n, w.kappa if ee else 1, self.capacity)
-        ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+        # one workspace for both calls (stream-ordered): the verify pass, then
+        # the acceptance's vocabulary statistics
+        ws = torch.empty(max(nb, M * msd.MSD_ACCEPT_WS_PER_ROW), dtype=torch.uint8, device=dev)
         msd.verify_block(self.model.handle, self.cache.c, blk, req, logits, argmax, lse, ws)
         # block rows written by the verify pass
         k_rows, v_rows = self._rows(si.ctx_len, np.full(B, n))
@@ -127,7 +129,7 @@ class GpuCase:
             smp = msd.Sampling(msd.MSD_GREEDY, 1.0, 0, None, None, None, None, TOL_LOGIT)
         tie = torch.empty(B, dtype=torch.uint8, device=dev) if want_logits else None
         msd.accept(self.model.handle, blk, logits, argmax, smp, acc, nxt, path, self.cache.status,
-                   near_tie=tie)
+                   ws=ws, near_tie=tie)
         k_com = v_com = None
         if commit:
             msd.kv_commit(self.model.handle, self.cache.c, blk, acc, path)

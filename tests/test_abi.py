@@ -34,6 +34,14 @@ def test_binding_structs_match_header_sizes():
     assert ctypes.sizeof(msd.Sampling) == 4 + 4 + 4 + 4 + 4 * 8 + 4 + 4
 
 
+def test_accept_workspace_constant():
+    """The acceptance workspace row size of msd.h (64 vocabulary chunks of an
+    fp64 (max, sum) pair) is the binding's."""
+    text = open(os.path.join(ROOT, "include", "msd.h")).read()
+    assert "#define MSD_ACCEPT_WS_PER_ROW 1024" in text
+    assert msd.MSD_ACCEPT_WS_PER_ROW == 64 * 16
+
+
 def test_tensor_slot_layout():
     assert len(msd.GLOBAL_SLOTS) == 5 and len(msd.LAYER_SLOTS) == 17
     text = open(os.path.join(ROOT, "include", "msd.h")).read()

@@ -37,7 +37,7 @@ def _model(vocab: int, n_layers: int = 1, n_kv_heads: int = 1, head_dim: int = 6
     return msd.Model(shape, synth.device_weights(shape, 3), max_positions=256), shape
 
 
-@pytest.fixture(scope="module", params=[4096, 152064], ids=["V4096", "V152064"])
+@pytest.fixture(scope="module", params=[4096, 5008, 152064], ids=["V4096", "V5008", "V152064"])
 def vmodel(request):
     _torch()
     m, shape = _model(request.param)
@@ -61,8 +61,11 @@ def _children(parent):
 
 
 def _run_accept(model, parent, tokens, logits, mode="greedy", temperature=1.0, cand=None, q=None,
-                ua=None, us=None, tol=TOL, chain=False):
-    """GPU acceptance of a batch through the C ABI; returns host arrays."""
+                ua=None, us=None, tol=TOL, chain=False, ws=False):
+    """GPU acceptance of a batch through the C ABI; returns host arrays. ws:
+    pass a workspace of MSD_ACCEPT_WS_PER_ROW bytes a row (the vocabulary
+    statistics kernel and the chunked draws), else none (the walk's own
+    passes)."""
     torch = _torch()
     from paper_2510_13161_amd import msd
     B, n = tokens.shape
@@ -82,7 +85,8 @@ def _run_accept(model, parent, tokens, logits, mode="greedy", temperature=1.0, c
     path = torch.full((B, n), -9, dtype=torch.int32, device="cuda")
     tie = torch.full((B,), 7, dtype=torch.uint8, device="cuda")
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
-    msd.accept(model.handle, blk, lg, am, smp, acc, nxt, path, status, near_tie=tie)
+    wsb = torch.empty(B * n * msd.MSD_ACCEPT_WS_PER_ROW, dtype=torch.uint8, device="cuda") if ws else None
+    msd.accept(model.handle, blk, lg, am, smp, acc, nxt, path, status, ws=wsb, near_tie=tie)
     torch.cuda.synchronize()
     return (acc.cpu().numpy(), nxt.cpu().numpy(), path.cpu().numpy(), tie.cpu().numpy(),
             int(status.item()))
@@ -318,8 +322,9 @@ def _tree_plan(gam, br, A, ystar):
     return [0] + [1 + br * gam + r - 1 for r in range(1, A + 1)], ystar
 
 
+@pytest.mark.parametrize("ws", [False, True], ids=["own", "stats"])
 @pytest.mark.parametrize("mode,temperature", [("rejection", 1.0), ("rejection", 0.7), ("match", 1.0)])
-def test_stochastic_chain_every_accepted_length(vmodel, mode, temperature):
+def test_stochastic_chain_every_accepted_length(vmodel, mode, temperature, ws):
     """Chain of 8 drafts, A = 0..8 planted; REJECTION accepts a child whose
     draft mass is below its target mass (alpha = 1) and descends; MATCH
     descends when the draw lands on the child. A = 8 ends in the leaf bonus."""
@@ -332,11 +337,12 @@ def test_stochastic_chain_every_accepted_length(vmodel, mode, temperature):
     want = _oracle_accept(parent, tok, z, mode, temperature, cand, q, ua, us)
     for b in range(B):
         assert want[b][0] == b and want[b][1] == plan[b][1], (b, want[b][:2])
-    _assert_same(_run_accept(model, parent, tok, z, mode, temperature, cand, q, ua, us, chain=True), want)
+    _assert_same(_run_accept(model, parent, tok, z, mode, temperature, cand, q, ua, us, chain=True, ws=ws), want)
 
 
+@pytest.mark.parametrize("ws", [False, True], ids=["own", "stats"])
 @pytest.mark.parametrize("mode", ["rejection", "match"])
-def test_stochastic_tree_descends_a_later_branch(vmodel, mode):
+def test_stochastic_tree_descends_a_later_branch(vmodel, mode, ws):
     """Tree of 4 x 6: the accepted branch is 1, 2 or 3 (REJECTION rejects the
     siblings tried before it, in slot order, recursively without replacement),
     A up to 6 with the leaf bonus."""
@@ -353,11 +359,12 @@ def test_stochastic_tree_descends_a_later_branch(vmodel, mode):
         assert want[b][0] == A and list(want[b][2]) == plan[b][0], (b, want[b])
         assert want[b][1] == plan[b][1]
     assert sum(w[0] >= 2 for w in want) >= 4
-    _assert_same(_run_accept(model, parent, tok, z, mode, 1.0, cand, q, ua, us), want)
+    _assert_same(_run_accept(model, parent, tok, z, mode, 1.0, cand, q, ua, us, ws=ws), want)
 
 
+@pytest.mark.parametrize("ws", [False, True], ids=["own", "stats"])
 @pytest.mark.parametrize("mode", ["rejection", "match"])
-def test_stochastic_seeded_workload_inputs(vmodel, mode):
+def test_stochastic_seeded_workload_inputs(vmodel, mode, ws):
     """The seeded tree workload's own inputs (Dirichlet(0.1) draft laws over 32
     candidates, children drawn from them, seeded uniforms) with random logits:
     whatever the oracle decides, the GPU decides the same, flags included."""
@@ -370,7 +377,7 @@ def test_stochastic_seeded_workload_inputs(vmodel, mode):
     want = _oracle_accept(si.parent, si.tokens, z, mode, 1.0, si.cand_ids, si.cand_q, si.u_accept,
                           si.u_sample)
     _assert_same(_run_accept(model, si.parent, si.tokens, z, mode, 1.0, si.cand_ids, si.cand_q,
-                             si.u_accept, si.u_sample), want)
+                             si.u_accept, si.u_sample, ws=ws), want)
 
 
 def test_rejection_child_outside_candidates_sets_status(vmodel):
