@@ -367,10 +367,13 @@ msd_status msd_reuse_select(const msd_model* model, const msd_block* block, cons
                             msd_reuse_stats* stats, hipStream_t stream);
 
 /*
- * Instrumentation (benchmarking only): when set, msd_verify_block records
- * begin[i] / end[i] on its stream around the launch of kernel class `kclass`
- * in layer i (i < n; classes: 0 QKV projection, 1 attention, 2 output
- * projection, 3 FFN up projection, 4 FFN down projection). The events are
+ * Instrumentation (benchmarking only): when set, msd_verify_block times the
+ * launch of kernel class `kclass` in layer i (i < n; classes: 0 QKV
+ * projection, 1 attention, 2 output projection, 3 FFN up projection, 4 FFN
+ * down projection) with begin[i] / end[i]: for the projections the events
+ * are attached to the kernel dispatch itself (begin stamped when its first
+ * kernel starts, end when its last one ends: the kernels' own duration);
+ * for attention they are recorded on the stream around its launches. The events are
  * caller-owned HIP events; a NULL pair skips that layer (sampling a few
  * layers keeps the events' own cost low); pass n = 0 to switch it off. Not
  * thread-safe with concurrent verify calls on the same model.

@@ -1074,40 +1074,43 @@ __global__ __launch_bounds__(256) void gemm_epi_kernel(GemmArgs a) {
 }
 
 template <int MT, int NW, int EPI>
-hipError_t launch_rows(const GemmArgs& a, hipStream_t s) {
+hipError_t launch_rows(const GemmArgs& a, hipStream_t s, LaunchEvents ev) {
   const int wgs = (a.n_tiles + NW - 1) / NW;
-  hipLaunchKernelGGL((gemm_rows_kernel<MT, NW, EPI>), dim3(wgs * a.splits), dim3(64 * (NW + 1)), 0, s, a);
-  if (a.splits > 1) {
+  const bool two = a.splits > 1;
+  hipExtLaunchKernelGGL((gemm_rows_kernel<MT, NW, EPI>), dim3(wgs * a.splits), dim3(64 * (NW + 1)), 0, s,
+                        ev.start, two ? nullptr : ev.stop, 0, a);
+  if (two) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm_epi_kernel<MT, EPI>), dim3((a.n_tiles * MT + 3) / 4), dim3(256), 0, s, a);
+    hipExtLaunchKernelGGL((gemm_epi_kernel<MT, EPI>), dim3((a.n_tiles * MT + 3) / 4), dim3(256), 0, s, nullptr,
+                          ev.stop, 0, a);
   }
   return hipGetLastError();
 }
 
 template <int MT, int NW, int EPI, int JT>
-hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_kernel<MT, NW, EPI, JT>), dim3(a.n_tiles * a.splits),
-                     dim3(64 * block_waves<MT, NW, EPI>()), 0, s, a);
+hipError_t launch_cfg(const GemmArgs& a, hipStream_t s, LaunchEvents ev) {
+  hipExtLaunchKernelGGL((gemm_kernel<MT, NW, EPI, JT>), dim3(a.n_tiles * a.splits),
+                        dim3(64 * block_waves<MT, NW, EPI>()), 0, s, ev.start, ev.stop, 0, a);
   return hipGetLastError();
 }
 
 template <int EPI>
-hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
+hipError_t launch_epi(const GemmArgs& a, hipStream_t s, LaunchEvents ev) {
   if (a.jt == 8) {  // 128-column tiles: the SwiGLU FFN up projection (up to 3
                     // row tiles, 2 waves) and the LM head (one row tile, 4 waves)
     if constexpr (EPI == EPI_SWIGLU) {
       if (a.waves != 2) return hipErrorInvalidValue;
       switch (a.MT) {
-        case 1: return launch_cfg<1, 2, EPI, 8>(a, s);
-        case 2: return launch_cfg<2, 2, EPI, 8>(a, s);
-        case 3: return launch_cfg<3, 2, EPI, 8>(a, s);
+        case 1: return launch_cfg<1, 2, EPI, 8>(a, s, ev);
+        case 2: return launch_cfg<2, 2, EPI, 8>(a, s, ev);
+        case 3: return launch_cfg<3, 2, EPI, 8>(a, s, ev);
         default: return hipErrorInvalidValue;
       }
     }
     if constexpr (EPI == EPI_HEAD) {
       if (a.waves != 4 || a.MT != 1) return hipErrorInvalidValue;
-      return launch_cfg<1, 4, EPI, 8>(a, s);
+      return launch_cfg<1, 4, EPI, 8>(a, s, ev);
     }
     return hipErrorInvalidValue;
   }
@@ -1115,19 +1118,19 @@ hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
   if (a.wg_tiles > 1) {  // tiles per workgroup, the activation shared through LDS
     if (a.wg_tiles != 4) return hipErrorInvalidValue;
     switch (a.MT) {
-      case 2: return launch_rows<2, 4, EPI>(a, s);
-      case 3: return launch_rows<3, 4, EPI>(a, s);
-      case 5: return launch_rows<5, 4, EPI>(a, s);
-      case 9: return launch_rows<9, 4, EPI>(a, s);
+      case 2: return launch_rows<2, 4, EPI>(a, s, ev);
+      case 3: return launch_rows<3, 4, EPI>(a, s, ev);
+      case 5: return launch_rows<5, 4, EPI>(a, s, ev);
+      case 9: return launch_rows<9, 4, EPI>(a, s, ev);
       default: return hipErrorInvalidValue;
     }
   }
   switch (a.MT) {
-    case 1: return a.waves == 8 ? launch_cfg<1, 8, EPI, 4>(a, s) : launch_cfg<1, 4, EPI, 4>(a, s);
-    case 2: return launch_cfg<2, 4, EPI, 4>(a, s);
-    case 3: return launch_cfg<3, 4, EPI, 4>(a, s);
-    case 5: return launch_cfg<5, 4, EPI, 4>(a, s);
-    case 9: return launch_cfg<9, 4, EPI, 4>(a, s);
+    case 1: return a.waves == 8 ? launch_cfg<1, 8, EPI, 4>(a, s, ev) : launch_cfg<1, 4, EPI, 4>(a, s, ev);
+    case 2: return launch_cfg<2, 4, EPI, 4>(a, s, ev);
+    case 3: return launch_cfg<3, 4, EPI, 4>(a, s, ev);
+    case 5: return launch_cfg<5, 4, EPI, 4>(a, s, ev);
+    case 9: return launch_cfg<9, 4, EPI, 4>(a, s, ev);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1177,15 +1180,15 @@ __global__ __launch_bounds__(256) void colsum_kernel(const uint16_t* w, int64_t 
 
 }  // namespace
 
-hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s, LaunchEvents ev) {
   if (a.n_tiles < 1 || a.splits < 1 || a.K % 32 || a.M < 1 || a.M > 16 * a.MT) return hipErrorInvalidValue;
   if (a.splits > 1 && (!a.partial || !a.counters)) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_QKV: return launch_epi<EPI_QKV>(a, s);
-    case EPI_RESID: return launch_epi<EPI_RESID>(a, s);
-    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, s);
-    case EPI_RELU: return launch_epi<EPI_RELU>(a, s);
-    case EPI_HEAD: return launch_epi<EPI_HEAD>(a, s);
+    case EPI_QKV: return launch_epi<EPI_QKV>(a, s, ev);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, s, ev);
+    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, s, ev);
+    case EPI_RELU: return launch_epi<EPI_RELU>(a, s, ev);
+    case EPI_HEAD: return launch_epi<EPI_HEAD>(a, s, ev);
     default: return hipErrorInvalidValue;
   }
 }

@@ -1,6 +1,7 @@
 // Launch interfaces of the verification kernels (host side).
 #pragma once
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 #include "common.h"
@@ -98,7 +99,13 @@ struct GemmArgs {
   int32_t kappa;
 };
 
-hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
+// HIP events attached to a launch (hipExtLaunchKernel): start is stamped when
+// the first kernel of the launch begins, stop when its last one ends, so they
+// time the kernels themselves, not the queue around them. Null: none.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s, LaunchEvents ev = {});
 // row-major [rows][K] -> k-step-major weight fragments (src and dst distinct)
 hipError_t launch_repack(const uint16_t* src, uint16_t* dst, int64_t rows, int32_t K,
                          hipStream_t s);

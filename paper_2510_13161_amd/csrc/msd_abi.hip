@@ -463,6 +463,16 @@ msd_status run_head(const msd_model* m, const Shapes& s, const Layout& L, char* 
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// The profiled class's events of a layer, to attach to a GEMM launch.
+LaunchEvents prof_events(const msd_model* m, int kclass, int layer) {
+  LaunchEvents ev;
+  if (m->prof_class == kclass && layer < (int)m->prof_begin.size()) {
+    ev.start = m->prof_begin[layer];
+    ev.stop = m->prof_end[layer];
+  }
+  return ev;
+}
+
 hipError_t prof_mark(const msd_model* m, int kclass, int layer, bool begin, hipStream_t s) {
   if (m->prof_class != kclass || layer >= (int)m->prof_begin.size()) return hipSuccess;
   hipEvent_t ev = begin ? m->prof_begin[layer] : m->prof_end[layer];
@@ -892,9 +902,7 @@ msd_status verify_launch(const msd_model* m, msd_kv_cache* kv, const msd_block* 
     g.rope = m->rope;
     g.rope_rows = c.max_positions;
     for (int i = 0; i < kMaxSlots; ++i) g.depth[i] = topo.depth[i];
-    MSD_HIP(prof_mark(m, MSD_K_QKV, l, true, stream));
-    MSD_HIP(launch_gemm(EPI_QKV, g, stream));
-    MSD_HIP(prof_mark(m, MSD_K_QKV, l, false, stream));
+    MSD_HIP(launch_gemm(EPI_QKV, g, stream, prof_events(m, MSD_K_QKV, l)));
 
     AttnArgs aa{};
     aa.q_img = q_img;
@@ -933,27 +941,23 @@ msd_status verify_launch(const msd_model* m, msd_kv_cache* kv, const msd_block* 
     g.x = x;
     g.stats_out = stats;
     g.img_out[0] = ImageOut{img_h, LT(m, l, MSD_L_MLP_G)};
-    MSD_HIP(prof_mark(m, MSD_K_OPROJ, l, true, stream));
-    MSD_HIP(launch_gemm(EPI_RESID, g, stream));
-    MSD_HIP(prof_mark(m, MSD_K_OPROJ, l, false, stream));
+    MSD_HIP(launch_gemm(EPI_RESID, g, stream, prof_events(m, MSD_K_OPROJ, l)));
 
     g = gemm_base(m, L, w, M, s.up, c.act == MSD_ACT_SWIGLU ? 2 * c.d_ffn : c.d_ffn);
     g.a_img = img_h;
     g.norm = prenorm(m, stats, m->up_c[l], m->up_e[l]);
     g.act_img = img_act;
-    MSD_HIP(prof_mark(m, MSD_K_FFN_UP, l, true, stream));
     if (c.act == MSD_ACT_SWIGLU) {
       g.map = MAP_GATEUP;
       g.w0 = LT(m, l, MSD_L_W_GATE);
       g.w1 = LT(m, l, MSD_L_W_UP);
-      MSD_HIP(launch_gemm(EPI_SWIGLU, g, stream));
+      MSD_HIP(launch_gemm(EPI_SWIGLU, g, stream, prof_events(m, MSD_K_FFN_UP, l)));
     } else {
       g.map = MAP_PLAIN;
       g.w0 = LT(m, l, MSD_L_W_UP);
       g.b0 = LT(m, l, MSD_L_B_UP);
-      MSD_HIP(launch_gemm(EPI_RELU, g, stream));
+      MSD_HIP(launch_gemm(EPI_RELU, g, stream, prof_events(m, MSD_K_FFN_UP, l)));
     }
-    MSD_HIP(prof_mark(m, MSD_K_FFN_UP, l, false, stream));
 
     const bool ee_here = ee && l + 1 == ee->layer;
     g = gemm_base(m, L, w, M, s.down, d);
@@ -965,9 +969,7 @@ msd_status verify_launch(const msd_model* m, msd_kv_cache* kv, const msd_block* 
     g.stats_out = stats;
     if (l + 1 < c.n_layers) g.img_out[0] = ImageOut{img_x, LT(m, l + 1, MSD_L_ATTN_G)};
     if (ee_here || l + 1 == c.n_layers) g.img_out[1] = ImageOut{img_f, T(m, MSD_T_FINAL_G)};
-    MSD_HIP(prof_mark(m, MSD_K_FFN_DOWN, l, true, stream));
-    MSD_HIP(launch_gemm(EPI_RESID, g, stream));
-    MSD_HIP(prof_mark(m, MSD_K_FFN_DOWN, l, false, stream));
+    MSD_HIP(launch_gemm(EPI_RESID, g, stream, prof_events(m, MSD_K_FFN_DOWN, l)));
 
     if (ee_here) {
       st = run_head(m, s, L, w, M, stats, ee->kappa, nullptr, ee->ids, ee->logp, nullptr, nullptr,
