@@ -772,6 +772,25 @@ def test_attention_ring_ragged_batch(monkeypatch, heads, defer):
     print("ring ragged", heads, defer, _compare(case, gr, seqs))
 
 
+def test_attention_ring_max_tree(monkeypatch):
+    """Ring-fed kernel (forced to chunks of 2 spans) on the 64-slot tree at
+    head dim 128 with 4 query heads per kv head: 256 queries, 16 query tiles
+    in 4 groups of 4 (all 8 compute waves hold a tile), after a 700-key
+    context; the tree rows straddle two 64-key blocks of the last chunk, so
+    the masked path runs in both halves of each."""
+    _torch()
+    monkeypatch.setenv("MSD_ATTN_SPANS", "2")
+    shape = synth.ModelShape("h128x8t", 2, 512, 8, 2, 128, 1024, 4096, rope_theta=1.0e4)
+    w = synth.WORKLOADS["tiny_chain"].with_model(shape, ctx=(700, 700), topology="tree", gamma=9,
+                                                 branches=7, ee_layer=1, kappa=4, seed=29)
+    assert w.n_slots == 64
+    case = H.GpuCase(w)
+    case.reset_len()
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    print("ring max tree:", _compare(case, gr, {0: o}))
+
+
 def test_streaming_attention_is_deterministic(monkeypatch):
     """Two steps over the same inputs through the streaming attention kernel
     (forced, 3 spans a chunk, ragged contexts: direct writes and two-chunk
