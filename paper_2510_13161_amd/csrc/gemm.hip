@@ -969,16 +969,33 @@ __global__ __launch_bounds__(64 * (NW + 1), rows_waves_per_simd<MT>()) void gemm
 #pragma unroll
     for (int j = 0; j < JT; ++j) x[j] = load_nt(wp[j] + (size_t)k * kstr);
   };
+  // Row tile by row tile: the hi products of the JT sub-tiles, then their lo
+  // products (4 MFMAs apart from the hi one they accumulate onto), while the
+  // next row tile's two fragments are read from LDS. The order is pinned:
+  // left to itself the scheduler ran every hi product first, which keeps
+  // all MT lo fragments live, and with the 144 accumulator registers of 9
+  // row tiles it then read each hi fragment into one register and waited
+  // for it, an LDS round trip per row tile.
   auto compute = [&](const bf16x8(&x)[JT], int slot) {
+    bf16x8 ah[2], al[2];
+    ah[0] = __builtin_bit_cast(bf16x8, act_sh[slot][0][lane]);
+    al[0] = __builtin_bit_cast(bf16x8, act_sh[slot][1][lane]);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const bf16x8 ah = __builtin_bit_cast(bf16x8, act_sh[slot][2 * mt][lane]);
-      const bf16x8 al = __builtin_bit_cast(bf16x8, act_sh[slot][2 * mt + 1][lane]);
-#pragma unroll
-      for (int j = 0; j < JT; ++j) {
-        acc[mt][j] = mfma16x16x32(x[j], ah, acc[mt][j]);
-        acc[mt][j] = mfma16x16x32(x[j], al, acc[mt][j]);
+      if (mt + 1 < MT) {
+        ah[(mt + 1) & 1] = __builtin_bit_cast(bf16x8, act_sh[slot][2 * mt + 2][lane]);
+        al[(mt + 1) & 1] = __builtin_bit_cast(bf16x8, act_sh[slot][2 * mt + 3][lane]);
       }
+#pragma unroll
+      for (int j = 0; j < JT; ++j) acc[mt][j] = mfma16x16x32(x[j], ah[mt & 1], acc[mt][j]);
+#pragma unroll
+      for (int j = 0; j < JT; ++j) acc[mt][j] = mfma16x16x32(x[j], al[mt & 1], acc[mt][j]);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // row tile 0's fragments
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      if (mt + 1 < MT) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // the next row tile's
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * JT, 0);              // this row tile's MFMAs
     }
   };
   // D k-steps of weights in flight; as in gemm_kernel the steady-state loop
