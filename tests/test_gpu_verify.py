@@ -791,6 +791,29 @@ def test_attention_ring_max_tree(monkeypatch):
     print("ring max tree:", _compare(case, gr, {0: o}))
 
 
+@pytest.mark.parametrize("which,spans", [("tiny", None), ("tiny", 1), ("h128", None)])
+def test_attention_at_maximum_capacity(monkeypatch, which, spans):
+    """A chain block that fills the cache to its maximum capacity (32768
+    positions: 32759 cached keys + 9 slots, 128 chunks of 256 keys per kv
+    head): head dim 64 under the kernel chosen by size, the one-span kernel
+    forced (128 chunks merged by the merge kernel), and head dim 128 (the
+    ring-fed kernel)."""
+    _torch()
+    if spans is not None:
+        monkeypatch.setenv("MSD_ATTN_SPANS", str(spans))
+    shape = synth.TINY if which == "tiny" else synth.ModelShape("h128x8t", 2, 512, 8, 2, 128, 1024, 4096,
+                                                              rope_theta=1.0e4)
+    L = 32768 - 9
+    w = synth.WORKLOADS["tiny_chain"].with_model(shape, ctx=(L, L), gamma=8, ee_layer=1, kappa=4, seed=37)
+    assert w.n_slots == 9
+    case = H.GpuCase(w, capacity=32768)
+    case.reset_len()
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    print("maximum capacity", which, spans, _compare(case, gr, {0: o}))
+    assert int(case.cache.len[0]) <= 32768
+
+
 def test_streaming_attention_is_deterministic(monkeypatch):
     """Two steps over the same inputs through the streaming attention kernel
     (forced, 3 spans a chunk, ragged contexts: direct writes and two-chunk
