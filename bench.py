@@ -509,8 +509,8 @@ def cu_masked_streams(torch, ranges):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported "
-              "(the multi-GPU sharding is a design note, not built)", file=sys.stderr)
+        print(f"bench.py: the library runs the verify step on exactly one GPU; --gpus {args.gpus} is not "
+              "supported (sharding over several GPUs is described, not implemented)", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
