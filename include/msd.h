@@ -146,7 +146,9 @@ typedef struct msd_model msd_model;
  * (split-K sized for about this many workgroups per GEMM; unset, for the
  * best balance over the device's compute units), MSD_GEMM_WAVES (4 or 8) and
  * MSD_ATTN_SPANS (256-key spans per attention workgroup: 1 forces the
- * one-span kernel, 2 or more the streaming one; unset, chosen per call),
+ * one-span kernel, 2 or more the ring-fed one at head dim 128, else the
+ * streaming one; unset, chosen per call), MSD_ATTN_RING (0: the streaming
+ * kernel also at head dim 128; 1 unset),
  * MSD_ATTN_DEFER (the attention's chunk merge in a kernel of its own: 1
  * always, 0 never; unset, from 6 chunks on),
  * MSD_ROWS_MIN_MT (row tiles from which GEMMs with 256 or more 64-column
@@ -156,7 +158,8 @@ typedef struct msd_model msd_model;
  * tiles), MSD_ROWS_MAX_SPLITS (its splits of K at most, 4 unset) and
  * MSD_ROWS_NARROW (narrower GEMMs of 3 or more row tiles in that kernel
  * with many splits and their split sum and epilogue in a second kernel: 0
- * never, 2 at any size; unset, for matrices of 32M weights or more). */
+ * never, 2 at any size; unset, for matrices of 32M weights or more) and
+ * MSD_ROWS_NARROW_MT (the row tiles from which that applies: 3 unset). */
 msd_status msd_model_create(const msd_model_config* cfg, const void* const* tensors,
                             int32_t n_tensors, msd_model** out);
 void msd_model_destroy(msd_model* model);
