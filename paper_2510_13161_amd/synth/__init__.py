@@ -84,7 +84,7 @@ class Workload:
     model: ModelShape
     batch: int
     ctx: Tuple[int, int]        # (lo, hi) inclusive range of committed context lengths
-    topology: str               # "chain" | "tree"
+    topology: str               # "chain" | "tree" | "forest" (the explicit parents below)
     gamma: int                  # chain length, or tree depth
     branches: int = 1           # tree: number of branches at the root
     ee_layer: int = 1           # early exit after this layer (1-indexed)
@@ -93,9 +93,12 @@ class Workload:
     temperature: float = 1.0
     n_cand: int = 32
     seed: int = 0
+    parents: Optional[Tuple[int, ...]] = None  # "forest": parent[i] < i, parent[0] = -1
 
     @property
     def n_slots(self) -> int:
+        if self.topology == "forest":
+            return len(self.parents)
         if self.topology == "chain":
             return self.gamma + 1
         return 1 + self.branches * self.gamma
@@ -363,6 +366,11 @@ def topology(w: Workload) -> np.ndarray:
     Eq. (branch-complete) seen from the verifier.
     """
     n = w.n_slots
+    if w.topology == "forest":
+        par = np.asarray(w.parents, dtype=np.int32)
+        if par[0] != -1 or any(not 0 <= par[i] < i for i in range(1, n)):
+            raise ValueError("parents must satisfy parent[0] = -1 and 0 <= parent[i] < i")
+        return par
     par = np.empty(n, dtype=np.int32)
     par[0] = -1
     if w.topology == "chain":

@@ -1,6 +1,4 @@
 """Parity of the HIP verification step (through the C ABI) against the oracle."""
-import dataclasses
-
 import numpy as np
 import pytest
 
@@ -497,35 +495,39 @@ def test_tiny_degenerate_blocks(name, ctx, topo, gamma, branches):
     print(name, rep)
 
 
-@pytest.mark.parametrize("seed", range(6))
-def test_tiny_random_tree_blocks(seed):
+@pytest.mark.parametrize("mode,seed", [("greedy", k) for k in range(6)] + [("rejection", k) for k in range(4)]
+                         + [("match", k) for k in range(2)])
+def test_tiny_random_tree_blocks(mode, seed):
     """Random trees (each slot's parent drawn among the earlier slots, 2 to 64
     slots, so depths and ancestor sets of every shape a forest in slot order
     allows) over random contexts and batch sizes: the attention's ancestor
     masks, the rotary positions and cache rows at each node's depth, and the
-    greedy walk over a general tree, element by element against the oracle."""
+    acceptance walk over a general tree (greedy, and the stochastic rules
+    with each child's token drawn from its parent's candidates), element by
+    element against the oracle."""
     _torch()
-    g = np.random.default_rng(1000 + seed)
+    g = np.random.default_rng(1000 + seed + (0 if mode == "greedy" else 100 * len(mode)))
     n = int(g.integers(2, 65))
     B = int(g.integers(1, min(4, 144 // n) + 1))
     lo = int(g.integers(0, 600))
     hi = lo + int(g.integers(0, 500))
-    w = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, batch=B, ctx=(lo, hi), topology="tree", gamma=n - 1,
-                                                 branches=1, ee_layer=1, kappa=4, seed=70 + seed)
-    assert w.n_slots == n and w.mode == "greedy"
-    parent = np.array([-1] + [int(g.integers(0, i)) for i in range(1, n)], dtype=np.int32)
-    si = dataclasses.replace(synth.step_inputs(w), parent=parent)
-    case = H.GpuCase(w, inputs=si)
+    parent = tuple([-1] + [int(g.integers(0, i)) for i in range(1, n)])
+    w = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, batch=B, ctx=(lo, hi), topology="forest", gamma=0,
+                                                 parents=parent, ee_layer=1, kappa=4, mode=mode,
+                                                 temperature=1.0, seed=70 + seed)
+    assert w.n_slots == n
+    case = H.GpuCase(w)
     case.reset_len()
     gr = case.run()
     weights = synth.host_weights(case.shape, w.seed)
     seqs = {b: H.oracle_sequence(case.shape, w, case.si, b, weights=weights) for b in range(B)}
+    par = np.asarray(parent)
     depth = np.zeros(n, dtype=np.int32)
     for i in range(1, n):
-        depth[i] = depth[parent[i]] + 1
-    leaves = n - len(set(parent[1:].tolist()))
-    print("random tree", seed, "slots", n, "batch", B, "ctx", case.si.ctx_len.tolist(), "max depth",
-          int(depth.max()), "leaves", leaves, _compare(case, gr, seqs))
+        depth[i] = depth[par[i]] + 1
+    leaves = n - len(set(par[1:].tolist()))
+    print("random tree", mode, seed, "slots", n, "batch", B, "ctx", case.si.ctx_len.tolist(), "max depth",
+          int(depth.max()), "leaves", leaves, "accepted", gr.acc_len.tolist(), _compare(case, gr, seqs))
 
 
 def test_tiny_ragged_batch():
