@@ -1,5 +1,6 @@
 """The shared seeded input generator: determinism and its own two implementations."""
 import numpy as np
+import pytest
 
 from paper_2510_13161_amd import synth
 
@@ -66,3 +67,22 @@ def test_workload_shapes():
     # 14B-shaped weights: ~29.5 GB of bf16 with an untied head
     gb = synth.QWEN14B.weight_bytes() / 1e9
     assert 29.0 < gb < 30.0
+
+
+def test_forest_topology_inputs():
+    """An explicit parent array ("forest") is returned as given, bad ones are
+    refused, and stochastic inputs follow it: each child's token lies in its
+    parent's candidate set."""
+    parents = (-1, 0, 0, 1, 3, 2, 0, 4)
+    w = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, topology="forest", parents=parents, gamma=0,
+                                                 mode="rejection", batch=2)
+    assert w.n_slots == 8 and w.rows == 16
+    assert synth.topology(w).tolist() == list(parents)
+    si = synth.step_inputs(w)
+    for b in range(2):
+        for c in range(1, 8):
+            assert si.tokens[b, c] in set(si.cand_ids[b, parents[c]].tolist())
+    for bad in [(0, 0), (-1, 1), (-1, 0, 2), (-1, -1)]:
+        wb = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY, topology="forest", parents=bad, gamma=0)
+        with pytest.raises(ValueError):
+            synth.topology(wb)
