@@ -577,6 +577,27 @@ def test_depth_reduced_14b_chain():
     print("14b L2 chain:", rep)
 
 
+@pytest.mark.parametrize("mode,seed,batch", [("greedy", 0, 1), ("rejection", 1, 1), ("greedy", 2, 3)])
+def test_depth_reduced_14b_random_tree(mode, seed, batch):
+    """Random trees at 14B widths with 2 layers: 20 to 64 slots whose parents
+    are drawn among the earlier slots, contexts of 600 to 3000 keys (the
+    ring-fed attention with the tree's ancestor masks; the multi-row-tile
+    GEMMs from 3 row tiles on), greedy and REJECTION acceptance."""
+    _torch()
+    g = np.random.default_rng(2000 + seed)
+    n = int(g.integers(20, 65))
+    n = min(n, 144 // batch)
+    parent = tuple([-1] + [int(g.integers(0, i)) for i in range(1, n)])
+    w = synth.WORKLOADS["14b_tree"].with_model(synth.QWEN14B, batch=batch, ctx=(600, 3000), topology="forest",
+                                               gamma=0, parents=parent, mode=mode, seed=80 + seed)
+    case = H.GpuCase(w, n_layers=2)
+    case.reset_len()
+    gr = case.run()
+    seqs = {b: H.oracle_sequence(case.shape, w, case.si, b) for b in range(batch)}
+    print("14b L2 random tree", mode, seed, "slots", n, "batch", batch, "ctx", case.si.ctx_len.tolist(),
+          _compare(case, gr, seqs))
+
+
 @pytest.mark.parametrize("gamma", [0, 8])
 def test_draft_shape(gamma):
     """The 0.6B-shaped draft decoder that the latency-law measurement runs (d
