@@ -103,11 +103,11 @@ def measured_traffic():
     return int(m.group(2))
 
 
-def cpu_baseline(shape, w, reps: int = 3) -> dict:
+def cpu_baseline(shape, w, reps: int = 4) -> dict:
     """The fp64 oracle on the host over one whole verification step of
     sequence 0: embed, every decoder layer, the early-exit and final heads,
     top-kappa and acceptance, each oracle call run `reps` times on the same
-    input (a bounded sample of about ten seconds). Layer weights are generated
+    input (a bounded sample of about ten to fifteen seconds). Layer weights are generated
     just before their layer runs and dropped after it (only the oracle calls
     are timed)."""
     import numpy as np
