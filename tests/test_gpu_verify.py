@@ -367,13 +367,15 @@ def test_tiny_wide_early_exit_message(kappa):
 
 
 @pytest.mark.parametrize("which,M,kappa", [("tiny", 9, 8), ("tiny", 144, 4), ("14b", 9, 8),
-                                             ("14b", 144, 4)])
+                                             ("14b", 144, 4), ("14b", 9, 32), ("14b", 144, 13),
+                                             ("14b", 9, 1)])
 def test_early_exit_topk_entry_point(which, M, kappa):
     """msd_early_exit_topk on its own (the Sec. 3.1 token channel from a
     residual): seeded fp32 residual rows, final norm, LM head and top-kappa
     with log-probabilities, at one row tile (M = 9) and at the batch-16 block
     size (M = 144, nine row tiles), checked row by row against the oracle's
-    head on the same rows (check_ee_message)."""
+    head on the same rows (check_ee_message); every merge width (kappa 1, up
+    to 8, up to 32) over the 14B vocabulary's 5 or 10 merge parts."""
     torch = _torch()
     import oracle as orc
     from paper_2510_13161_amd import msd
