@@ -144,7 +144,9 @@ typedef struct msd_model msd_model;
  * Launch-shape overrides, read from the environment here (tuning and tests;
  * results differ only by floating-point summation order): MSD_GEMM_TARGET_WGS
  * (split-K sized for about this many workgroups per GEMM; unset, for the
- * best balance over the device's compute units), MSD_GEMM_WAVES (4 or 8) and
+ * best balance over the device's compute units), MSD_GEMM_WAVES (4 or 8),
+ * MSD_QKV_JT (the QKV projection's tile width at one row tile in 16-column
+ * sub-tiles: 2 unset, whole K; 4: 64-column tiles with splits of K) and
  * MSD_ATTN_SPANS (256-key spans per attention workgroup: 1 forces the
  * one-span kernel, 2 or more the ring-fed one at head dim 128, else the
  * streaming one; unset, chosen per call), MSD_ATTN_RING (0: the streaming

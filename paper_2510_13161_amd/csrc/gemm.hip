@@ -4,8 +4,10 @@
 // bytes: every projection of every layer plus the two LM-head passes.
 //
 // Mapping (gfx950, wave64, MFMA 16x16x32 bf16 -> fp32):
-//  * a workgroup of NW waves owns a 64-column output tile and one of
-//    `splits` contiguous slices of K; its waves cut the slice in NW k-ranges;
+//  * a workgroup of NW waves owns a 64-column output tile (128 columns for
+//    the FFN up projection and the LM head, 32 for the QKV projection at
+//    one row tile) and one of `splits` contiguous slices of K; its waves cut
+//    the slice in NW k-ranges;
 //  * weights are stored k-step-major (for each k-step, the 1 KB MFMA operands
 //    of all 16-row groups one after the other), so the workgroups working at
 //    the same k-step read one contiguous window of HBM; each wave keeps D
@@ -40,10 +42,11 @@ template <int JT>
 __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t, int j, int lane) {
   const uint16_t* base;
   int grp;
-  if (a.map == MAP_QKV) {  // JT = 4: a tile is 32 rotary pairs of one head
-    const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
+  if (a.map == MAP_QKV) {  // a tile is 8 JT rotary pairs of one head (JT = 4 or 2)
+    constexpr int HJ = JT / 2;
+    const int hd = a.head_dim, half = hd >> 1, tph = hd / (32 * HJ);
     const int hh = t / tph, gi = t - hh * tph;
-    const int c0 = j < 2 ? gi * 32 + 16 * j : half + gi * 32 + 16 * (j - 2);
+    const int c0 = j < HJ ? gi * 16 * HJ + 16 * j : half + gi * 16 * HJ + 16 * (j - HJ);
     int hl = hh;
     base = a.w0;
     if (hh >= a.n_heads + a.n_kv_heads) {
@@ -70,10 +73,11 @@ __device__ __forceinline__ const uint16_t* weight_frag(const GemmArgs& a, int t,
 // Elements from one k-step of tile t's weights to the next: the group count
 // of its matrix times 512 (the same for every sub-tile of a tile: one
 // matrix, or the gate and up matrices of equal size).
+template <int JT = 4>
 __device__ __forceinline__ uint32_t weight_kstride(const GemmArgs& a, int t) {
   int rows;
   if (a.map == MAP_QKV) {
-    const int hh = t / (a.head_dim >> 6);
+    const int hh = t / (a.head_dim / (16 * JT));
     rows = (hh < a.n_heads ? a.n_heads : a.n_kv_heads) * a.head_dim;
   } else if (a.map == MAP_GATEUP) {
     rows = a.N >> 1;
@@ -88,9 +92,10 @@ __device__ __forceinline__ uint32_t weight_kstride(const GemmArgs& a, int t) {
 template <int JT>
 __device__ __forceinline__ int out_col(const GemmArgs& a, int t, int j, int q, int r) {
   if (a.map == MAP_QKV) {
-    const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
+    constexpr int HJ = JT / 2;
+    const int hd = a.head_dim, half = hd >> 1, tph = hd / (32 * HJ);
     const int hh = t / tph, gi = t - hh * tph;
-    const int dim = (j < 2 ? 0 : half) + gi * 32 + 16 * (j & 1) + 4 * q + r;
+    const int dim = (j < HJ ? 0 : half) + gi * 16 * HJ + 16 * (j % HJ) + 4 * q + r;
     return hh * hd + dim;
   }
   if (a.map == MAP_GATEUP) {
@@ -161,7 +166,7 @@ __device__ __forceinline__ void stats_load(const GemmArgs& a, int mt, EpiIn& in)
   }
 }
 
-template <int EPI, bool NORM = true>
+template <int EPI, bool NORM = true, int JT = 4>
 __device__ __forceinline__ void epi_load(const GemmArgs& a, int t, int mt, EpiIn& in) {
   const int lane = threadIdx.x & 63, q = lane >> 4, r16 = lane & 15;
   const int m = 16 * mt + r16;
@@ -183,7 +188,8 @@ __device__ __forceinline__ void epi_load(const GemmArgs& a, int t, int mt, EpiIn
                             : kUnitGain;
   }
   if constexpr (EPI == EPI_QKV) {
-    const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
+    constexpr int HJ = JT / 2;  // rotary pairs of a tile: 16 HJ
+    const int hd = a.head_dim, half = hd >> 1, tph = hd / (32 * HJ);
     const int H = a.n_heads, Hk = a.n_kv_heads;
     const int hh = t / tph, gi = t - hh * tph;
     const int which = hh < H ? 0 : (hh < H + Hk ? 1 : 2);
@@ -193,8 +199,8 @@ __device__ __forceinline__ void epi_load(const GemmArgs& a, int t, int mt, EpiIn
     int pos = in.L + a.depth[slot];
     pos = pos < 0 ? 0 : (pos < a.rope_rows ? pos : a.rope_rows - 1);  // out-of-range rows are flagged, not used
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int dlo = gi * 32 + 16 * j + 4 * q, dhi = half + dlo;
+    for (int j = 0; j < HJ; ++j) {
+      const int dlo = gi * 16 * HJ + 16 * j + 4 * q, dhi = half + dlo;
       if (which < 2 && a.rope) {
         const float2* cs = a.rope + (size_t)pos * half + dlo;
 #pragma unroll
@@ -382,10 +388,12 @@ __device__ void epi_relu(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[
   wave_lds_sync();
 }
 
-__device__ void epi_qkv(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4], float mu,
+template <int JT>
+__device__ void epi_qkv(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[JT], float mu,
                         float rs, const EpiIn& in) {
+  constexpr int HJ = JT / 2;  // sub-tile j holds dims d of rotary pairs (d, d + half) with sub-tile j + HJ
   const int lane = threadIdx.x & 63, r16 = lane & 15, q = lane >> 4;
-  const int hd = a.head_dim, half = hd >> 1, tph = hd >> 6;
+  const int hd = a.head_dim, half = hd >> 1, tph = hd / (32 * HJ);
   const int H = a.n_heads, Hk = a.n_kv_heads;
   const int hh = t / tph, gi = t - hh * tph;
   const int which = hh < H ? 0 : (hh < H + Hk ? 1 : 2);
@@ -399,8 +407,8 @@ __device__ void epi_qkv(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4
     return;
   }
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int dlo = gi * 32 + 16 * j + 4 * q, dhi = half + dlo;
+  for (int j = 0; j < HJ; ++j) {
+    const int dlo = gi * 16 * HJ + 16 * j + 4 * q, dhi = half + dlo;
     const float blo[4] = {bf_lo(in.qb[j][0][0]), bf_hi(in.qb[j][0][0]), bf_lo(in.qb[j][0][1]),
                           bf_hi(in.qb[j][0][1])};
     const float bhi[4] = {bf_lo(in.qb[j][1][0]), bf_hi(in.qb[j][1][0]), bf_lo(in.qb[j][1][1]),
@@ -409,7 +417,7 @@ __device__ void epi_qkv(const GemmArgs& a, int t, int mt, const floatx4 (&acc)[4
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       lo[r] = normed(a, acc[j][r], mu, rs, hh * hd + dlo + r) + blo[r];
-      hi[r] = normed(a, acc[j + 2][r], mu, rs, hh * hd + dhi + r) + bhi[r];
+      hi[r] = normed(a, acc[j + HJ][r], mu, rs, hh * hd + dhi + r) + bhi[r];
     }
     if (which < 2 && a.rope) {
 #pragma unroll
@@ -520,7 +528,7 @@ __device__ __forceinline__ void epilogue_tile(const GemmArgs& a, int t, int mt, 
   EpiIn inl;
   if constexpr (!AHEAD) {
     if constexpr (EPI == EPI_QKV) inl.L = row_len(a, 16 * mt + (threadIdx.x & 15));
-    epi_load<EPI, !NLDS>(a, t, mt, inl);
+    epi_load<EPI, !NLDS, JT>(a, t, mt, inl);
   }
   const EpiIn& in = AHEAD ? in1 : inl;
   float mu = 0.0f, rs = 1.0f;
@@ -535,9 +543,9 @@ __device__ __forceinline__ void epilogue_tile(const GemmArgs& a, int t, int mt, 
   }
   if constexpr (EPI == EPI_SWIGLU) epi_swiglu<JT>(a, t, mt, acc, scr, mu, rs);
   else if constexpr (EPI == EPI_HEAD) epi_head<JT>(a, t, mt, acc, mu, rs);
+  else if constexpr (EPI == EPI_QKV) epi_qkv<JT>(a, t, mt, acc, mu, rs, in);  // 64- or 32-column tiles
   else if constexpr (JT == 4) {  // the other epilogues run on 64-column tiles only
     if constexpr (EPI == EPI_RESID) epi_resid(a, t, mt, acc, scr, in);
-    else if constexpr (EPI == EPI_QKV) epi_qkv(a, t, mt, acc, mu, rs, in);
     else epi_relu(a, t, mt, acc, scr, mu, rs);
   }
 }
@@ -586,7 +594,7 @@ template <int MT, int NW, int EPI, int JT>
 __global__ __launch_bounds__((64 * block_waves<MT, NW, EPI>())) void gemm_kernel(GemmArgs a) {
   // k-steps in flight per wave (measured per shape with the k-step-major
   // layout: the 2-wave 128-column FFN up tiles 5, 8-wave split-K tiles 6)
-  constexpr int D = MT == 1 ? (JT == 8 ? (NW == 2 ? 5 : 4) : (NW == 8 ? 4 : 8)) : (MT <= 3 ? 4 : 2);
+  constexpr int D = MT == 1 ? (JT == 8 ? (NW == 2 ? 5 : 4) : (JT == 2 ? 6 : (NW == 8 ? 4 : 8))) : (MT <= 3 ? 4 : 2);
   constexpr int RCH = MT < 3 ? MT : 3;  // row tiles per LDS reduction round
   constexpr int TF = MT * JT * 256;     // floats of one tile's partial
   __shared__ floatx4 red[NW][RCH * JT][kWave];
@@ -605,7 +613,7 @@ __global__ __launch_bounds__((64 * block_waves<MT, NW, EPI>())) void gemm_kernel
       // the row norm, while the other waves stream; then the reduction's two
       // barriers, which order the LDS write before the epilogue reads it
       EpiIn hin;
-      epi_load<EPI>(a, t, 0, hin);
+      epi_load<EPI, true, JT>(a, t, 0, hin);
       float mu, rs;
       norm_finish(a, hin, mu, rs);
       if (lane < 16) norm_sh[lane] = make_float2(mu, rs);
@@ -623,7 +631,7 @@ __global__ __launch_bounds__((64 * block_waves<MT, NW, EPI>())) void gemm_kernel
   const uint16_t* wp[JT];
 #pragma unroll
   for (int j = 0; j < JT; ++j) wp[j] = weight_frag<JT>(a, t, j, lane);
-  const size_t kstr = __builtin_amdgcn_readfirstlane(weight_kstride(a, t));
+  const size_t kstr = __builtin_amdgcn_readfirstlane(weight_kstride<JT>(a, t));
   const uint16_t* ap = a.a_img + lane * 8;
 
   // one row tile: the epilogue's inputs are loaded ahead (the sequence
@@ -702,7 +710,7 @@ __global__ __launch_bounds__((64 * block_waves<MT, NW, EPI>())) void gemm_kernel
   }
 
   if constexpr (MT == 1) {
-    if (wave == 0) epi_load<EPI, !norm_helper<MT, NW, EPI>()>(a, t, 0, in1);
+    if (wave == 0) epi_load<EPI, !norm_helper<MT, NW, EPI>(), JT>(a, t, 0, in1);
   }
 
   if constexpr (MT == 1) {
@@ -1130,6 +1138,13 @@ hipError_t launch_epi(const GemmArgs& a, hipStream_t s, LaunchEvents ev) {
       return launch_cfg<1, 4, EPI, 8>(a, s, ev);
     }
     return hipErrorInvalidValue;
+  }
+  if constexpr (EPI == EPI_QKV) {
+    // one row tile, 32-column tiles (16 rotary pairs of a head), 8 waves, whole K
+    if (a.jt == 2) {
+      if (a.MT != 1 || a.waves != 8 || a.wg_tiles != 1) return hipErrorInvalidValue;
+      return launch_cfg<1, 8, EPI, 2>(a, s, ev);
+    }
   }
   if (a.jt != 4) return hipErrorInvalidValue;
   if (a.wg_tiles > 1) {  // tiles per workgroup, the activation shared through LDS

@@ -53,9 +53,10 @@ struct GemmArgs {
   const uint16_t* a_img;   // input image [K/32][MT][2][64][8]
   int32_t M, MT, K, N;     // N = logical output columns (padding masked)
   int32_t n_tiles, splits, waves;
-  int32_t jt;              // 16-column sub-tiles per tile: 4 (64 columns), or 8 (128
+  int32_t jt;              // 16-column sub-tiles per tile: 4 (64 columns), 8 (128
                            // columns: EPI_SWIGLU with up to 3 row tiles and 2 waves,
-                           // EPI_HEAD with one row tile and 4 waves)
+                           // EPI_HEAD with one row tile and 4 waves) or 2 (32 columns:
+                           // EPI_QKV with one row tile and 8 waves)
   int32_t wg_tiles;        // 64-column tiles per workgroup: 1, or 4 (2 to 9 row tiles:
                            // one compute wave a tile and a wave that stages the
                            // activation through LDS; then waves = 4, and with

@@ -568,6 +568,34 @@ def test_device_errors_are_flagged():
     assert gr2.status & msd.MSD_DEV_TOKEN
 
 
+# LayerNorm, ReLU, learned positions, biases and a tied head (the 66B
+# shape's features) at tiny widths: 4 MHA heads of 64
+TINY_LN = synth.ModelShape("tiny_ln", 2, 256, 4, 4, 64, 1024, 4096, norm="layer", act="relu", pos="learned",
+                           bias=True, tied_head=True, norm_eps=1.0e-5, max_positions=1024)
+
+
+@pytest.mark.parametrize("which", ["tiny", "14b", "tiny_ln"])
+@pytest.mark.parametrize("jt", [2, 4])
+def test_qkv_tile_widths_at_one_row_tile(monkeypatch, which, jt):
+    """The QKV projection at one row tile in 32-column whole-K tiles (the
+    default where they fit the compute units) and in 64-column tiles with
+    splits of K (MSD_QKV_JT=4): RoPE pairs split across the tile's halves,
+    the KV append and the query image (tiny and 14B widths, 2 layers of the
+    latter), and the q/k/v biases without a rotary table (tiny LayerNorm
+    model with learned positions)."""
+    _torch()
+    monkeypatch.setenv("MSD_QKV_JT", str(jt))
+    if which == "14b":
+        w = synth.WORKLOADS["14b_chain"].with_model(synth.QWEN14B)
+    else:
+        w = synth.WORKLOADS["tiny_chain"].with_model(synth.TINY if which == "tiny" else TINY_LN, seed=43)
+    case = H.GpuCase(w, n_layers=2 if which == "14b" else None)
+    case.reset_len()
+    gr = case.run()
+    o = H.oracle_sequence(case.shape, w, case.si, 0)
+    print("qkv tiles", which, jt, _compare(case, gr, {0: o}))
+
+
 def test_depth_reduced_14b_chain():
     """14B widths (d 5120, GQA 40/8, FFN 13824, vocab 152064) with 2 layers."""
     _torch()
